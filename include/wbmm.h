@@ -1,0 +1,118 @@
+/*
+ * wbmm.h — C ABI of the MI355X (gfx950) WBMM library.
+ *
+ * Windowed Batch Matrix Multiplication (WBMM), from "WBMM: Windowed Batch
+ * Matrix Multiplication for Efficient Large Receptive Field Convolution":
+ * the input X[B,C,H,W] is cut into non-overlapping w x w windows; each window,
+ * flattened row-major to a d = w*w vector, is multiplied by a per-channel
+ * d x d matrix M_c built from a relative-position table T[C,(2w-1)^2]
+ * (Sec. 3.4 and Alg. 1; eq. index_computation; eq. index_select):
+ *
+ *   I[i, j] = (h_i - h_j + w - 1) * (2w - 1) + (w_i - w_j + w - 1)
+ *   M_c[i, j] = T[c, I[i, j]]
+ *   Y_window = X_window * M_c        (row vector times matrix, Theorem 3.2:
+ *                                     i = input position, j = output position)
+ *
+ * M_c is never stored in memory: the kernels build its blocks on the fly from
+ * T in on-chip memory (the tiled scheme the paper names as future work in its
+ * Limitations section).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - All tensor pointers are DEVICE pointers, owned by the caller, dense and
+ *   contiguous.  x, y, dy, dx are NCHW in `dtype`.  table is [C, (2w-1)^2] in
+ *   `dtype`, row-major over (dh, dw) = input - output offsets.
+ * - dtable is always float32 [C, (2w-1)^2] and is OVERWRITTEN (not
+ *   accumulated into), whatever `dtype` is.
+ * - H and W need not be multiples of w: the map is zero-padded at the bottom
+ *   and right up to window multiples and the outputs are cropped back to
+ *   H x W (Sec. 3.4.1, "Handling Arbitrary Input Sizes").
+ * - 16-bit inputs are multiplied on the matrix cores with float32
+ *   accumulation; every output element is rounded once (nearest-even) from
+ *   its float32 sum.  float32 inputs use float32 matrix-core products.
+ * - Work is enqueued on `stream` (a hipStream_t passed as void*, NULL = the
+ *   default stream).  Calls are asynchronous: nothing is synchronised, and the
+ *   caller must keep every buffer alive until the stream has passed the work.
+ * - The library keeps no state and allocates no memory; calls are
+ *   thread-safe.  Every argument is validated on the host before any GPU work
+ *   is enqueued; errors are returned, never printed, never fatal.
+ * - Supported window sizes: 1 <= w <= 16.  w = 7 and w = 14 are the sizes the
+ *   paper uses; the others run the same kernels.
+ * - Pointers must be aligned to their element size.  Outputs must not
+ *   overlap inputs (WBMM_ERR_INVALID_ARG).
+ */
+#ifndef WBMM_H
+#define WBMM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  WBMM_F32 = 0,  /* float32 storage and float32 products          */
+  WBMM_BF16 = 1, /* bfloat16 storage, float32 accumulation        */
+  WBMM_F16 = 2   /* IEEE half storage, float32 accumulation       */
+} wbmm_dtype;
+
+typedef enum {
+  WBMM_OK = 0,
+  WBMM_ERR_INVALID_ARG = 1, /* null pointer, non-positive size, overlap,
+                               misalignment, too-small workspace, overflow */
+  WBMM_ERR_UNSUPPORTED = 2, /* window size or dtype without a kernel       */
+  WBMM_ERR_HIP = 3          /* the HIP runtime refused the launch          */
+} wbmm_status;
+
+/* Forward pass, Alg. 1: y = WBMM(x; table, w).
+ * x, y: [B,C,H,W] in dtype; table: [C,(2w-1)^2] in dtype. */
+wbmm_status wbmm_forward(const void *x, const void *table, void *y,
+                         int64_t B, int64_t C, int64_t H, int64_t W, int w,
+                         wbmm_dtype dtype, void *stream);
+
+/* Gradient with respect to the input for upstream gradient dy: per window,
+ * dx = dy * M_c^T.  Because I[j,i] = (2w-1)^2 - 1 - I[i,j], M_c^T is the
+ * matrix of the reversed table, so this runs the forward kernels with the
+ * table read back to front.  dy, dx: [B,C,H,W] in dtype. */
+wbmm_status wbmm_backward_input(const void *dy, const void *table, void *dx,
+                                int64_t B, int64_t C, int64_t H, int64_t W,
+                                int w, wbmm_dtype dtype, void *stream);
+
+/* Size in bytes of the device workspace wbmm_backward_table needs for this
+ * shape (0 when none is needed).  Returns 0 for invalid arguments as well;
+ * wbmm_backward_table reports those. */
+size_t wbmm_backward_table_workspace_bytes(int64_t B, int64_t C, int64_t H,
+                                           int64_t W, int w,
+                                           wbmm_dtype dtype);
+
+/* Gradient with respect to the table:
+ *   dtable[c, k] = sum over images, windows and (input i, output j) pairs with
+ *                  I[i, j] = k of x[.., i] * dy[.., j]
+ * (the scatter-add of the per-window products X^T dY over the relative-offset
+ * index).  x, dy: [B,C,H,W] in dtype; dtable: float32 [C,(2w-1)^2],
+ * overwritten.  workspace: device buffer of at least
+ * wbmm_backward_table_workspace_bytes(...) bytes (may be NULL when that is 0);
+ * its contents on entry do not matter.  The reduction has a fixed order: the
+ * result is bitwise reproducible for a given shape. */
+wbmm_status wbmm_backward_table(const void *x, const void *dy, float *dtable,
+                                void *workspace, size_t workspace_bytes,
+                                int64_t B, int64_t C, int64_t H, int64_t W,
+                                int w, wbmm_dtype dtype, void *stream);
+
+/* Static description of a status code (never NULL). */
+const char *wbmm_status_string(wbmm_status s);
+
+/* Host-only: writes the d*d int32 relative position index I[i][j]
+ * (eq. index_computation) that the kernels evaluate arithmetically, row-major,
+ * d = w*w, into caller-owned host memory.  No GPU work. */
+wbmm_status wbmm_relative_index(int w, int32_t *out_host);
+
+/* Library version, e.g. "0.1.0". */
+const char *wbmm_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WBMM_H */

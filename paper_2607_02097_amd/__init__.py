@@ -1,0 +1,14 @@
+"""MI355X-native WBMM (Windowed Batch Matrix Multiplication).
+
+The operator runs in hand-written HIP kernels for gfx950 behind the C ABI of
+include/wbmm.h (libwbmm.so, built in-tree by ``python -m
+paper_2607_02097_amd.build``).  This package only marshals torch tensors to
+that library.
+"""
+from .binding import (WBMMFunction, WbmmError, load_library, wbmm, wbmm_backward_input,
+                   wbmm_backward_table, wbmm_backward_table_workspace_bytes, wbmm_forward,
+                   wbmm_relative_index, wbmm_status_string, wbmm_version)
+
+__all__ = ["WBMMFunction", "WbmmError", "load_library", "wbmm", "wbmm_backward_input",
+           "wbmm_backward_table", "wbmm_backward_table_workspace_bytes", "wbmm_forward",
+           "wbmm_relative_index", "wbmm_status_string", "wbmm_version"]

@@ -1,0 +1,206 @@
+"""Thin Python binding of the WBMM C ABI (include/wbmm.h).
+
+Argument marshalling only: tensors are handed to libwbmm.so as raw device
+pointers together with torch's current HIP stream; every step of the operator
+runs in the library's HIP kernels.  There is no fallback: if libwbmm.so is not
+built, or a call fails, an exception is raised.
+
+Names follow the C entry points: ``wbmm_forward``, ``wbmm_backward_input``,
+``wbmm_backward_table``, ``wbmm_backward_table_workspace_bytes``,
+``wbmm_relative_index``, ``wbmm_status_string``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libwbmm.so")
+
+WBMM_OK = 0
+WBMM_ERR_INVALID_ARG = 1
+WBMM_ERR_UNSUPPORTED = 2
+WBMM_ERR_HIP = 3
+
+DTYPE_CODES = {torch.float32: 0, torch.bfloat16: 1, torch.float16: 2}
+
+EXPORTED = ("wbmm_forward", "wbmm_backward_input", "wbmm_backward_table",
+            "wbmm_backward_table_workspace_bytes", "wbmm_status_string",
+            "wbmm_relative_index", "wbmm_version")
+
+_lib = None
+
+
+class WbmmError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__("%s: %s" % (what, wbmm_status_string(status)))
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libwbmm.so and declare its signatures.  Raises if it is missing."""
+    global _lib
+    if _lib is not None and path == LIB_PATH:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError("libwbmm.so is not built (%s); run `python -m "
+                           "paper_2607_02097_amd.build` first" % path)
+    lib = ctypes.CDLL(path)
+    vp, i64, ci, st = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_int
+    shape = [i64, i64, i64, i64, ci, ci, vp]
+    lib.wbmm_forward.argtypes = [vp, vp, vp] + shape
+    lib.wbmm_forward.restype = st
+    lib.wbmm_backward_input.argtypes = [vp, vp, vp] + shape
+    lib.wbmm_backward_input.restype = st
+    lib.wbmm_backward_table_workspace_bytes.argtypes = [i64, i64, i64, i64, ci, ci]
+    lib.wbmm_backward_table_workspace_bytes.restype = ctypes.c_size_t
+    lib.wbmm_backward_table.argtypes = [vp, vp, vp, vp, ctypes.c_size_t] + shape
+    lib.wbmm_backward_table.restype = st
+    lib.wbmm_status_string.argtypes = [st]
+    lib.wbmm_status_string.restype = ctypes.c_char_p
+    lib.wbmm_relative_index.argtypes = [ci, ctypes.POINTER(ctypes.c_int32)]
+    lib.wbmm_relative_index.restype = st
+    lib.wbmm_version.argtypes = []
+    lib.wbmm_version.restype = ctypes.c_char_p
+    if path == LIB_PATH:
+        _lib = lib
+    return lib
+
+
+def wbmm_status_string(status: int) -> str:
+    return load_library().wbmm_status_string(int(status)).decode()
+
+
+def _stream(t: torch.Tensor, stream):
+    if stream is None:
+        return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+    if isinstance(stream, torch.cuda.Stream):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def _check_tensor(t: torch.Tensor, name: str):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if t.device.type != "cuda":
+        raise ValueError("%s must be a GPU tensor (got %s)" % (name, t.device))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+
+
+def _code(dtype) -> int:
+    if dtype not in DTYPE_CODES:
+        raise TypeError("unsupported dtype %s (float32, bfloat16, float16)" % dtype)
+    return DTYPE_CODES[dtype]
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _forward_like(fn_name, src, table, w, out, stream):
+    _check_tensor(src, "input")
+    _check_tensor(table, "table")
+    if src.dim() != 4:
+        raise ValueError("input must be [B, C, H, W]")
+    B, C, H, W = src.shape
+    if table.dtype != src.dtype or table.device != src.device:
+        raise ValueError("table must match the input's dtype and device")
+    if out is None:
+        out = torch.empty_like(src)
+    else:
+        _check_tensor(out, "out")
+        if out.shape != src.shape or out.dtype != src.dtype or out.device != src.device:
+            raise ValueError("out must match the input's shape, dtype and device")
+    with torch.cuda.device(src.device):
+        st = getattr(load_library(), fn_name)(_ptr(src), _ptr(table), _ptr(out), B, C, H, W,
+                                              int(w), _code(src.dtype), _stream(src, stream))
+    if st != WBMM_OK:
+        raise WbmmError(st, fn_name)
+    return out
+
+
+def wbmm_forward(x: torch.Tensor, table: torch.Tensor, w: int, out=None, stream=None):
+    """y = WBMM(x; table, w).  x [B,C,H,W], table [C,(2w-1)^2], same dtype."""
+    return _forward_like("wbmm_forward", x, table, w, out, stream)
+
+
+def wbmm_backward_input(dy: torch.Tensor, table: torch.Tensor, w: int, out=None, stream=None):
+    """dx for upstream gradient dy (per window dx = dy M^T)."""
+    return _forward_like("wbmm_backward_input", dy, table, w, out, stream)
+
+
+def wbmm_backward_table_workspace_bytes(shape, w: int, dtype) -> int:
+    B, C, H, W = shape
+    return int(load_library().wbmm_backward_table_workspace_bytes(B, C, H, W, int(w), _code(dtype)))
+
+
+def wbmm_backward_table(x: torch.Tensor, dy: torch.Tensor, w: int, out=None, workspace=None,
+                        stream=None):
+    """dtable (float32 [C,(2w-1)^2], overwritten) for input x and gradient dy."""
+    _check_tensor(x, "x")
+    _check_tensor(dy, "dy")
+    if dy.shape != x.shape or dy.dtype != x.dtype or dy.device != x.device:
+        raise ValueError("dy must match x's shape, dtype and device")
+    B, C, H, W = x.shape
+    k = (2 * int(w) - 1) ** 2
+    if out is None:
+        out = torch.empty((C, k), dtype=torch.float32, device=x.device)
+    else:
+        _check_tensor(out, "out")
+        if out.dtype != torch.float32 or out.numel() != C * k or out.device != x.device:
+            raise ValueError("out must be float32 [C, (2w-1)^2] on x's device")
+    need = wbmm_backward_table_workspace_bytes(x.shape, w, x.dtype)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
+    ws_ptr = ctypes.c_void_p(workspace.data_ptr() if workspace is not None else 0)
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    with torch.cuda.device(x.device):
+        st = load_library().wbmm_backward_table(_ptr(x), _ptr(dy), _ptr(out), ws_ptr, ws_bytes,
+                                                B, C, H, W, int(w), _code(x.dtype),
+                                                _stream(x, stream))
+    if st != WBMM_OK:
+        raise WbmmError(st, "wbmm_backward_table")
+    return out
+
+
+def wbmm_relative_index(w: int) -> torch.Tensor:
+    """The int32 [d, d] index I of eq. index_computation (host tensor)."""
+    d = int(w) * int(w)
+    out = torch.empty((d, d), dtype=torch.int32)
+    st = load_library().wbmm_relative_index(
+        int(w), ctypes.cast(out.data_ptr(), ctypes.POINTER(ctypes.c_int32)))
+    if st != WBMM_OK:
+        raise WbmmError(st, "wbmm_relative_index")
+    return out
+
+
+def wbmm_version() -> str:
+    return load_library().wbmm_version().decode()
+
+
+class WBMMFunction(torch.autograd.Function):
+    """Autograd composition of the three entry points (the table gradient is
+    computed in float32 and cast to the table's dtype)."""
+
+    @staticmethod
+    def forward(ctx, x, table, w):
+        ctx.w = int(w)
+        ctx.save_for_backward(x, table)
+        return wbmm_forward(x.contiguous(), table.contiguous(), ctx.w)
+
+    @staticmethod
+    def backward(ctx, dy):
+        x, table = ctx.saved_tensors
+        dy = dy.contiguous()
+        dx = wbmm_backward_input(dy, table, ctx.w) if ctx.needs_input_grad[0] else None
+        dt = None
+        if ctx.needs_input_grad[1]:
+            dt = wbmm_backward_table(x, dy, ctx.w).to(table.dtype)
+        return dx, dt, None
+
+
+def wbmm(x, table, w):
+    """Differentiable WBMM: y = WBMM(x; table, w)."""
+    return WBMMFunction.apply(x, table, w)

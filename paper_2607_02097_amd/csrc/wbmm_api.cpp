@@ -1,0 +1,149 @@
+// C-ABI front end of the WBMM library: argument validation, status codes and
+// dispatch to the HIP kernels.  Every check runs on the host before any GPU
+// work is enqueued; nothing here allocates, prints or aborts.
+#include "wbmm.h"
+
+#include <stdint.h>
+#include <string.h>
+
+#include "wbmm_internal.h"
+
+namespace {
+
+using wbmm::Dt;
+using wbmm::Geom;
+
+size_t elem_size(wbmm_dtype d) {
+  switch (d) {
+    case WBMM_F32: return 4;
+    case WBMM_BF16: return 2;
+    case WBMM_F16: return 2;
+  }
+  return 0;
+}
+
+bool valid_dtype(int d) { return d == WBMM_F32 || d == WBMM_BF16 || d == WBMM_F16; }
+
+// Overflow-checked product of non-negative int64 values.
+bool mul_ok(int64_t a, int64_t b, int64_t *out) {
+  if (a < 0 || b < 0) return false;
+  if (a != 0 && b > INT64_MAX / a) return false;
+  *out = a * b;
+  return true;
+}
+
+// Validates the shape and fills g.  Returns WBMM_OK, INVALID_ARG or
+// UNSUPPORTED; bytes receives the size of one [B,C,H,W] tensor.
+wbmm_status check_shape(int64_t B, int64_t C, int64_t H, int64_t W, int w, wbmm_dtype dtype,
+                        Geom *g, int64_t *bytes) {
+  if (!valid_dtype((int)dtype)) return WBMM_ERR_UNSUPPORTED;
+  if (B <= 0 || C <= 0 || H <= 0 || W <= 0 || w <= 0) return WBMM_ERR_INVALID_ARG;
+  if (w < wbmm::kMinWindow || w > wbmm::kMaxWindow) return WBMM_ERR_UNSUPPORTED;
+  int64_t bc, hw, n, b;
+  if (!mul_ok(B, C, &bc) || !mul_ok(H, W, &hw) || !mul_ok(bc, hw, &n) ||
+      !mul_ok(n, (int64_t)elem_size(dtype), &b))
+    return WBMM_ERR_INVALID_ARG;
+  g->B = B; g->C = C; g->H = H; g->W = W; g->w = w;
+  g->NH = (H + w - 1) / w;
+  g->NW = (W + w - 1) / w;
+  int64_t nwin;
+  if (!mul_ok(B, g->NH * g->NW, &nwin)) return WBMM_ERR_INVALID_ARG;
+  g->N = nwin;
+  // Kernel-side limits: a band (w image rows) is indexed with 32-bit ints and
+  // the grid is one-dimensional.
+  if ((int64_t)w * W * 4 > INT32_MAX / 2) return WBMM_ERR_UNSUPPORTED;
+  if (C * g->N > (int64_t)UINT32_MAX) return WBMM_ERR_UNSUPPORTED;
+  *bytes = b;
+  return WBMM_OK;
+}
+
+bool overlap(const void *a, int64_t an, const void *b, int64_t bn) {
+  const uintptr_t pa = (uintptr_t)a, pb = (uintptr_t)b;
+  return pa < pb + (uintptr_t)bn && pb < pa + (uintptr_t)an;
+}
+
+bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+wbmm_status from_hip(hipError_t e) { return e == hipSuccess ? WBMM_OK : WBMM_ERR_HIP; }
+
+wbmm_status forward_like(const void *in, const void *table, void *out, int64_t B, int64_t C,
+                         int64_t H, int64_t W, int w, wbmm_dtype dtype, void *stream, bool rev) {
+  Geom g;
+  int64_t bytes = 0;
+  wbmm_status s = check_shape(B, C, H, W, w, dtype, &g, &bytes);
+  if (s != WBMM_OK) return s;
+  if (!in || !table || !out) return WBMM_ERR_INVALID_ARG;
+  const size_t es = elem_size(dtype);
+  if (!aligned(in, es) || !aligned(table, es) || !aligned(out, es)) return WBMM_ERR_INVALID_ARG;
+  const int64_t tbytes = C * (int64_t)(2 * w - 1) * (2 * w - 1) * (int64_t)es;
+  if (overlap(in, bytes, out, bytes) || overlap(table, tbytes, out, bytes)) return WBMM_ERR_INVALID_ARG;
+  return from_hip(wbmm::launch_forward((Dt)dtype, in, table, out, g, rev, (hipStream_t)stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+wbmm_status wbmm_forward(const void *x, const void *table, void *y, int64_t B, int64_t C, int64_t H,
+                         int64_t W, int w, wbmm_dtype dtype, void *stream) {
+  return forward_like(x, table, y, B, C, H, W, w, dtype, stream, false);
+}
+
+wbmm_status wbmm_backward_input(const void *dy, const void *table, void *dx, int64_t B, int64_t C,
+                                int64_t H, int64_t W, int w, wbmm_dtype dtype, void *stream) {
+  return forward_like(dy, table, dx, B, C, H, W, w, dtype, stream, true);
+}
+
+size_t wbmm_backward_table_workspace_bytes(int64_t B, int64_t C, int64_t H, int64_t W, int w,
+                                           wbmm_dtype dtype) {
+  Geom g;
+  int64_t bytes = 0;
+  if (check_shape(B, C, H, W, w, dtype, &g, &bytes) != WBMM_OK) return 0;
+  return wbmm::dtable_workspace_bytes((Dt)dtype, g);
+}
+
+wbmm_status wbmm_backward_table(const void *x, const void *dy, float *dtable, void *workspace,
+                                size_t workspace_bytes, int64_t B, int64_t C, int64_t H, int64_t W,
+                                int w, wbmm_dtype dtype, void *stream) {
+  Geom g;
+  int64_t bytes = 0;
+  wbmm_status s = check_shape(B, C, H, W, w, dtype, &g, &bytes);
+  if (s != WBMM_OK) return s;
+  if (!x || !dy || !dtable) return WBMM_ERR_INVALID_ARG;
+  const size_t es = elem_size(dtype);
+  if (!aligned(x, es) || !aligned(dy, es) || !aligned(dtable, 4)) return WBMM_ERR_INVALID_ARG;
+  const int64_t tbytes = C * (int64_t)(2 * w - 1) * (2 * w - 1) * 4;
+  if (overlap(x, bytes, dtable, tbytes) || overlap(dy, bytes, dtable, tbytes)) return WBMM_ERR_INVALID_ARG;
+  const size_t need = wbmm::dtable_workspace_bytes((Dt)dtype, g);
+  if (need > 0) {
+    if (!workspace || workspace_bytes < need || !aligned(workspace, 4)) return WBMM_ERR_INVALID_ARG;
+    if (overlap(workspace, (int64_t)need, dtable, tbytes) || overlap(workspace, (int64_t)need, x, bytes) ||
+        overlap(workspace, (int64_t)need, dy, bytes))
+      return WBMM_ERR_INVALID_ARG;
+  }
+  return from_hip(wbmm::launch_dtable((Dt)dtype, x, dy, dtable, workspace, g, (hipStream_t)stream));
+}
+
+const char *wbmm_status_string(wbmm_status s) {
+  switch (s) {
+    case WBMM_OK: return "WBMM_OK";
+    case WBMM_ERR_INVALID_ARG: return "WBMM_ERR_INVALID_ARG: invalid argument";
+    case WBMM_ERR_UNSUPPORTED: return "WBMM_ERR_UNSUPPORTED: unsupported window size or dtype";
+    case WBMM_ERR_HIP: return "WBMM_ERR_HIP: HIP runtime error";
+  }
+  return "WBMM: unknown status";
+}
+
+wbmm_status wbmm_relative_index(int w, int32_t *out_host) {
+  if (!out_host || w <= 0) return WBMM_ERR_INVALID_ARG;
+  if (w > wbmm::kMaxWindow) return WBMM_ERR_UNSUPPORTED;
+  const int d = w * w, k1 = 2 * w - 1;
+  for (int i = 0; i < d; ++i)
+    for (int j = 0; j < d; ++j)
+      out_host[i * d + j] = (i / w - j / w + w - 1) * k1 + (i % w - j % w + w - 1);
+  return WBMM_OK;
+}
+
+const char *wbmm_version(void) { return "0.1.0"; }
+
+}  // extern "C"

@@ -1,0 +1,56 @@
+// Dispatch of (dtype, window size) to the kernel instantiations compiled in
+// the wbmm_inst.hip translation units.
+#include <hip/hip_runtime.h>
+
+#include "wbmm_internal.h"
+
+namespace wbmm {
+
+extern Entry entries_TagF32_1[8], entries_TagF32_9[8];
+extern Entry entries_TagBF16_1[8], entries_TagBF16_9[8];
+extern Entry entries_TagF16_1[8], entries_TagF16_9[8];
+
+namespace {
+
+const Entry *find(Dt dt, int w) {
+  if (w < kMinWindow || w > kMaxWindow) return nullptr;
+  const int hi = w > 8;
+  const int k = hi ? w - 9 : w - 1;
+  switch (dt) {
+    case Dt::F32: return hi ? &entries_TagF32_9[k] : &entries_TagF32_1[k];
+    case Dt::BF16: return hi ? &entries_TagBF16_9[k] : &entries_TagBF16_1[k];
+    case Dt::F16: return hi ? &entries_TagF16_9[k] : &entries_TagF16_1[k];
+  }
+  return nullptr;
+}
+
+}  // namespace
+
+hipError_t launch_forward(Dt dt, const void *x, const void *table, void *y, const Geom &g,
+                          bool reverse_table, hipStream_t stream) {
+  const Entry *e = find(dt, g.w);
+  if (!e) return hipErrorInvalidValue;
+  return e->fwd(x, table, y, g, reverse_table, stream);
+}
+
+hipError_t launch_dtable(Dt dt, const void *x, const void *dy, float *dtable, void *workspace,
+                         const Geom &g, hipStream_t stream) {
+  const Entry *e = find(dt, g.w);
+  if (!e) return hipErrorInvalidValue;
+  return e->dtable(x, dy, dtable, workspace, g, stream);
+}
+
+DtPlan plan_dtable(Dt dt, const Geom &g) {
+  const Entry *e = find(dt, g.w);
+  if (!e) return DtPlan{0, 0};
+  return e->plan(g);
+}
+
+size_t dtable_workspace_bytes(Dt dt, const Geom &g) {
+  const DtPlan p = plan_dtable(dt, g);
+  if (p.slabs <= 1) return 0;
+  const int64_t k1 = 2 * g.w - 1;
+  return (size_t)p.slabs * (size_t)g.C * (size_t)(k1 * k1) * sizeof(float);
+}
+
+}  // namespace wbmm

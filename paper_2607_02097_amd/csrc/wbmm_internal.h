@@ -1,0 +1,54 @@
+// Internal interface between the C-ABI front end (wbmm_api.cpp) and the HIP
+// kernels (wbmm_kernels.hip).  Not installed, not part of the ABI.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime.h>
+
+namespace wbmm {
+
+enum class Dt { F32 = 0, BF16 = 1, F16 = 2 };
+
+// Geometry of one call.  N is the number of windows per channel,
+// N = B * NH * NW with NH = ceil(H / w), NW = ceil(W / w).
+struct Geom {
+  int64_t B, C, H, W;
+  int w;
+  int64_t NH, NW, N;
+};
+
+constexpr int kMinWindow = 1;
+constexpr int kMaxWindow = 16;
+
+// Launch plan of the dtable pass: windows per slab and number of slabs; one
+// workgroup per (channel, slab).  Slabs > 1 need a float32 workspace of
+// slabs * C * (2w-1)^2 entries.
+struct DtPlan {
+  int64_t slab_windows;
+  int64_t slabs;
+};
+
+DtPlan plan_dtable(Dt dt, const Geom &g);
+size_t dtable_workspace_bytes(Dt dt, const Geom &g);
+
+// Each returns hipSuccess or the error of the launch.
+hipError_t launch_forward(Dt dt, const void *x, const void *table, void *y,
+                          const Geom &g, bool reverse_table,
+                          hipStream_t stream);
+hipError_t launch_dtable(Dt dt, const void *x, const void *dy, float *dtable,
+                         void *workspace, const Geom &g, hipStream_t stream);
+
+// Per-(dtype, window) entry points, defined by the wbmm_inst.hip
+// translation units and collected into tables by wbmm_dispatch.cpp.
+typedef hipError_t (*FwdFn)(const void *, const void *, void *, const Geom &, bool, hipStream_t);
+typedef hipError_t (*DtFn)(const void *, const void *, float *, void *, const Geom &, hipStream_t);
+typedef DtPlan (*PlanFn)(const Geom &);
+struct Entry {
+  FwdFn fwd;
+  DtFn dtable;
+  PlanFn plan;
+};
+
+}  // namespace wbmm

@@ -1,0 +1,37 @@
+"""Shared helpers of the test-suite: tensor marshalling and error metrics."""
+import numpy as np
+import torch
+
+from paper_2607_02097_amd import synth
+
+TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}
+# Tolerances on the infinity-norm relative error max|gpu - oracle| / max|oracle|
+# (float32: products and sums in fp32; 16-bit: one rounding of the fp32 result
+# to bf16/fp16, whose half-ulp is 2^-9 resp. 2^-12 relative, plus fp32 sums).
+TOL = {"f32": 1e-4, "bf16": 2e-2, "f16": 2e-2}
+
+
+def to_device(storage: np.ndarray, dtype: str, device="cuda") -> torch.Tensor:
+    """Storage array from synth.round_to -> torch tensor on the device."""
+    if dtype == "bf16":
+        t = torch.from_numpy(storage.view(np.int16).copy()).view(torch.bfloat16)
+    else:
+        t = torch.from_numpy(np.ascontiguousarray(storage))
+    return t.to(device)
+
+
+def to_f64(t: torch.Tensor) -> np.ndarray:
+    return t.detach().to("cpu").to(torch.float64).numpy()
+
+
+def rel_inf(got, want) -> float:
+    got = np.asarray(got, np.float64)
+    want = np.asarray(want, np.float64)
+    den = np.abs(want).max()
+    if den == 0:
+        return float(np.abs(got).max())
+    return float(np.abs(got - want).max() / den)
+
+
+def draw(B, C, H, W, w, dtype, seed=0):
+    return synth.draw(B, C, H, W, w, dtype, seed)

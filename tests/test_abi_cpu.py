@@ -1,0 +1,106 @@
+"""CPU-side checks of the C-ABI library: it loads, exports every function that
+include/wbmm.h declares, and rejects bad arguments on the host before any GPU
+work (only argument combinations that fail validation are sent, so no kernel
+is ever launched here)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_02097_amd import binding as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "wbmm.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(wbmm_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return W.load_library()
+
+
+def test_library_exports_every_declared_function(lib):
+    names = declared_functions()
+    assert set(names) == set(W.EXPORTED)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(lib):
+    for s in (0, 1, 2, 3):
+        assert W.wbmm_status_string(s).startswith("WBMM")
+    assert "unknown" in W.wbmm_status_string(77)
+    assert W.wbmm_version().count(".") == 2
+
+
+@pytest.mark.parametrize("w", [1, 2, 5, 7, 14, 16])
+def test_relative_index_matches_oracle_bit_exact(lib, w, olib):
+    assert np.array_equal(W.wbmm_relative_index(w).numpy(), oracle.relative_index(w, lib=olib))
+
+
+def test_relative_index_errors(lib):
+    buf = (ctypes.c_int32 * 4)()
+    assert lib.wbmm_relative_index(0, buf) == W.WBMM_ERR_INVALID_ARG
+    assert lib.wbmm_relative_index(17, buf) == W.WBMM_ERR_UNSUPPORTED
+    assert lib.wbmm_relative_index(2, None) == W.WBMM_ERR_INVALID_ARG
+
+
+FAKE = 0x100000  # never dereferenced: every call below fails validation
+
+
+def fwd(lib, x=FAKE, t=FAKE * 4, y=FAKE * 8, B=1, C=2, H=7, Wd=7, w=7, dt=1, fn="wbmm_forward"):
+    return getattr(lib, fn)(ctypes.c_void_p(x), ctypes.c_void_p(t), ctypes.c_void_p(y),
+                            B, C, H, Wd, w, dt, None)
+
+
+@pytest.mark.parametrize("fn", ["wbmm_forward", "wbmm_backward_input"])
+def test_forward_like_rejects_bad_arguments(lib, fn):
+    E, U = W.WBMM_ERR_INVALID_ARG, W.WBMM_ERR_UNSUPPORTED
+    assert fwd(lib, x=0, fn=fn) == E
+    assert fwd(lib, t=0, fn=fn) == E
+    assert fwd(lib, y=0, fn=fn) == E
+    for k in ("B", "C", "H", "Wd"):
+        assert fwd(lib, fn=fn, **{k: 0}) == E
+        assert fwd(lib, fn=fn, **{k: -3}) == E
+    assert fwd(lib, w=0, fn=fn) == E
+    assert fwd(lib, w=17, fn=fn) == U
+    assert fwd(lib, dt=7, fn=fn) == U
+    assert fwd(lib, x=FAKE + 1, fn=fn) == E            # misaligned bf16 pointer
+    assert fwd(lib, y=FAKE, fn=fn) == E                # output aliases input
+    assert fwd(lib, y=FAKE + 2 * 49, fn=fn) == E      # output overlaps input tail
+    assert fwd(lib, B=2 ** 40, C=2 ** 20, fn=fn) == E  # size overflow
+
+
+def test_backward_table_rejects_bad_arguments(lib):
+    E = W.WBMM_ERR_INVALID_ARG
+    vp = ctypes.c_void_p
+
+    def call(x=FAKE, dy=FAKE * 8, dt=FAKE * 16, ws=0, wsb=0, B=1, C=2, H=7, Wd=7, w=7, d=1):
+        return lib.wbmm_backward_table(vp(x), vp(dy), vp(dt), vp(ws), wsb, B, C, H, Wd, w, d, None)
+
+    assert call(x=0) == E
+    assert call(dy=0) == E
+    assert call(dt=0) == E
+    assert call(dt=FAKE * 16 + 2) == E                 # dtable must be 4-byte aligned
+    assert call(dt=FAKE) == E                          # dtable overlaps x
+    assert call(w=18) == W.WBMM_ERR_UNSUPPORTED
+    # a shape that needs a workspace: missing / too small workspace is rejected
+    need = lib.wbmm_backward_table_workspace_bytes(64, 192, 28, 28, 14, 1)
+    assert need > 0
+    assert call(B=64, C=192, H=28, Wd=28, w=14, x=FAKE, dy=FAKE * 64, dt=FAKE * 128) == E
+    assert call(B=64, C=192, H=28, Wd=28, w=14, x=FAKE, dy=FAKE * 64, dt=FAKE * 128,
+                ws=FAKE * 256, wsb=need - 4) == E
+
+
+def test_workspace_query(lib):
+    assert lib.wbmm_backward_table_workspace_bytes(0, 1, 1, 1, 7, 1) == 0
+    assert lib.wbmm_backward_table_workspace_bytes(1, 8, 28, 28, 7, 0) == 0  # one slab
+    n = lib.wbmm_backward_table_workspace_bytes(64, 192, 28, 28, 14, 1)
+    assert n % (192 * 729 * 4) == 0
