@@ -1,0 +1,251 @@
+#!/usr/bin/env python3
+"""Benchmark of the WBMM hot path on one MI355X.
+
+One step = forward + input gradient + table gradient (all three passes of the
+operator) over one batch of seeded synthetic input already resident in device
+memory.  The headline workload is the w=14 stage shape B=64, C=192, H=W=28 in
+bfloat16 with float32 accumulation.
+
+Prints ONE JSON line with the throughput (algorithmic TFLOP/s, 6*C*N*d^2 per
+step), the roofline of the dominant kernel (timed live with HIP events on the
+stream the kernels run on) and the fp64 CPU oracle timed on the host cores.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0      # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2516.6  # MI355X dense bf16/fp16 matrix-core peak
+F32_PEAK_TFLOPS = 157.3    # MI355X fp32 matrix/vector peak
+HEADLINE = "bf16_b64_c192_28_w14"
+METRIC = "WBMM fwd+bwd TFLOP/s & % bf16 MFMA peak, B=64 C=192 28² w=14"
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=2000)
+    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--workload", default=HEADLINE)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cold", action="store_true",
+                   help="rotate through enough input sets to defeat the 256 MB Infinity Cache")
+    return p.parse_args()
+
+
+def pass_bytes(wl, p, es):
+    """Algorithmic bytes of one pass (each tensor touched once)."""
+    act = wl.B * wl.C * wl.H * wl.W * es
+    tab = wl.C * wl.table_len
+    if p in ("fwd", "dx"):
+        return 2 * act + tab * es          # read input, write output, read table
+    return 2 * act + tab * 4               # read x and dy, write float32 dtable
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on one GPU only: the WBMM path shards over channels "
+              "with no collective, so there is no multi-GPU step to time "
+              "(asked for --gpus %d, WORLD_SIZE=%d)" % (args.gpus, world), file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2607_02097_amd import binding as W
+    from paper_2607_02097_amd import synth
+
+    wl = synth.WORKLOADS[args.workload]
+    es = 4 if wl.dtype == "f32" else 2
+    tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[wl.dtype]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    W.load_library()
+
+    d = synth.draw_workload(wl, seed=0)
+
+    def put(a):
+        if wl.dtype == "bf16":
+            return torch.from_numpy(a.view(np.int16).copy()).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    nsets = 1
+    if args.cold:
+        per = 3 * wl.B * wl.C * wl.H * wl.W * es
+        nsets = max(2, int(np.ceil(2 * 256e6 / per)) + 1)
+    sets = []
+    for i in range(nsets):
+        x, t, dy = put(d["x"]), put(d["t"]), put(d["dy"])
+        y, dx = torch.empty_like(x), torch.empty_like(dy)
+        dtab = torch.empty((wl.C, wl.table_len), dtype=torch.float32, device=dev)
+        need = W.wbmm_backward_table_workspace_bytes(x.shape, wl.w, tdt)
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+        sets.append((x, t, dy, y, dx, dtab, ws))
+
+    passes = wl.passes
+    lib = W.load_library()
+    code = W.DTYPE_CODES[tdt]
+    import ctypes
+    vp = ctypes.c_void_p
+
+    def launch(p, i):
+        """One pass through the C ABI on torch's current stream (raw pointers,
+        no per-call Python checks: the shapes were validated above)."""
+        x, t, dy, y, dx, dtab, ws = sets[i % nsets]
+        st = vp(torch.cuda.current_stream(dev).cuda_stream)
+        dims = (wl.B, wl.C, wl.H, wl.W, wl.w, code, st)
+        if p == "fwd":
+            r = lib.wbmm_forward(vp(x.data_ptr()), vp(t.data_ptr()), vp(y.data_ptr()), *dims)
+        elif p == "dx":
+            r = lib.wbmm_backward_input(vp(dy.data_ptr()), vp(t.data_ptr()), vp(dx.data_ptr()), *dims)
+        else:
+            r = lib.wbmm_backward_table(vp(x.data_ptr()), vp(dy.data_ptr()), vp(dtab.data_ptr()),
+                                        vp(ws.data_ptr()), ws.numel(), *dims)
+        if r != 0:
+            raise RuntimeError("%s failed: %s" % (p, W.wbmm_status_string(r)))
+
+    # warm-up, eager
+    for i in range(args.warmup):
+        for p in passes:
+            launch(p, i)
+    torch.cuda.synchronize()
+
+    # eager timing (includes host launch overhead; reported, not the value)
+    stream = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    n_eager = min(args.steps, 50)
+    e0.record(stream)
+    for i in range(n_eager):
+        for p in passes:
+            launch(p, i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    eager_ms = e0.elapsed_time(e1) / n_eager
+
+    # HIP graphs: R consecutive steps per graph (and R launches per pass graph)
+    R = 10
+
+    def capture(seq):
+        g = torch.cuda.CUDAGraph()
+        cs = torch.cuda.Stream(dev)
+        cs.wait_stream(stream)
+        with torch.cuda.graph(g, stream=cs):
+            for i, p in enumerate(seq):
+                launch(p, i // len(passes) if len(seq) > R else i)
+        stream.wait_stream(cs)
+        torch.cuda.synchronize()
+        return g
+
+    g_step = capture([p for _ in range(R) for p in passes])
+    g_pass = {p: capture([p] * R) for p in passes}
+    for _ in range(3):
+        g_step.replay()
+        for p in passes:
+            g_pass[p].replay()
+    torch.cuda.synchronize()
+
+    # timed region: K steps = K/R replays of the step graph, bracketed by
+    # synchronisation; then each pass graph timed with HIP events on the
+    # same stream to get the average duration of each kernel launch
+    reps = max(1, args.steps // R)
+    steps = reps * R
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for _ in range(reps):
+        g_step.replay()
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    ms_step = total_ms / steps
+    per_pass = {}
+    for p in passes:
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(reps):
+            g_pass[p].replay()
+        b.record(stream)
+        torch.cuda.synchronize()
+        per_pass[p] = a.elapsed_time(b) / (reps * R)
+    args.steps = steps
+
+    flops = wl.flops()
+    tflops = flops / (ms_step * 1e-3) / 1e12
+    peak = BF16_PEAK_TFLOPS if wl.dtype in ("bf16", "f16") else F32_PEAK_TFLOPS
+
+    # dominant kernel: the pass with the largest average duration
+    dom = max(per_pass, key=per_pass.get)
+    dom_ms = per_pass[dom]
+    dom_bytes = pass_bytes(wl, dom, es)
+    dom_flops = wl.flops((dom,))
+    ai = dom_flops / dom_bytes
+    ridge = peak * 1e12 / (HBM_PEAK_GBS * 1e9)
+    kernel_name = {"fwd": "wbmm_fwd_kernel", "dx": "wbmm_fwd_kernel(reversed table)",
+                   "dt": "wbmm_dt_kernel+wbmm_dt_reduce_kernel"}[dom]
+    if ai < ridge:
+        achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
+    else:
+        achieved = dom_flops / (dom_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
+                "unit": "TFLOP/s", "frac": round(achieved / peak, 4)}
+    roof.update({"traffic": None, "kernel": kernel_name, "pass": dom,
+                 "avg_ms": round(dom_ms, 5), "algorithmic_bytes": dom_bytes,
+                 "algorithmic_flops": dom_flops})
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        t0 = time.perf_counter()
+        if "fwd" in passes:
+            oracle.forward(d["x64"], d["t64"], wl.w)
+        if "dx" in passes:
+            oracle.backward_input(d["dy64"], d["t64"], wl.w)
+        if "dt" in passes:
+            oracle.backward_table(d["x64"], d["dy64"], wl.w)
+        cpu_s = time.perf_counter() - t0
+        cpu = {"value": round(flops / cpu_s / 1e12, 6), "unit": "TFLOP/s",
+               "cores": oracle.max_threads(), "kind": "oracle",
+               "sample": "whole workload, all passes (%s), fp64, %.2f s" % ("+".join(passes), cpu_s)}
+
+    out = {
+        "metric": METRIC if args.workload == HEADLINE else "WBMM %s TFLOP/s, %s" % ("+".join(passes), args.workload),
+        "value": round(tflops, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic (seeded N(0,1) activations/gradients, N(0,0.02^2) table)",
+        "config": {"workload": wl.name, "B": wl.B, "C": wl.C, "H": wl.H, "W": wl.W, "w": wl.w,
+                   "passes": list(passes), "cold_cache": bool(args.cold), "input_sets": nsets},
+        "pct_bf16_mfma_peak": round(100 * tflops / peak, 3),
+        "per_pass_ms": {k: round(v, 5) for k, v in per_pass.items()},
+        "launch": "HIP graph replay, %d steps per graph" % R,
+        "eager_ms_per_step": round(eager_ms, 5),
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -49,9 +49,9 @@ wbmm_status check_shape(int64_t B, int64_t C, int64_t H, int64_t W, int w, wbmm_
   int64_t nwin;
   if (!mul_ok(B, g->NH * g->NW, &nwin)) return WBMM_ERR_INVALID_ARG;
   g->N = nwin;
-  // Kernel-side limits: a band (w image rows) is indexed with 32-bit ints and
-  // the grid is one-dimensional.
-  if ((int64_t)w * W * 4 > INT32_MAX / 2) return WBMM_ERR_UNSUPPORTED;
+  // Kernel-side limits: window indices per channel are split with a float
+  // reciprocal (exact below 2^24) and the grid is one-dimensional.
+  if (g->N >= (int64_t)1 << 24) return WBMM_ERR_UNSUPPORTED;
   if (C * g->N > (int64_t)UINT32_MAX) return WBMM_ERR_UNSUPPORTED;
   *bytes = b;
   return WBMM_OK;

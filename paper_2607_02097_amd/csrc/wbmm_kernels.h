@@ -1,4 +1,3 @@
-#pragma once
 // WBMM kernels for gfx950 (MI355X, CDNA4): device code and per-shape host
 // launchers.  Included by wbmm_inst.hip, which instantiates it for one dtype
 // and a range of window sizes per translation unit.
@@ -8,38 +7,45 @@
 //   I(i, j) = (h_i - h_j + w - 1)(2w - 1) + (w_i - w_j + w - 1)
 // with i the input and j the output position inside one w x w window.
 //
-// Data layout inside the kernels
-// ------------------------------
-// Window positions are stored "row padded": position (h, x) of a window sits at
-// p = h * RP + x with RP = 8 (w <= 8) or 16 (w <= 16); the columns x >= w and
-// the rows h >= w are zero.  A 16-wide tile of p is then one padded window row
-// (RP = 16) or two (RP = 8), which is what makes the matrix M_c cheap to
-// produce on chip: M_c is block-Toeplitz (Theorem 3.2), the block linking input
-// row h_i to output row h_j depends only on h_i - h_j, so every matrix-core
-// B fragment of M_c depends only on (2 * kstep - ntile) and a kernel needs at
-// most 2S + NT - 2 distinct fragments (26 at w = 14) instead of all of M_c.
+// Layout on chip
+// --------------
+// Window positions are "row padded": position (h, x) of a window sits at
+// p = h * RP + x with RP = 8 (w <= 8) or 16 (w <= 16), columns x >= w and rows
+// h >= w being zero.  A 16-wide tile of p is then one padded window row
+// (RP = 16) or two (RP = 8).  M_c is block-Toeplitz (Theorem 3.2): the block
+// linking input row h_i to output row h_j depends only on h_i - h_j.  So every
+// matrix-core B fragment of M_c depends only on (2 * kstep - ntile), and a
+// kernel needs 2S + NT - 2 distinct fragments (26 at w = 14) instead of M_c.
 //
-// Global memory is read and written in aligned 16-byte chunks of window
-// "bands" (w consecutive image rows of one (b, c) plane, contiguous in NCHW);
-// each element is routed to its LDS slot by its (row, column).  Chunks that
-// straddle the edge of a band fall back to element accesses, so no byte
-// outside the caller's tensors is touched.
+// Data movement
+// -------------
+// The unit of global traffic is one window row (w consecutive elements of an
+// image row).  Lanes walk rows in memory order (window column fastest, then
+// the row inside the band, then the band), so a wavefront touches one
+// contiguous stretch of the tensor; a row moves as dwords when it is
+// dword-aligned and whole, element by element otherwise (image edges, odd
+// windows).  Forward: rows land in a window-major LDS tile, already padded,
+// so a matrix-core A fragment is one aligned 16-byte LDS read.  Table
+// gradient: rows land position-major (windows contiguous), so fragments of
+// X^T and dY are contiguous too; the write of a row is w 16-bit LDS stores at
+// a constant stride.
 //
-// Forward / backward-input kernel: one workgroup = (channel, tile of
-// windows).  X tile -> LDS (window-major); T[c] -> LDS; Toeplitz blocks
-// TB[dh][x_out][x_in] -> LDS; each wave keeps the distinct B fragments in
-// registers and runs 16-window sub-tiles through v_mfma_f32_16x16x32_{bf16,
-// f16} (or v_mfma_f32_16x16x4_f32); results go back through LDS to coalesced
-// band stores.  The input gradient reuses it with the table read reversed,
-// because M_c^T is the matrix of the reversed table.
+// Forward / backward-input: one workgroup = (channel, tile of windows).  The
+// table T[c] -> LDS, Toeplitz blocks TB[dh][x_out][x_in] -> LDS, each wave
+// keeps the distinct B fragments in registers and runs 16-window sub-tiles
+// through v_mfma_f32_16x16x32_{bf16,f16} (v_mfma_f32_16x16x4_f32 for
+// float32); results are rounded once and go back through LDS.  The input
+// gradient is the same kernel with the table read back to front, since M_c^T
+// is the matrix of the reversed table.
 //
-// Backward-table kernel: one workgroup = (channel, slab of windows).  X and dY
-// chunks -> LDS position-major (windows contiguous), so matrix-core fragments
-// of X^T and dY are contiguous.  The accumulator for the 16x16 block pair
-// (input tile pi, output tile po) only matters through pi - po, so all pairs
-// with equal pi - po share one accumulator (27 16x16 fp32 tiles at w = 14),
-// split across the four waves.  Diagonal sums of those tiles give dT.  Slabs
-// are combined by a second kernel in a fixed order (no atomics anywhere).
+// Table gradient: one workgroup = (channel, slab of windows), K = windows.
+// The 16x16 block pair (input tile pi, output tile po) only matters through
+// pi - po, so all pairs with equal pi - po share one accumulator (27 16x16
+// fp32 tiles at w = 14), split across the four waves.  The next stage's rows
+// are loaded into registers while the current stage computes.  Diagonal sums
+// of the tiles give dT; slabs are combined by a second kernel in a fixed
+// order (no atomics anywhere, bitwise reproducible).
+#pragma once
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -51,8 +57,12 @@ namespace wbmm {
 typedef unsigned short u16;
 typedef u16 u16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+// dword-aligned 16-byte vector (global rows are only 4-byte aligned)
+typedef uint32_t u32x4a __attribute__((ext_vector_type(4))) __attribute__((aligned(4)));
 
 constexpr int kThreads = 256;  // 4 waves of 64
 constexpr int kWaves = 4;
@@ -64,7 +74,7 @@ __host__ __device__ constexpr int cdiv(int a, int b) { return (a + b - 1) / b; }
 // ----------------------------------------------------------------- dtypes
 
 struct TagF32 {
-  typedef float S;   // storage
+  typedef float S;     // storage
   typedef float Frag;  // matrix-core operand per lane
   static constexpr int ES = 4;
   static constexpr bool W16 = false;
@@ -85,19 +95,17 @@ struct TagF16 {
   static constexpr int KS = 32;
 };
 
-__device__ inline float bf16_to_f(u16 v) { return __uint_as_float((uint32_t)v << 16); }
-__device__ inline u16 f_to_bf16(float f) {  // round to nearest even
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (u16)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (u16)(u >> 16);
+// Two float32 values rounded once (nearest even) and packed into a dword,
+// the first in the low half.
+template <class Tag> __device__ inline uint32_t pack2(float a, float b);
+template <> __device__ inline uint32_t pack2<TagBF16>(float a, float b) {
+  const bf16x2 v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
 }
-__device__ inline u16 f_to_f16(float f) { return __builtin_bit_cast(u16, (_Float16)f); }
-
-template <class Tag> __device__ inline typename Tag::S from_f32(float f);
-template <> __device__ inline float from_f32<TagF32>(float f) { return f; }
-template <> __device__ inline u16 from_f32<TagBF16>(float f) { return f_to_bf16(f); }
-template <> __device__ inline u16 from_f32<TagF16>(float f) { return f_to_f16(f); }
+template <> __device__ inline uint32_t pack2<TagF16>(float a, float b) {
+  const f16x2 v = {(_Float16)a, (_Float16)b};
+  return __builtin_bit_cast(uint32_t, v);
+}
 
 template <class Tag> __device__ inline f32x4 mma(typename Tag::Frag a, typename Tag::Frag b, f32x4 c);
 template <> __device__ inline f32x4 mma<TagF32>(float a, float b, f32x4 c) {
@@ -112,82 +120,124 @@ template <> __device__ inline f32x4 mma<TagF16>(u16x8 a, u16x8 b, f32x4 c) {
                                                 __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
 }
 
-// Element u of a 16-byte chunk held as uint4.
-template <int ES> __device__ inline uint32_t chunk_elem(const uint4 &v, int u);
-template <> __device__ inline uint32_t chunk_elem<4>(const uint4 &v, int u) {
-  return u == 0 ? v.x : u == 1 ? v.y : u == 2 ? v.z : v.w;
-}
-template <> __device__ inline uint32_t chunk_elem<2>(const uint4 &v, int u) {
-  const uint32_t d = (u >> 1) == 0 ? v.x : (u >> 1) == 1 ? v.y : (u >> 1) == 2 ? v.z : v.w;
-  return (u & 1) ? (d >> 16) : (d & 0xffffu);
+// floor(v / d) for 0 <= v, d < 2^24 from a float reciprocal, corrected.
+__device__ inline int fdiv(int v, int d, float inv) {
+  int q = (int)((float)v * inv);
+  if (q * d > v) --q;
+  else if ((q + 1) * d <= v) ++q;
+  return q;
 }
 
 // ------------------------------------------------------------- geometry
 
 struct KArgs {
   int64_t B, C, H, W;
-  int64_t NH, NW, N;
-  int64_t tile;          // windows per workgroup tile (forward) / per slab (dtable)
-  int64_t tiles_per_ch;  // tiles (slabs) per channel
-  int dense;             // H and W are multiples of w
+  int NH, NW;
+  int64_t N;           // windows per channel, B * NH * NW
+  int tile;            // windows per workgroup tile (forward) / per slab (dtable)
+  int tiles_per_ch;    // workgroups per channel
+  float inv_nw, inv_nhw;
 };
 
-// One aligned 16-byte chunk of a band.  The band of window-row index bi of
-// channel c covers image rows [wy*w, wy*w + rows) of plane (b, c); it is
-// contiguous in NCHW.  Chunk ci of the band starts at the 16-byte boundary at
-// or below the band start.  On success: ca = chunk address, elements [u0, u1)
-// of the chunk belong to the band, and (r, x) = band row / image column of
-// element u0.
+// A window row: element offset (from the tensor base) of its first element,
+// number of columns inside the image (0: the row lies outside the image or the
+// window does not exist), and whether it can move as dwords.
 template <int WIN, int ES>
-__device__ inline bool band_chunk(const KArgs &a, int64_t c, int64_t bi, int ci, uintptr_t base,
-                                  uintptr_t &ca, int &u0, int &u1, int &r, int &x) {
-  constexpr int VE = 16 / ES;
-  const int64_t b = bi / a.NH;
-  const int64_t wy = bi - b * a.NH;
-  const int64_t rows64 = a.H - wy * WIN;
-  const int rows = rows64 < WIN ? (int)rows64 : WIN;
-  const int64_t estart = ((b * a.C + c) * a.H + wy * WIN) * a.W;
-  const int64_t elen = (int64_t)rows * a.W;
-  const uintptr_t bs = base + (uintptr_t)(estart * ES);
-  const uintptr_t be = bs + (uintptr_t)(elen * ES);
-  ca = (bs & ~(uintptr_t)15) + (uintptr_t)ci * 16u;
-  if (ca >= be) return false;
-  const int64_t e_ca = ((int64_t)ca - (int64_t)bs) / ES;  // may be negative
-  u0 = e_ca < 0 ? (int)(-e_ca) : 0;
-  const int64_t rem = elen - e_ca;
-  u1 = rem < VE ? (int)rem : VE;
-  const int e0 = (int)(e_ca + u0);
-  const int Wi = (int)a.W;
-  r = e0 / Wi;
-  x = e0 - r * Wi;
-  return true;
-}
+struct Row {
+  int64_t eoff;
+  int cols;
+  bool fast;
+};
 
 template <int WIN, int ES>
-__device__ inline int chunks_per_band(const KArgs &a) {
-  return (int)((WIN * a.W * ES) / 16) + 2;
+__device__ inline Row<WIN, ES> row_of(const KArgs &a, const void *base, int64_t c, int64_t n, int hi) {
+  Row<WIN, ES> r;
+  r.eoff = 0;
+  r.cols = 0;
+  r.fast = false;
+  if (n >= a.N || hi >= WIN) return r;
+  const int nhw = a.NH * a.NW;
+  const int b = fdiv((int)n, nhw, a.inv_nhw);
+  const int rem = (int)n - b * nhw;
+  const int wy = fdiv(rem, a.NW, a.inv_nw);
+  const int wx = rem - wy * a.NW;
+  const int64_t h = (int64_t)wy * WIN + hi;
+  if (h >= a.H) return r;
+  const int64_t cw = a.W - (int64_t)wx * WIN;
+  r.cols = cw < WIN ? (int)cw : WIN;
+  r.eoff = (((int64_t)b * a.C + c) * a.H + h) * a.W + (int64_t)wx * WIN;
+  r.fast = r.cols == WIN && ((WIN * ES) & 3) == 0 &&
+           (((reinterpret_cast<uintptr_t>(base) + (uint64_t)r.eoff * ES) & 3u) == 0);
+  return r;
 }
 
-// Load a chunk: whole-vector when the chunk lies inside the band, otherwise
-// only the band's elements.
-template <int ES>
-__device__ inline uint4 load_chunk(uintptr_t ca, int u0, int u1) {
-  constexpr int VE = 16 / ES;
-  if (u0 == 0 && u1 == VE) return *reinterpret_cast<const uint4 *>(ca);
-  uint4 v = make_uint4(0, 0, 0, 0);
-  uint32_t w4[4] = {0, 0, 0, 0};
+// Dwords of one padded row (RP elements) in registers.
+template <int WIN, int ES>
+struct RowData {
+  static constexpr int RP = rp_of(WIN);
+  static constexpr int ND = RP * ES / 4;  // dwords per padded row
+  uint32_t d[ND];
+};
+
+// Load a window row: columns >= cols and padded columns read as zero.
+template <int WIN, int ES>
+__device__ inline void load_row(const void *base, const Row<WIN, ES> &r, RowData<WIN, ES> &o) {
+  constexpr int ND = RowData<WIN, ES>::ND;
+  constexpr int NDV = (WIN * ES) / 4;  // data dwords of a whole row (fast path)
 #pragma unroll
-  for (int u = 0; u < VE; ++u) {
-    if (u >= u0 && u < u1) {
-      uint32_t e;
-      if (ES == 4) e = *reinterpret_cast<const uint32_t *>(ca + 4 * u);
-      else e = *reinterpret_cast<const u16 *>(ca + 2 * u);
-      if (ES == 4) w4[u] = e;
-      else w4[u >> 1] |= (u & 1) ? (e << 16) : e;
+  for (int i = 0; i < ND; ++i) o.d[i] = 0;
+  if (r.cols == 0) return;
+  const char *p = reinterpret_cast<const char *>(base) + r.eoff * ES;
+  if (r.fast) {
+    const uint32_t *p4 = reinterpret_cast<const uint32_t *>(p);
+#pragma unroll
+    for (int i = 0; i + 4 <= NDV; i += 4) {
+      const u32x4a v = *reinterpret_cast<const u32x4a *>(p4 + i);
+      o.d[i] = v.x; o.d[i + 1] = v.y; o.d[i + 2] = v.z; o.d[i + 3] = v.w;
+    }
+#pragma unroll
+    for (int i = NDV & ~3; i < NDV; ++i) o.d[i] = p4[i];
+  } else {
+    // branch-free: element x reads column min(x, cols - 1), which is inside
+    // the row, and is then zeroed when x >= cols
+    const int last = r.cols - 1;
+#pragma unroll
+    for (int x = 0; x < WIN; ++x) {
+      const int xc = x < last ? x : last;
+      if (ES == 4) {
+        const uint32_t e = reinterpret_cast<const uint32_t *>(p)[xc];
+        o.d[x] = x < r.cols ? e : 0u;
+      } else {
+        const uint32_t e = reinterpret_cast<const u16 *>(p)[xc];
+        const uint32_t m = x < r.cols ? e : 0u;
+        o.d[x >> 1] |= (x & 1) ? (m << 16) : m;
+      }
     }
   }
-  v.x = w4[0]; v.y = w4[1]; v.z = w4[2]; v.w = w4[3];
-  return v;
+}
+
+// Store the first cols elements of a padded row held as dwords.
+template <int WIN, int ES>
+__device__ inline void store_row(void *base, const Row<WIN, ES> &r, const uint32_t *d) {
+  constexpr int NDV = (WIN * ES) / 4;
+  if (r.cols == 0) return;
+  char *p = reinterpret_cast<char *>(base) + r.eoff * ES;
+  if (r.fast) {
+    uint32_t *p4 = reinterpret_cast<uint32_t *>(p);
+#pragma unroll
+    for (int i = 0; i + 4 <= NDV; i += 4)
+      *reinterpret_cast<u32x4a *>(p4 + i) = u32x4a{d[i], d[i + 1], d[i + 2], d[i + 3]};
+#pragma unroll
+    for (int i = NDV & ~3; i < NDV; ++i) p4[i] = d[i];
+  } else {
+#pragma unroll
+    for (int x = 0; x < WIN; ++x) {
+      if (x < r.cols) {
+        if (ES == 4) reinterpret_cast<uint32_t *>(p)[x] = d[x];
+        else reinterpret_cast<u16 *>(p)[x] = (u16)((x & 1) ? (d[x >> 1] >> 16) : (d[x >> 1] & 0xffffu));
+      }
+    }
+  }
 }
 
 // ======================================================= forward kernel
@@ -197,6 +247,7 @@ struct FwdCfg {
   static constexpr int RP = rp_of(WIN);
   static constexpr int PP = WIN * RP;                 // padded positions
   static constexpr int KP = rup(PP, Tag::KS);         // padded K
+  static constexpr int KR = KP / RP;                  // padded rows per window
   static constexpr int S = KP / Tag::KS;              // K steps
   static constexpr int NT = cdiv(PP, 16);             // 16-wide output tiles
   static constexpr int NB = 2 * S + NT - 2;           // distinct B fragments (16-bit)
@@ -210,7 +261,7 @@ struct FwdCfg {
 };
 
 template <class Tag, int WIN>
-__host__ __device__ constexpr size_t fwd_lds_bytes(int64_t tile) {
+__host__ __device__ constexpr size_t fwd_lds_bytes(int tile) {
   typedef FwdCfg<Tag, WIN> G;
   return (size_t)tile * G::LDSW * Tag::ES + (size_t)(G::TS_LEN + G::TB_LEN) * Tag::ES;
 }
@@ -222,8 +273,8 @@ __global__ __launch_bounds__(kThreads) void wbmm_fwd_kernel(const typename Tag::
   typedef typename Tag::S S;
   typedef typename Tag::Frag Frag;
   typedef FwdCfg<Tag, WIN> G;
-  constexpr int RP = G::RP, KP = G::KP, LDSW = G::LDSW, K1 = G::K1, K2 = G::K2;
-  constexpr int VE = 16 / Tag::ES;
+  typedef RowData<WIN, Tag::ES> RD;
+  constexpr int RP = G::RP, KR = G::KR, LDSW = G::LDSW, K1 = G::K1, K2 = G::K2, ES = Tag::ES;
 
   extern __shared__ __align__(16) unsigned char smem[];
   S *tile = reinterpret_cast<S *>(smem);
@@ -234,95 +285,47 @@ __global__ __launch_bounds__(kThreads) void wbmm_fwd_kernel(const typename Tag::
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int64_t c = blockIdx.x / a.tiles_per_ch;
-  const int64_t tix = blockIdx.x - c * a.tiles_per_ch;
-  const int64_t n0 = tix * a.tile;
-  const int64_t n1 = (n0 + a.tile < a.N) ? n0 + a.tile : a.N;
-  const int nwin = (int)(n1 - n0);
+  const int64_t n0 = (int64_t)(blockIdx.x - c * a.tiles_per_ch) * a.tile;
+  const int nwin = (int)((n0 + a.tile <= a.N) ? a.tile : a.N - n0);
 
-  // ---- 1. zero what the scatter will not write; stage the table
-  const bool full = a.dense && nwin == a.tile;
-  if (!full) {
-    uint4 *t4 = reinterpret_cast<uint4 *>(tile);
-    const int n16 = (int)((a.tile * LDSW * Tag::ES) / 16);
-    for (int i = tid; i < n16; i += kThreads) t4[i] = make_uint4(0, 0, 0, 0);
-  } else {
-    constexpr int PADS = KP - WIN * WIN;  // padded slots per window
-    constexpr int PADC = RP - WIN;        // padded columns per row
-    if constexpr (PADS > 0) {
-      for (int i = tid; i < nwin * PADS; i += kThreads) {
-        const int v = i / PADS;
-        const int q = i - v * PADS;
-        int p;
-        if constexpr (PADC > 0) {
-          if (q < WIN * PADC) {
-            const int h = q / PADC;
-            p = h * RP + WIN + (q - h * PADC);
-          } else {
-            p = WIN * RP + (q - WIN * PADC);
-          }
-        } else {
-          p = WIN * RP + q;
-        }
-        tile[v * LDSW + p] = (S)0;
-      }
-    }
-  }
+  // ---- 1. table -> LDS; rows -> window-major LDS tile (padding included)
   for (int k = tid; k < K2; k += kThreads) Ts[k] = tab[c * K2 + (REV ? K2 - 1 - k : k)];
-  if (!full) __syncthreads();
-
-  // ---- 2. scatter the X tile: bands -> window-major LDS
   {
-    const int64_t bi0 = n0 / a.NW, bi1 = (n1 - 1) / a.NW;
-    const int nb = (int)(bi1 - bi0 + 1);
-    const int cpb = chunks_per_band<WIN, Tag::ES>(a);
-    const int total = nb * cpb;
-    const uintptr_t xb = reinterpret_cast<uintptr_t>(x);
+    const int nrows = nwin * KR;
     constexpr int U = 4;
-    for (int s0 = tid; s0 < total; s0 += kThreads * U) {
-      uint4 v[U];
-      uintptr_t ca[U];
-      int u0[U], u1[U], r[U], xx[U];
-      bool ok[U];
-      int64_t bi[U];
+    for (int q0 = tid; q0 < nrows; q0 += kThreads * U) {
+      RD rd[U];
+      int dst[U];
 #pragma unroll
       for (int k = 0; k < U; ++k) {
-        const int slot = s0 + k * kThreads;
-        ok[k] = false;
-        if (slot < total) {
-          const int bl = slot / cpb;
-          const int ci = slot - bl * cpb;
-          bi[k] = bi0 + bl;
-          ok[k] = band_chunk<WIN, Tag::ES>(a, c, bi[k], ci, xb, ca[k], u0[k], u1[k], r[k], xx[k]);
-          if (ok[k]) v[k] = load_chunk<Tag::ES>(ca[k], u0[k], u1[k]);
+        const int q = q0 + k * kThreads;
+        dst[k] = -1;
+        if (q < nrows) {
+          const int v = q / KR;  // rows of one window are consecutive
+          const int hi = q - v * KR;
+          const Row<WIN, ES> r = row_of<WIN, ES>(a, x, c, n0 + v, hi);
+          load_row<WIN, ES>(x, r, rd[k]);
+          dst[k] = (v * LDSW + hi * RP) * ES;
         }
       }
 #pragma unroll
       for (int k = 0; k < U; ++k) {
-        if (!ok[k]) continue;
-        int rr = r[k], cx = xx[k];
+        if (dst[k] < 0) continue;
+        uint32_t *l4 = reinterpret_cast<uint32_t *>(smem + dst[k]);
 #pragma unroll
-        for (int u = 0; u < VE; ++u) {
-          if (u >= u0[k] && u < u1[k]) {
-            const int wx = cx / WIN;
-            const int xi = cx - wx * WIN;
-            const int64_t n = bi[k] * a.NW + wx;
-            if (n >= n0 && n < n1) {
-              const uint32_t e = chunk_elem<Tag::ES>(v[k], u);
-              S val;
-              if constexpr (Tag::ES == 4) val = __uint_as_float(e);
-              else val = (u16)e;
-              tile[(int)(n - n0) * LDSW + rr * RP + xi] = val;
-            }
-            if (++cx == (int)a.W) { cx = 0; ++rr; }
-          }
-        }
+        for (int i = 0; i < RD::ND; i += 4)
+          *reinterpret_cast<uint4 *>(l4 + i) = make_uint4(rd[k].d[i], rd[k].d[i + 1], rd[k].d[i + 2], rd[k].d[i + 3]);
       }
     }
   }
   __syncthreads();
 
-  // ---- 3. Toeplitz blocks of M_c (16-bit path): TB[dh][x_out][x_in]
+  const int g = lane >> 4;   // lane group
+  const int ln = lane & 15;  // row (A) / column (B, C) inside a 16x16 tile
+  const int nsub = (nwin + 15) >> 4;
   if constexpr (Tag::W16) {
+    constexpr int S_ = G::S, NT = G::NT, NB = G::NB;
+    // ---- 2. Toeplitz blocks of M_c: TB[dh][x_out][x_in]
     for (int i = tid; i < G::TB_LEN; i += kThreads) {
       const int dhi = i / (RP * RP);
       const int rem = i - dhi * RP * RP;
@@ -331,13 +334,7 @@ __global__ __launch_bounds__(kThreads) void wbmm_fwd_kernel(const typename Tag::
       TB[i] = (xo < WIN && xi < WIN) ? Ts[dhi * K1 + xi - xo + WIN - 1] : (S)0;
     }
     __syncthreads();
-  }
-
-  // ---- 4. matrix-core products, 16 windows at a time per wave
-  const int g = lane >> 4;   // lane group
-  const int ln = lane & 15;  // row (A) / column (B, C) inside a 16x16 tile
-  if constexpr (Tag::W16) {
-    constexpr int S_ = G::S, NT = G::NT, NB = G::NB;
+    // ---- 3. the distinct B fragments, in registers
     Frag bf[NB];
 #pragma unroll
     for (int q = 0; q < NB; ++q) {
@@ -351,103 +348,73 @@ __global__ __launch_bounds__(kThreads) void wbmm_fwd_kernel(const typename Tag::
       else
         bf[q] = Frag{0, 0, 0, 0, 0, 0, 0, 0};
     }
-    const int nsub = (nwin + 15) >> 4;
+    // ---- 4. 16-window sub-tiles: A fragments, products, rounded results
     for (int sub = wave; sub < nsub; sub += kWaves) {
       S *rowp = tile + (sub * 16) * LDSW;
       Frag af[S_];
 #pragma unroll
       for (int s = 0; s < S_; ++s)
         af[s] = *reinterpret_cast<const Frag *>(&rowp[ln * LDSW + s * 32 + 8 * g]);
+      S *outp = rowp + (4 * g) * LDSW + ln;
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int s = 0; s < S_; ++s) acc = mma<Tag>(af[s], bf[2 * s - t + NT - 1], acc);
-        const int p = 16 * t + ln;
-        const int ho = p / RP, xo = p - (p / RP) * RP;
-        if (ho < WIN && xo < WIN) {
-#pragma unroll
-          for (int rr = 0; rr < 4; ++rr) rowp[(4 * g + rr) * LDSW + p] = from_f32<Tag>(acc[rr]);
-        }
+        const uint32_t lo = pack2<Tag>(acc[0], acc[1]);
+        const uint32_t hi = pack2<Tag>(acc[2], acc[3]);
+        outp[0 * LDSW + 16 * t] = (u16)(lo & 0xffffu);
+        outp[1 * LDSW + 16 * t] = (u16)(lo >> 16);
+        outp[2 * LDSW + 16 * t] = (u16)(hi & 0xffffu);
+        outp[3 * LDSW + 16 * t] = (u16)(hi >> 16);
       }
     }
   } else {
     constexpr int S_ = G::S, NT = G::NT;
-    const int nsub = (nwin + 15) >> 4;
     for (int sub = wave; sub < nsub; sub += kWaves) {
       S *rowp = tile + (sub * 16) * LDSW;
       float af[S_];
 #pragma unroll
       for (int s = 0; s < S_; ++s) af[s] = rowp[ln * LDSW + 4 * s + g];
+      S *outp = rowp + (4 * g) * LDSW + ln;
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
         const int pn = 16 * t + ln;
-        const int ho = pn / RP, xo = pn - (pn / RP) * RP;
+        const int ho = pn / RP, xo = pn % RP;
 #pragma unroll
         for (int s = 0; s < S_; ++s) {
           const int k = 4 * s + g;
-          const int hi = k / RP, xi = k - (k / RP) * RP;
+          const int hi = k / RP, xi = k % RP;
           const int dh = hi - ho;
           float bv = 0.f;
           if (xo < WIN && xi < WIN && dh >= -(WIN - 1) && dh <= WIN - 1)
             bv = Ts[(dh + WIN - 1) * K1 + xi - xo + WIN - 1];
           acc = mma<Tag>(af[s], bv, acc);
         }
-        if (ho < WIN && xo < WIN) {
 #pragma unroll
-          for (int rr = 0; rr < 4; ++rr) rowp[(4 * g + rr) * LDSW + pn] = acc[rr];
-        }
+        for (int rr = 0; rr < 4; ++rr) outp[rr * LDSW + 16 * t] = acc[rr];
       }
     }
   }
   __syncthreads();
 
-  // ---- 5. store the Y tile: window-major LDS -> bands
+  // ---- 5. window-major LDS tile -> global rows
   {
-    const int64_t bi0 = n0 / a.NW, bi1 = (n1 - 1) / a.NW;
-    const int nb = (int)(bi1 - bi0 + 1);
-    const int cpb = chunks_per_band<WIN, Tag::ES>(a);
-    const int total = nb * cpb;
-    const uintptr_t yb = reinterpret_cast<uintptr_t>(y);
-    for (int slot = tid; slot < total; slot += kThreads) {
-      const int bl = slot / cpb;
-      const int ci = slot - bl * cpb;
-      const int64_t bi = bi0 + bl;
-      uintptr_t ca;
-      int u0, u1, rr, cx;
-      if (!band_chunk<WIN, Tag::ES>(a, c, bi, ci, yb, ca, u0, u1, rr, cx)) continue;
-      uint32_t w4[4] = {0, 0, 0, 0};
-      int mask = 0;
+    const int nrows = nwin * WIN;
+    for (int q = tid; q < nrows; q += kThreads) {
+      const int v = q / WIN;
+      const int hi = q - v * WIN;
+      const Row<WIN, ES> r = row_of<WIN, ES>(a, y, c, n0 + v, hi);
+      if (r.cols == 0) continue;
+      const uint32_t *l4 = reinterpret_cast<const uint32_t *>(smem + (v * LDSW + hi * RP) * ES);
+      uint32_t d[RD::ND];
 #pragma unroll
-      for (int u = 0; u < VE; ++u) {
-        if (u >= u0 && u < u1) {
-          const int wx = cx / WIN;
-          const int xi = cx - wx * WIN;
-          const int64_t n = bi * a.NW + wx;
-          if (n >= n0 && n < n1) {
-            const S val = tile[(int)(n - n0) * LDSW + rr * RP + xi];
-            uint32_t e;
-            if constexpr (Tag::ES == 4) e = __float_as_uint(val);
-            else e = (uint32_t)val;
-            if (Tag::ES == 4) w4[u] = e;
-            else w4[u >> 1] |= (u & 1) ? (e << 16) : e;
-            mask |= 1 << u;
-          }
-          if (++cx == (int)a.W) { cx = 0; ++rr; }
-        }
+      for (int i = 0; i < RD::ND; i += 4) {
+        const uint4 u = *reinterpret_cast<const uint4 *>(l4 + i);
+        d[i] = u.x; d[i + 1] = u.y; d[i + 2] = u.z; d[i + 3] = u.w;
       }
-      if (mask == (1 << VE) - 1) {
-        *reinterpret_cast<uint4 *>(ca) = make_uint4(w4[0], w4[1], w4[2], w4[3]);
-      } else {
-#pragma unroll
-        for (int u = 0; u < VE; ++u) {
-          if (mask & (1 << u)) {
-            if (Tag::ES == 4) *reinterpret_cast<uint32_t *>(ca + 4 * u) = w4[u];
-            else *reinterpret_cast<u16 *>(ca + 2 * u) = (u16)((u & 1) ? (w4[u >> 1] >> 16) : (w4[u >> 1] & 0xffffu));
-          }
-        }
-      }
+      store_row<WIN, ES>(y, r, d);
     }
   }
 }
@@ -461,117 +428,143 @@ struct DtCfg {
   static constexpr int NPT = cdiv(PP, 16);        // 16-position tiles
   static constexpr int KPT = NPT * 16;            // padded positions
   static constexpr int R = 16 / RP;               // window rows per tile
-  static constexpr int CW = Tag::W16 ? 32 : 16;   // windows per LDS chunk
-  static constexpr int CWS = Tag::W16 ? CW + 8 : CW + 4;  // row stride (elements)
+  static constexpr int CW = Tag::W16 ? 32 : 16;   // windows per LDS stage
+  static constexpr int CWS = Tag::W16 ? CW + 8 : CW + 4;  // position row stride (elements)
+  // bytes of one position row plus a 16-byte shift per window row, so the w
+  // strided stores of a row copy from different window rows hit other banks
+  static constexpr int PB = CWS * Tag::ES;
+  static constexpr int BUF = KPT * PB + (KPT / RP) * 16;  // bytes per operand buffer
   static constexpr int NACC = 2 * NPT - 1;        // accumulators: pi - po
   static constexpr int K1 = 2 * WIN - 1;
   static constexpr int K2 = K1 * K1;
   static constexpr int NBT = (2 * R - 1) * K1;    // bins per accumulator tile
-  static constexpr int BUF = KPT * CWS;           // elements per operand buffer
+  static constexpr int ROWS = 2 * CW * WIN;       // row copies per stage (x and dy)
+  static constexpr int RPT = cdiv(ROWS, kThreads);  // row copies per thread
 };
 
-// Accumulator tiles are assigned to waves by longest-processing-time: tile P
-// (= pi - po) carries NPT - |P| block products per K step.
-template <int NPT>
-struct PAssign {
-  int count[kWaves];
-  int list[kWaves][2 * NPT - 1];
+// Byte offset of (position p, window v) in a position-major operand buffer.
+template <class Tag, int WIN>
+__device__ __host__ constexpr int dt_off(int p, int v) {
+  typedef DtCfg<Tag, WIN> G;
+  return p * G::PB + (p / G::RP) * 16 + v * Tag::ES;
+}
+
+// Accumulator tiles are split among the waves in contiguous ranges of
+// P = pi - po (tile P carries NPT - |P| block products per K step), the
+// ranges chosen to balance that work.  With a contiguous range, the B
+// fragment of output tile po is live only while pi runs over po + [lo, hi].
+struct PRange {
+  int lo[kWaves];
+  int hi[kWaves];
 };
 
 template <int NPT>
-__host__ __device__ constexpr PAssign<NPT> make_passign() {
-  PAssign<NPT> pa{};
-  int load[kWaves] = {0, 0, 0, 0};
-  for (int w = 0; w < kWaves; ++w) pa.count[w] = 0;
-  // work NPT - |P|, P = 0, 1, -1, 2, -2, ...: already in non-increasing work order
-  for (int i = 0; i < 2 * NPT - 1; ++i) {
-    const int P = (i & 1) ? (i + 1) / 2 : -(i / 2);
-    int best = 0;
-    for (int w = 1; w < kWaves; ++w)
-      if (load[w] < load[best] || (load[w] == load[best] && pa.count[w] < pa.count[best])) best = w;
-    pa.list[best][pa.count[best]++] = P + NPT - 1;
-    load[best] += NPT - (P < 0 ? -P : P);
+__host__ __device__ constexpr PRange make_prange() {
+  constexpr int n = 2 * NPT - 1;  // P = -(NPT-1) .. NPT-1
+  int work[n] = {};
+  for (int i = 0; i < n; ++i) {
+    const int P = i - (NPT - 1);
+    work[i] = NPT - (P < 0 ? -P : P);
   }
-  return pa;
+  int pre[n + 1] = {};
+  for (int i = 0; i < n; ++i) pre[i + 1] = pre[i] + work[i];
+  // cut points 0 <= c1 <= c2 <= c3 <= n minimising the largest share
+  int best = 1 << 30, b1 = 0, b2 = 0, b3 = 0;
+  for (int c1 = 0; c1 <= n; ++c1)
+    for (int c2 = c1; c2 <= n; ++c2)
+      for (int c3 = c2; c3 <= n; ++c3) {
+        int m = pre[c1];
+        if (pre[c2] - pre[c1] > m) m = pre[c2] - pre[c1];
+        if (pre[c3] - pre[c2] > m) m = pre[c3] - pre[c2];
+        if (pre[n] - pre[c3] > m) m = pre[n] - pre[c3];
+        if (m < best) { best = m; b1 = c1; b2 = c2; b3 = c3; }
+      }
+  PRange r{};
+  const int cut[kWaves + 1] = {0, b1, b2, b3, n};
+  for (int w = 0; w < kWaves; ++w) {
+    r.lo[w] = cut[w] - (NPT - 1);
+    r.hi[w] = cut[w + 1] - 1 - (NPT - 1);  // hi < lo: the wave owns nothing
+  }
+  return r;
 }
 
 template <class Tag, int WIN>
 __host__ __device__ constexpr size_t dt_lds_bytes() {
   typedef DtCfg<Tag, WIN> G;
-  const size_t ops = 2 * (size_t)G::BUF * Tag::ES;
+  const size_t ops = 2 * (size_t)G::BUF;
   const size_t bins = (size_t)(kWaves * 16 * 17 + G::NACC * G::NBT) * 4;
   return ops > bins ? ops : bins;
 }
 
-// Scatter one chunk of windows [m0, m1) of channel c from tensor `src` into
-// the position-major buffer dst[p * CWS + (n - m0)].
+// Row copies of one stage: task q covers tensor (q / (CW * WIN)), window
+// (q / WIN) % CW of the stage and window row q % WIN.
 template <class Tag, int WIN>
-__device__ inline void dt_scatter(const KArgs &a, int64_t c, int64_t m0, int64_t m1,
-                                  uintptr_t src, typename Tag::S *dst, int tid) {
-  typedef typename Tag::S S;
+struct DtStage {
   typedef DtCfg<Tag, WIN> G;
-  constexpr int RP = G::RP, CWS = G::CWS;
-  constexpr int VE = 16 / Tag::ES;
-  const int64_t bi0 = m0 / a.NW, bi1 = (m1 - 1) / a.NW;
-  const int nb = (int)(bi1 - bi0 + 1);
-  const int cpb = chunks_per_band<WIN, Tag::ES>(a);
-  const int total = nb * cpb;
-  constexpr int U = 4;
-  for (int s0 = tid; s0 < total; s0 += kThreads * U) {
-    uint4 v[U];
-    uintptr_t ca[U];
-    int u0[U], u1[U], r[U], xx[U];
-    bool ok[U];
-    int64_t bi[U];
+  RowData<WIN, Tag::ES> rd[G::RPT];
+};
+
+template <class Tag, int WIN>
+__device__ inline void dt_load_stage(const KArgs &a, const void *x, const void *dy, int64_t c, int64_t m0,
+                                     int64_t m1, int tid, DtStage<Tag, WIN> &st) {
+  typedef DtCfg<Tag, WIN> G;
 #pragma unroll
-    for (int k = 0; k < U; ++k) {
-      const int slot = s0 + k * kThreads;
-      ok[k] = false;
-      if (slot < total) {
-        const int bl = slot / cpb;
-        const int ci = slot - bl * cpb;
-        bi[k] = bi0 + bl;
-        ok[k] = band_chunk<WIN, Tag::ES>(a, c, bi[k], ci, src, ca[k], u0[k], u1[k], r[k], xx[k]);
-        if (ok[k]) v[k] = load_chunk<Tag::ES>(ca[k], u0[k], u1[k]);
-      }
-    }
+  for (int k = 0; k < G::RPT; ++k) {
+    const int q = tid + k * kThreads;
+    const int tens = q / (G::CW * WIN);
+    const int rem = q - tens * (G::CW * WIN);
+    const int v = rem / WIN;
+    const int hi = rem - v * WIN;
+    const void *src = tens ? dy : x;
+    Row<WIN, Tag::ES> r;
+    r.cols = 0; r.eoff = 0; r.fast = false;
+    if (q < G::ROWS && m0 + v < m1) r = row_of<WIN, Tag::ES>(a, src, c, m0 + v, hi);
+    load_row<WIN, Tag::ES>(src, r, st.rd[k]);
+  }
+}
+
+// Write a loaded stage position-major: element x of row hi of window v goes to
+// (p = hi * RP + x, v).  Positions past the window (x >= w, rows >= w) are
+// never written and stay zero from the initial clear.
+template <class Tag, int WIN>
+__device__ inline void dt_write_stage(unsigned char *smem, int tid, const DtStage<Tag, WIN> &st) {
+  typedef DtCfg<Tag, WIN> G;
+  constexpr int RP = G::RP;
 #pragma unroll
-    for (int k = 0; k < U; ++k) {
-      if (!ok[k]) continue;
-      int rr = r[k], cx = xx[k];
+  for (int k = 0; k < G::RPT; ++k) {
+    const int q = tid + k * kThreads;
+    if (q >= G::ROWS) continue;
+    const int tens = q / (G::CW * WIN);
+    const int rem = q - tens * (G::CW * WIN);
+    const int v = rem / WIN;
+    const int hi = rem - v * WIN;
+    unsigned char *base = smem + tens * G::BUF + dt_off<Tag, WIN>(hi * RP, v);
 #pragma unroll
-      for (int u = 0; u < VE; ++u) {
-        if (u >= u0[k] && u < u1[k]) {
-          const int wx = cx / WIN;
-          const int xi = cx - wx * WIN;
-          const int64_t n = bi[k] * a.NW + wx;
-          if (n >= m0 && n < m1) {
-            const uint32_t e = chunk_elem<Tag::ES>(v[k], u);
-            S val;
-            if constexpr (Tag::ES == 4) val = __uint_as_float(e);
-            else val = (u16)e;
-            dst[(rr * RP + xi) * CWS + (int)(n - m0)] = val;
-          }
-          if (++cx == (int)a.W) { cx = 0; ++rr; }
-        }
+    for (int xi = 0; xi < WIN; ++xi) {
+      if (Tag::ES == 4) {
+        *reinterpret_cast<uint32_t *>(base + xi * G::PB) = st.rd[k].d[xi];
+      } else {
+        const uint32_t d = st.rd[k].d[xi >> 1];
+        *reinterpret_cast<u16 *>(base + xi * G::PB) = (u16)((xi & 1) ? (d >> 16) : (d & 0xffffu));
       }
     }
   }
 }
 
 template <class Tag, int WIN, int WAVE>
-__device__ void dt_wave(const typename Tag::S *__restrict__ x, const typename Tag::S *__restrict__ dy,
+__device__ __attribute__((always_inline)) void dt_wave(const typename Tag::S *__restrict__ x, const typename Tag::S *__restrict__ dy,
                         float *__restrict__ out, const KArgs &a, unsigned char *smem) {
-  typedef typename Tag::S S;
   typedef typename Tag::Frag Frag;
   typedef DtCfg<Tag, WIN> G;
-  constexpr int NPT = G::NPT, CW = G::CW, CWS = G::CWS, RP = G::RP, R = G::R;
+  constexpr int NPT = G::NPT, CW = G::CW, RP = G::RP, R = G::R;
   constexpr int K1 = G::K1, K2 = G::K2, NBT = G::NBT;
-  constexpr PAssign<NPT> PA = make_passign<NPT>();
-  constexpr int NP = PA.count[WAVE];
+  constexpr PRange PR = make_prange<NPT>();
+  constexpr int PLO = PR.lo[WAVE];
+  constexpr int NP = PR.hi[WAVE] - PR.lo[WAVE] + 1;  // may be 0
+  constexpr int PHI = PLO + NP - 1;
 
-  S *Xt = reinterpret_cast<S *>(smem);
-  S *Dt = Xt + G::BUF;
+  const unsigned char *Xt = smem;
+  const unsigned char *Dt = smem + G::BUF;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -586,66 +579,70 @@ __device__ void dt_wave(const typename Tag::S *__restrict__ x, const typename Ta
 #pragma unroll
   for (int j = 0; j < NP; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // padded slots must read as zero: clear both buffers once
+  // padded positions must read as zero: clear both buffers once
   {
     uint4 *t4 = reinterpret_cast<uint4 *>(smem);
-    const int n16 = (2 * G::BUF * Tag::ES) / 16;
-    for (int i = tid; i < n16; i += kThreads) t4[i] = make_uint4(0, 0, 0, 0);
+    for (int i = tid; i < (2 * G::BUF) / 16; i += kThreads) t4[i] = make_uint4(0, 0, 0, 0);
   }
-  __syncthreads();
+  DtStage<Tag, WIN> st;
+  dt_load_stage<Tag, WIN>(a, x, dy, c, s0, s1, tid, st);
 
   for (int64_t m0 = s0; m0 < s1; m0 += CW) {
-    const int64_t m1 = (m0 + CW < s1) ? m0 + CW : s1;
-    if (!(a.dense && m1 - m0 == CW) && m0 != s0) {
-      uint4 *t4 = reinterpret_cast<uint4 *>(smem);
-      const int n16 = (2 * G::BUF * Tag::ES) / 16;
-      for (int i = tid; i < n16; i += kThreads) t4[i] = make_uint4(0, 0, 0, 0);
-      __syncthreads();
-    }
-    dt_scatter<Tag, WIN>(a, c, m0, m1, reinterpret_cast<uintptr_t>(x), Xt, tid);
-    dt_scatter<Tag, WIN>(a, c, m0, m1, reinterpret_cast<uintptr_t>(dy), Dt, tid);
+    __syncthreads();  // previous stage consumed (first pass: clear done)
+    dt_write_stage<Tag, WIN>(smem, tid, st);
     __syncthreads();
+    if (m0 + CW < s1) dt_load_stage<Tag, WIN>(a, x, dy, c, m0 + CW, s1, tid, st);
 
-    if constexpr (Tag::W16) {
-      Frag bf[NPT];
-#pragma unroll
-      for (int po = 0; po < NPT; ++po)
-        bf[po] = *reinterpret_cast<const Frag *>(&Dt[(16 * po + ln) * CWS + 8 * g]);
-#pragma unroll
-      for (int pi = 0; pi < NPT; ++pi) {
-        const Frag af = *reinterpret_cast<const Frag *>(&Xt[(16 * pi + ln) * CWS + 8 * g]);
-#pragma unroll
-        for (int j = 0; j < NP; ++j) {
-          const int po = pi - (PA.list[WAVE][j] - (NPT - 1));
-          if (po >= 0 && po < NPT) acc[j] = mma<Tag>(af, bf[po], acc[j]);
-        }
-      }
-    } else {
-#pragma unroll
-      for (int ks = 0; ks < CW / 4; ++ks) {
-        float bf[NPT];
-#pragma unroll
-        for (int po = 0; po < NPT; ++po) bf[po] = Dt[(16 * po + ln) * CWS + 4 * ks + g];
+    if constexpr (NP > 0) {
+      if constexpr (Tag::W16) {
+        Frag bf[NPT];
 #pragma unroll
         for (int pi = 0; pi < NPT; ++pi) {
-          const float af = Xt[(16 * pi + ln) * CWS + 4 * ks + g];
+          // B fragments first needed at this pi: po with max(0, po + PLO) == pi
+#pragma unroll
+          for (int po = 0; po < NPT; ++po) {
+            const bool used = po + PHI >= 0 && po + PLO <= NPT - 1;
+            if (used && (po + PLO > 0 ? po + PLO : 0) == pi)
+              bf[po] = *reinterpret_cast<const Frag *>(Dt + dt_off<Tag, WIN>(16 * po + ln, 8 * g));
+          }
+          const Frag af = *reinterpret_cast<const Frag *>(Xt + dt_off<Tag, WIN>(16 * pi + ln, 8 * g));
 #pragma unroll
           for (int j = 0; j < NP; ++j) {
-            const int po = pi - (PA.list[WAVE][j] - (NPT - 1));
+            const int po = pi - (PLO + j);
             if (po >= 0 && po < NPT) acc[j] = mma<Tag>(af, bf[po], acc[j]);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int ks = 0; ks < CW / 4; ++ks) {
+          float bf[NPT];
+#pragma unroll
+          for (int pi = 0; pi < NPT; ++pi) {
+#pragma unroll
+            for (int po = 0; po < NPT; ++po) {
+              const bool used = po + PHI >= 0 && po + PLO <= NPT - 1;
+              if (used && (po + PLO > 0 ? po + PLO : 0) == pi)
+                bf[po] = *reinterpret_cast<const float *>(Dt + dt_off<Tag, WIN>(16 * po + ln, 4 * ks + g));
+            }
+            const float af = *reinterpret_cast<const float *>(Xt + dt_off<Tag, WIN>(16 * pi + ln, 4 * ks + g));
+#pragma unroll
+            for (int j = 0; j < NP; ++j) {
+              const int po = pi - (PLO + j);
+              if (po >= 0 && po < NPT) acc[j] = mma<Tag>(af, bf[po], acc[j]);
+            }
           }
         }
       }
     }
-    __syncthreads();
   }
+  __syncthreads();
 
   // ---- diagonal binning, fixed order
   float *scr = reinterpret_cast<float *>(smem) + WAVE * 16 * 17;
   float *binsum = reinterpret_cast<float *>(smem) + kWaves * 16 * 17;
 #pragma unroll
   for (int j = 0; j < NP; ++j) {
-    const int pidx = PA.list[WAVE][j];
+    const int pidx = PLO + j + NPT - 1;
 #pragma unroll
     for (int rr = 0; rr < 4; ++rr) scr[(4 * g + rr) * 17 + ln] = acc[j][rr];
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -717,21 +714,20 @@ static int64_t cdiv64(int64_t a, int64_t b) { return (a + b - 1) / b; }
 static KArgs make_args(const Geom &g) {
   KArgs a;
   a.B = g.B; a.C = g.C; a.H = g.H; a.W = g.W;
-  a.NH = g.NH; a.NW = g.NW; a.N = g.N;
+  a.NH = (int)g.NH; a.NW = (int)g.NW; a.N = g.N;
   a.tile = 0; a.tiles_per_ch = 0;
-  a.dense = (g.H % g.w == 0) && (g.W % g.w == 0);
+  a.inv_nw = 1.0f / (float)g.NW;
+  a.inv_nhw = 1.0f / (float)(g.NH * g.NW);
   return a;
 }
 
 static constexpr size_t kLdsBudget = 64 * 1024;
 
 template <class Tag, int WIN>
-static int64_t pick_fwd_tile(const Geom &g) {
-  int64_t tile = rp_of(WIN) == 8 ? 128 : 64;
-  if (!Tag::W16) tile = rp_of(WIN) == 8 ? 64 : 32;
+static int pick_fwd_tile(const Geom &g) {
+  int tile = rp_of(WIN) == 8 ? 128 : 64;
   while (tile > 16 && fwd_lds_bytes<Tag, WIN>(tile) > kLdsBudget) tile /= 2;
-  // keep enough workgroups to cover 256 compute units several times over
-  while (tile > (Tag::W16 ? 64 : 16) && g.C * cdiv64(g.N, tile) < 1024) tile /= 2;
+  while (tile > 64 && g.C * cdiv64(g.N, tile) < 1024) tile /= 2;
   return tile;
 }
 
@@ -741,15 +737,13 @@ static hipError_t run_forward(const void *x, const void *t, void *y, const Geom 
   typedef typename Tag::S S;
   KArgs a = make_args(g);
   a.tile = pick_fwd_tile<Tag, WIN>(g);
-  a.tiles_per_ch = cdiv64(g.N, a.tile);
-  const int64_t grid = g.C * a.tiles_per_ch;
+  a.tiles_per_ch = (int)cdiv64(g.N, a.tile);
+  const dim3 grid((unsigned)(g.C * a.tiles_per_ch));
   const size_t lds = fwd_lds_bytes<Tag, WIN>(a.tile);
   if (rev)
-    wbmm_fwd_kernel<Tag, WIN, true><<<dim3((unsigned)grid), dim3(kThreads), lds, st>>>(
-        (const S *)x, (const S *)t, (S *)y, a);
+    wbmm_fwd_kernel<Tag, WIN, true><<<grid, dim3(kThreads), lds, st>>>((const S *)x, (const S *)t, (S *)y, a);
   else
-    wbmm_fwd_kernel<Tag, WIN, false><<<dim3((unsigned)grid), dim3(kThreads), lds, st>>>(
-        (const S *)x, (const S *)t, (S *)y, a);
+    wbmm_fwd_kernel<Tag, WIN, false><<<grid, dim3(kThreads), lds, st>>>((const S *)x, (const S *)t, (S *)y, a);
   return hipGetLastError();
 }
 
@@ -757,9 +751,9 @@ template <class Tag, int WIN>
 static DtPlan plan_dt(const Geom &g) {
   typedef DtCfg<Tag, WIN> G;
   DtPlan p;
-  const int64_t chunks = cdiv64(g.N, G::CW);
+  const int64_t stages = cdiv64(g.N, G::CW);
   int64_t slabs = cdiv64(1024, g.C);
-  if (slabs > chunks) slabs = chunks;
+  if (slabs > stages) slabs = stages;
   if (slabs < 1) slabs = 1;
   p.slab_windows = cdiv64(cdiv64(g.N, slabs), G::CW) * G::CW;
   p.slabs = cdiv64(g.N, p.slab_windows);
@@ -773,8 +767,8 @@ static hipError_t run_dtable(const void *x, const void *dy, float *dt, void *ws,
   typedef DtCfg<Tag, WIN> G;
   KArgs a = make_args(g);
   const DtPlan p = plan_dt<Tag, WIN>(g);
-  a.tile = p.slab_windows;
-  a.tiles_per_ch = p.slabs;
+  a.tile = (int)p.slab_windows;
+  a.tiles_per_ch = (int)p.slabs;
   float *out = p.slabs > 1 ? (float *)ws : dt;
   const size_t lds = dt_lds_bytes<Tag, WIN>();
   wbmm_dt_kernel<Tag, WIN><<<dim3((unsigned)(g.C * p.slabs)), dim3(kThreads), lds, st>>>(
