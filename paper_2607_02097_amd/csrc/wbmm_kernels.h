@@ -132,6 +132,7 @@ __device__ inline int fdiv(int v, int d, float inv) {
 
 struct KArgs {
   int64_t B, C, H, W;
+  int64_t numel;       // elements of one [B,C,H,W] tensor
   int NH, NW;
   int64_t N;           // windows per channel, B * NH * NW
   int tile;            // windows per workgroup tile (forward) / per slab (dtable)
@@ -141,12 +142,20 @@ struct KArgs {
 
 // A window row: element offset (from the tensor base) of its first element,
 // number of columns inside the image (0: the row lies outside the image or the
-// window does not exist), and whether it can move as dwords.
+// window does not exist) and how it moves:
+//   kDword: whole row, dword-aligned, whole dwords;
+//   kShift: whole 16-bit row that starts in the middle of a dword: the
+//           enclosing aligned dwords are read and shifted by 16 bits (every
+//           dword read holds at least one element of the tensor);
+//   kElem:  element by element (rows cut by the image edge).
+enum RowMode { kNone = 0, kDword = 1, kShift = 2, kElem = 3 };
+
 template <int WIN, int ES>
 struct Row {
   int64_t eoff;
   int cols;
-  bool fast;
+  int mode;
+  int odd;  // kShift: the row starts at the upper half of a dword
 };
 
 template <int WIN, int ES>
@@ -154,7 +163,8 @@ __device__ inline Row<WIN, ES> row_of(const KArgs &a, const void *base, int64_t 
   Row<WIN, ES> r;
   r.eoff = 0;
   r.cols = 0;
-  r.fast = false;
+  r.mode = kNone;
+  r.odd = 0;
   if (n >= a.N || hi >= WIN) return r;
   const int nhw = a.NH * a.NW;
   const int b = fdiv((int)n, nhw, a.inv_nhw);
@@ -166,8 +176,19 @@ __device__ inline Row<WIN, ES> row_of(const KArgs &a, const void *base, int64_t 
   const int64_t cw = a.W - (int64_t)wx * WIN;
   r.cols = cw < WIN ? (int)cw : WIN;
   r.eoff = (((int64_t)b * a.C + c) * a.H + h) * a.W + (int64_t)wx * WIN;
-  r.fast = r.cols == WIN && ((WIN * ES) & 3) == 0 &&
-           (((reinterpret_cast<uintptr_t>(base) + (uint64_t)r.eoff * ES) & 3u) == 0);
+  r.mode = kElem;
+  if (r.cols == WIN) {
+    const uint64_t addr = reinterpret_cast<uintptr_t>(base) + (uint64_t)r.eoff * ES;
+    if ((addr & 3u) == 0 && ((WIN * ES) & 3) == 0) {
+      r.mode = kDword;
+    } else if (ES == 2 && (WIN & 1)) {
+      // (even windows are only misaligned for odd image widths: element path)
+      r.odd = (int)((addr >> 1) & 1u);
+      const int64_t first = r.eoff - r.odd;                 // first element read
+      const int64_t last = first + 2 * (WIN / 2 + 1);       // one past the last
+      if (first >= 0 && last <= a.numel) r.mode = kShift;
+    }
+  }
   return r;
 }
 
@@ -183,12 +204,12 @@ struct RowData {
 template <int WIN, int ES>
 __device__ inline void load_row(const void *base, const Row<WIN, ES> &r, RowData<WIN, ES> &o) {
   constexpr int ND = RowData<WIN, ES>::ND;
-  constexpr int NDV = (WIN * ES) / 4;  // data dwords of a whole row (fast path)
+  constexpr int NDV = (WIN * ES) / 4;  // data dwords of a whole aligned row
 #pragma unroll
   for (int i = 0; i < ND; ++i) o.d[i] = 0;
-  if (r.cols == 0) return;
+  if (r.mode == kNone) return;
   const char *p = reinterpret_cast<const char *>(base) + r.eoff * ES;
-  if (r.fast) {
+  if (r.mode == kDword) {
     const uint32_t *p4 = reinterpret_cast<const uint32_t *>(p);
 #pragma unroll
     for (int i = 0; i + 4 <= NDV; i += 4) {
@@ -197,6 +218,17 @@ __device__ inline void load_row(const void *base, const Row<WIN, ES> &r, RowData
     }
 #pragma unroll
     for (int i = NDV & ~3; i < NDV; ++i) o.d[i] = p4[i];
+  } else if (ES == 2 && (WIN & 1) && r.mode == kShift) {
+    constexpr int NL = WIN / 2 + 1;  // dwords read
+    const uint32_t *p4 = reinterpret_cast<const uint32_t *>(p - 2 * r.odd);
+    uint32_t in[NL];
+#pragma unroll
+    for (int i = 0; i < NL; ++i) in[i] = p4[i];
+    const int sh = 16 * r.odd;
+#pragma unroll
+    for (int i = 0; i < (WIN + 1) / 2; ++i)
+      o.d[i] = (uint32_t)((((uint64_t)(i + 1 < NL ? in[i + 1] : 0u) << 32) | in[i]) >> sh);
+    if (WIN & 1) o.d[WIN / 2] &= 0xffffu;
   } else {
     // branch-free: element x reads column min(x, cols - 1), which is inside
     // the row, and is then zeroed when x >= cols
@@ -220,15 +252,31 @@ __device__ inline void load_row(const void *base, const Row<WIN, ES> &r, RowData
 template <int WIN, int ES>
 __device__ inline void store_row(void *base, const Row<WIN, ES> &r, const uint32_t *d) {
   constexpr int NDV = (WIN * ES) / 4;
-  if (r.cols == 0) return;
+  if (r.mode == kNone) return;
   char *p = reinterpret_cast<char *>(base) + r.eoff * ES;
-  if (r.fast) {
+  if (r.mode == kDword) {
     uint32_t *p4 = reinterpret_cast<uint32_t *>(p);
 #pragma unroll
     for (int i = 0; i + 4 <= NDV; i += 4)
       *reinterpret_cast<u32x4a *>(p4 + i) = u32x4a{d[i], d[i + 1], d[i + 2], d[i + 3]};
 #pragma unroll
     for (int i = NDV & ~3; i < NDV; ++i) p4[i] = d[i];
+  } else if (ES == 2 && (WIN & 1) && r.mode == kShift) {
+    u16 *p2 = reinterpret_cast<u16 *>(p);
+    auto elem = [&](int x) -> uint32_t { return (x & 1) ? (d[x >> 1] >> 16) : (d[x >> 1] & 0xffffu); };
+    if (r.odd) {
+      // element 0 shares its dword with the previous element of the tensor
+      p2[0] = (u16)elem(0);
+#pragma unroll
+      for (int x = 1; x + 1 < WIN; x += 2)
+        *reinterpret_cast<uint32_t *>(p2 + x) = elem(x) | (elem(x + 1) << 16);
+      if ((WIN - 1) & 1) p2[WIN - 1] = (u16)elem(WIN - 1);
+    } else {
+#pragma unroll
+      for (int x = 0; x + 1 < WIN; x += 2)
+        *reinterpret_cast<uint32_t *>(p2 + x) = elem(x) | (elem(x + 1) << 16);
+      if (WIN & 1) p2[WIN - 1] = (u16)elem(WIN - 1);
+    }
   } else {
 #pragma unroll
     for (int x = 0; x < WIN; ++x) {
@@ -288,12 +336,14 @@ __global__ __launch_bounds__(kThreads) void wbmm_fwd_kernel(const typename Tag::
   const int64_t n0 = (int64_t)(blockIdx.x - c * a.tiles_per_ch) * a.tile;
   const int nwin = (int)((n0 + a.tile <= a.N) ? a.tile : a.N - n0);
 
-  // ---- 1. table -> LDS; rows -> window-major LDS tile (padding included)
-  for (int k = tid; k < K2; k += kThreads) Ts[k] = tab[c * K2 + (REV ? K2 - 1 - k : k)];
+  // ---- 1. rows -> window-major LDS tile (padding included); while the first
+  //         rows are in flight, the Toeplitz blocks of M_c are built straight
+  //         from the table in global memory: TB[dh][x_out][x_in] (16-bit
+  //         path), or the table itself goes to LDS (float32 path).
   {
     const int nrows = nwin * KR;
     constexpr int U = 4;
-    for (int q0 = tid; q0 < nrows; q0 += kThreads * U) {
+    for (int q0 = tid; q0 < nrows || q0 == tid; q0 += kThreads * U) {
       RD rd[U];
       int dst[U];
 #pragma unroll
@@ -306,6 +356,33 @@ __global__ __launch_bounds__(kThreads) void wbmm_fwd_kernel(const typename Tag::
           const Row<WIN, ES> r = row_of<WIN, ES>(a, x, c, n0 + v, hi);
           load_row<WIN, ES>(x, r, rd[k]);
           dst[k] = (v * LDSW + hi * RP) * ES;
+        }
+      }
+      if (q0 == tid) {
+        const S *tc = tab + c * K2;
+        if constexpr (Tag::W16) {
+          constexpr int CPR = RP / 8;               // 8-element chunks per TB row
+          constexpr int NCH = K1 * RP * CPR;
+          for (int ch = tid; ch < NCH; ch += kThreads) {
+            const int row = ch / CPR;               // = dhi * RP + xo
+            const int xi0 = (ch - row * CPR) * 8;
+            const int dhi = row / RP;
+            const int xo = row - dhi * RP;
+            u16x8 v = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+            if (xo < WIN) {
+              const int k0 = dhi * K1 - xo + WIN - 1;  // table index of x_in = 0
+#pragma unroll
+              for (int e = 0; e < 8; ++e) {
+                const int xi = xi0 + e < WIN ? xi0 + e : WIN - 1;
+                const int k = k0 + xi;
+                const u16 t = tc[REV ? K2 - 1 - k : k];
+                v[e] = xi0 + e < WIN ? t : (u16)0;
+              }
+            }
+            *reinterpret_cast<u16x8 *>(&TB[row * RP + xi0]) = v;
+          }
+        } else {
+          for (int k = tid; k < K2; k += kThreads) Ts[k] = tc[REV ? K2 - 1 - k : k];
         }
       }
 #pragma unroll
@@ -325,15 +402,6 @@ __global__ __launch_bounds__(kThreads) void wbmm_fwd_kernel(const typename Tag::
   const int nsub = (nwin + 15) >> 4;
   if constexpr (Tag::W16) {
     constexpr int S_ = G::S, NT = G::NT, NB = G::NB;
-    // ---- 2. Toeplitz blocks of M_c: TB[dh][x_out][x_in]
-    for (int i = tid; i < G::TB_LEN; i += kThreads) {
-      const int dhi = i / (RP * RP);
-      const int rem = i - dhi * RP * RP;
-      const int xo = rem / RP;
-      const int xi = rem - xo * RP;
-      TB[i] = (xo < WIN && xi < WIN) ? Ts[dhi * K1 + xi - xo + WIN - 1] : (S)0;
-    }
-    __syncthreads();
     // ---- 3. the distinct B fragments, in registers
     Frag bf[NB];
 #pragma unroll
@@ -406,7 +474,7 @@ __global__ __launch_bounds__(kThreads) void wbmm_fwd_kernel(const typename Tag::
       const int v = q / WIN;
       const int hi = q - v * WIN;
       const Row<WIN, ES> r = row_of<WIN, ES>(a, y, c, n0 + v, hi);
-      if (r.cols == 0) continue;
+      if (r.mode == kNone) continue;
       const uint32_t *l4 = reinterpret_cast<const uint32_t *>(smem + (v * LDSW + hi * RP) * ES);
       uint32_t d[RD::ND];
 #pragma unroll
@@ -426,28 +494,21 @@ struct DtCfg {
   static constexpr int RP = rp_of(WIN);
   static constexpr int PP = WIN * RP;
   static constexpr int NPT = cdiv(PP, 16);        // 16-position tiles
-  static constexpr int KPT = NPT * 16;            // padded positions
+  static constexpr int KR = cdiv(NPT * 16, RP);   // rows per staged window
   static constexpr int R = 16 / RP;               // window rows per tile
   static constexpr int CW = Tag::W16 ? 32 : 16;   // windows per LDS stage
-  static constexpr int CWS = Tag::W16 ? CW + 8 : CW + 4;  // position row stride (elements)
-  // bytes of one position row plus a 16-byte shift per window row, so the w
-  // strided stores of a row copy from different window rows hit other banks
-  static constexpr int PB = CWS * Tag::ES;
-  static constexpr int BUF = KPT * PB + (KPT / RP) * 16;  // bytes per operand buffer
+  // window-major staging, as in the forward, with a row pitch (elements) that
+  // keeps the fragment reads free of bank conflicts: 16-bit transposing reads
+  // of 4 windows x 16 positions; float32 reads of 4 windows x 16 positions
+  static constexpr int LDSW = Tag::W16 ? NPT * 16 + 8 : NPT * 16 + ((16 - NPT * 16) % 64 + 64) % 64;
+  static constexpr int BUF = CW * LDSW * Tag::ES;  // bytes per operand buffer
   static constexpr int NACC = 2 * NPT - 1;        // accumulators: pi - po
   static constexpr int K1 = 2 * WIN - 1;
   static constexpr int K2 = K1 * K1;
   static constexpr int NBT = (2 * R - 1) * K1;    // bins per accumulator tile
-  static constexpr int ROWS = 2 * CW * WIN;       // row copies per stage (x and dy)
+  static constexpr int ROWS = 2 * CW * KR;        // row copies per stage (x and dy)
   static constexpr int RPT = cdiv(ROWS, kThreads);  // row copies per thread
 };
-
-// Byte offset of (position p, window v) in a position-major operand buffer.
-template <class Tag, int WIN>
-__device__ __host__ constexpr int dt_off(int p, int v) {
-  typedef DtCfg<Tag, WIN> G;
-  return p * G::PB + (p / G::RP) * 16 + v * Tag::ES;
-}
 
 // Accumulator tiles are split among the waves in contiguous ranges of
 // P = pi - po (tile P carries NPT - |P| block products per K step), the
@@ -492,12 +553,12 @@ template <class Tag, int WIN>
 __host__ __device__ constexpr size_t dt_lds_bytes() {
   typedef DtCfg<Tag, WIN> G;
   const size_t ops = 2 * (size_t)G::BUF;
-  const size_t bins = (size_t)(kWaves * 16 * 17 + G::NACC * G::NBT) * 4;
+  const size_t bins = (size_t)(kWaves * 2 * 16 * 17 + G::NACC * G::NBT) * 4;
   return ops > bins ? ops : bins;
 }
 
-// Row copies of one stage: task q covers tensor (q / (CW * WIN)), window
-// (q / WIN) % CW of the stage and window row q % WIN.
+// Row copies of one stage: task q covers tensor (q / (CW * KR)), window
+// (q / KR) % CW of the stage and padded row q % KR (rows >= w are zero).
 template <class Tag, int WIN>
 struct DtStage {
   typedef DtCfg<Tag, WIN> G;
@@ -511,44 +572,59 @@ __device__ inline void dt_load_stage(const KArgs &a, const void *x, const void *
 #pragma unroll
   for (int k = 0; k < G::RPT; ++k) {
     const int q = tid + k * kThreads;
-    const int tens = q / (G::CW * WIN);
-    const int rem = q - tens * (G::CW * WIN);
-    const int v = rem / WIN;
-    const int hi = rem - v * WIN;
+    const int tens = q / (G::CW * G::KR);
+    const int rem = q - tens * (G::CW * G::KR);
+    const int v = rem / G::KR;
+    const int hi = rem - v * G::KR;
     const void *src = tens ? dy : x;
     Row<WIN, Tag::ES> r;
-    r.cols = 0; r.eoff = 0; r.fast = false;
+    r.cols = 0; r.eoff = 0; r.mode = kNone; r.odd = 0;
     if (q < G::ROWS && m0 + v < m1) r = row_of<WIN, Tag::ES>(a, src, c, m0 + v, hi);
     load_row<WIN, Tag::ES>(src, r, st.rd[k]);
   }
 }
 
-// Write a loaded stage position-major: element x of row hi of window v goes to
-// (p = hi * RP + x, v).  Positions past the window (x >= w, rows >= w) are
-// never written and stay zero from the initial clear.
+// Write a loaded stage window-major (padded rows, as in the forward tile).
 template <class Tag, int WIN>
 __device__ inline void dt_write_stage(unsigned char *smem, int tid, const DtStage<Tag, WIN> &st) {
   typedef DtCfg<Tag, WIN> G;
-  constexpr int RP = G::RP;
+  typedef RowData<WIN, Tag::ES> RD;
 #pragma unroll
   for (int k = 0; k < G::RPT; ++k) {
     const int q = tid + k * kThreads;
     if (q >= G::ROWS) continue;
-    const int tens = q / (G::CW * WIN);
-    const int rem = q - tens * (G::CW * WIN);
-    const int v = rem / WIN;
-    const int hi = rem - v * WIN;
-    unsigned char *base = smem + tens * G::BUF + dt_off<Tag, WIN>(hi * RP, v);
+    const int tens = q / (G::CW * G::KR);
+    const int rem = q - tens * (G::CW * G::KR);
+    const int v = rem / G::KR;
+    const int hi = rem - v * G::KR;
+    uint32_t *l4 = reinterpret_cast<uint32_t *>(smem + tens * G::BUF + (v * G::LDSW + hi * G::RP) * Tag::ES);
 #pragma unroll
-    for (int xi = 0; xi < WIN; ++xi) {
-      if (Tag::ES == 4) {
-        *reinterpret_cast<uint32_t *>(base + xi * G::PB) = st.rd[k].d[xi];
-      } else {
-        const uint32_t d = st.rd[k].d[xi >> 1];
-        *reinterpret_cast<u16 *>(base + xi * G::PB) = (u16)((xi & 1) ? (d >> 16) : (d & 0xffffu));
-      }
-    }
+    for (int i = 0; i < RD::ND; i += 4)
+      *reinterpret_cast<uint4 *>(l4 + i) = make_uint4(st.rd[k].d[i], st.rd[k].d[i + 1], st.rd[k].d[i + 2], st.rd[k].d[i + 3]);
   }
+}
+
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+// Matrix-core fragment of a position-major view of a window-major stage
+// (16-bit): lane (g, i) receives the 8 values of positions 16 * pt + i for
+// windows 8g .. 8g + 7, by two transposing LDS reads.  Within a 16-lane group
+// the transposing read hands lane i the i-th column of the 4 x 16 block whose
+// row r is the 4-element chunks of lanes 4r .. 4r + 3; lane 4r + q points at
+// window 8g + r (+4), positions 16 * pt + 4q .. + 3.
+template <class Tag, int WIN>
+__device__ inline u16x8 dt_frag16(const unsigned char *buf, int pt, int lane) {
+  typedef DtCfg<Tag, WIN> G;
+  const int g = lane >> 4;
+  const int i = lane & 15;
+  const int r = i >> 2, q = i & 3;
+  const int e0 = (8 * g + r) * G::LDSW + 16 * pt + 4 * q;
+  lds_i16x4 *p0 = (lds_i16x4 *)(buf + 2 * e0);
+  lds_i16x4 *p1 = (lds_i16x4 *)(buf + 2 * (e0 + 4 * G::LDSW));
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(p0);
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(p1);
+  return __builtin_bit_cast(u16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
 template <class Tag, int WIN, int WAVE>
@@ -579,16 +655,11 @@ __device__ __attribute__((always_inline)) void dt_wave(const typename Tag::S *__
 #pragma unroll
   for (int j = 0; j < NP; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // padded positions must read as zero: clear both buffers once
-  {
-    uint4 *t4 = reinterpret_cast<uint4 *>(smem);
-    for (int i = tid; i < (2 * G::BUF) / 16; i += kThreads) t4[i] = make_uint4(0, 0, 0, 0);
-  }
   DtStage<Tag, WIN> st;
   dt_load_stage<Tag, WIN>(a, x, dy, c, s0, s1, tid, st);
 
   for (int64_t m0 = s0; m0 < s1; m0 += CW) {
-    __syncthreads();  // previous stage consumed (first pass: clear done)
+    if (m0 != s0) __syncthreads();  // previous stage consumed
     dt_write_stage<Tag, WIN>(smem, tid, st);
     __syncthreads();
     if (m0 + CW < s1) dt_load_stage<Tag, WIN>(a, x, dy, c, m0 + CW, s1, tid, st);
@@ -603,9 +674,9 @@ __device__ __attribute__((always_inline)) void dt_wave(const typename Tag::S *__
           for (int po = 0; po < NPT; ++po) {
             const bool used = po + PHI >= 0 && po + PLO <= NPT - 1;
             if (used && (po + PLO > 0 ? po + PLO : 0) == pi)
-              bf[po] = *reinterpret_cast<const Frag *>(Dt + dt_off<Tag, WIN>(16 * po + ln, 8 * g));
+              bf[po] = dt_frag16<Tag, WIN>(Dt, po, lane);
           }
-          const Frag af = *reinterpret_cast<const Frag *>(Xt + dt_off<Tag, WIN>(16 * pi + ln, 8 * g));
+          const Frag af = dt_frag16<Tag, WIN>(Xt, pi, lane);
 #pragma unroll
           for (int j = 0; j < NP; ++j) {
             const int po = pi - (PLO + j);
@@ -622,9 +693,9 @@ __device__ __attribute__((always_inline)) void dt_wave(const typename Tag::S *__
             for (int po = 0; po < NPT; ++po) {
               const bool used = po + PHI >= 0 && po + PLO <= NPT - 1;
               if (used && (po + PLO > 0 ? po + PLO : 0) == pi)
-                bf[po] = *reinterpret_cast<const float *>(Dt + dt_off<Tag, WIN>(16 * po + ln, 4 * ks + g));
+                bf[po] = reinterpret_cast<const float *>(Dt)[(4 * ks + g) * G::LDSW + 16 * po + ln];
             }
-            const float af = *reinterpret_cast<const float *>(Xt + dt_off<Tag, WIN>(16 * pi + ln, 4 * ks + g));
+            const float af = reinterpret_cast<const float *>(Xt)[(4 * ks + g) * G::LDSW + 16 * pi + ln];
 #pragma unroll
             for (int j = 0; j < NP; ++j) {
               const int po = pi - (PLO + j);
@@ -637,31 +708,45 @@ __device__ __attribute__((always_inline)) void dt_wave(const typename Tag::S *__
   }
   __syncthreads();
 
-  // ---- diagonal binning, fixed order
-  float *scr = reinterpret_cast<float *>(smem) + WAVE * 16 * 17;
-  float *binsum = reinterpret_cast<float *>(smem) + kWaves * 16 * 17;
+  // ---- diagonal binning, two accumulator tiles per round, fixed order.
+  // Bin (da, dw) of tile P sums the elements (ra*RP + xo + dw, rb*RP + xo)
+  // with ra - rb = da over xo; every lane issues all its reads at once
+  // (out-of-range terms read a valid slot and are masked to zero).
+  float *scr = reinterpret_cast<float *>(smem) + WAVE * 2 * 16 * 17;
+  float *binsum = reinterpret_cast<float *>(smem) + kWaves * 2 * 16 * 17;
 #pragma unroll
-  for (int j = 0; j < NP; ++j) {
-    const int pidx = PLO + j + NPT - 1;
+  for (int j0 = 0; j0 < NP; j0 += 2) {
 #pragma unroll
-    for (int rr = 0; rr < 4; ++rr) scr[(4 * g + rr) * 17 + ln] = acc[j][rr];
+    for (int h = 0; h < 2; ++h) {
+      if (j0 + h < NP) {
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) scr[h * 272 + (4 * g + rr) * 17 + ln] = acc[j0 + h][rr];
+      }
+    }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    for (int bin = lane; bin < NBT; bin += 64) {
+    const int nb2 = (j0 + 1 < NP ? 2 : 1) * NBT;
+    for (int b2 = lane; b2 < nb2; b2 += 64) {
+      const int h = b2 >= NBT ? 1 : 0;
+      const int bin = b2 - h * NBT;
       const int da = bin / K1 - (R - 1);  // input sub-row minus output sub-row
       const int dw = bin - (bin / K1) * K1 - (WIN - 1);
-      float s = 0.f;
+      const float *t = scr + h * 272;
+      float sum = 0.f;
+#pragma unroll
       for (int ra = 0; ra < R; ++ra) {
         const int rb = ra - da;
-        if (rb < 0 || rb >= R) continue;
+        const bool rok = rb >= 0 && rb < R;
+#pragma unroll
         for (int xo = 0; xo < WIN; ++xo) {
           const int xi = xo + dw;
-          if (xi < 0 || xi >= WIN) continue;
-          s += scr[(ra * RP + xi) * 17 + rb * RP + xo];
+          const bool ok = rok && xi >= 0 && xi < WIN;
+          const float v = t[ok ? (ra * RP + xi) * 17 + rb * RP + xo : 0];
+          sum += ok ? v : 0.f;
         }
       }
-      binsum[pidx * NBT + bin] = s;
+      binsum[(PLO + j0 + h + NPT - 1) * NBT + bin] = sum;
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -683,7 +768,7 @@ __device__ __attribute__((always_inline)) void dt_wave(const typename Tag::S *__
 }
 
 template <class Tag, int WIN>
-__global__ __launch_bounds__(kThreads) void wbmm_dt_kernel(const typename Tag::S *__restrict__ x,
+__global__ __launch_bounds__(kThreads, 3) void wbmm_dt_kernel(const typename Tag::S *__restrict__ x,
                                                            const typename Tag::S *__restrict__ dy,
                                                            float *__restrict__ out, KArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
@@ -714,6 +799,7 @@ static int64_t cdiv64(int64_t a, int64_t b) { return (a + b - 1) / b; }
 static KArgs make_args(const Geom &g) {
   KArgs a;
   a.B = g.B; a.C = g.C; a.H = g.H; a.W = g.W;
+  a.numel = g.B * g.C * g.H * g.W;
   a.NH = (int)g.NH; a.NW = (int)g.NW; a.N = g.N;
   a.tile = 0; a.tiles_per_ch = 0;
   a.inv_nw = 1.0f / (float)g.NW;
