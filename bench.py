@@ -91,7 +91,7 @@ def main():
         y, dx = torch.empty_like(x), torch.empty_like(dy)
         dtab = torch.empty((wl.C, wl.table_len), dtype=torch.float32, device=dev)
         need = W.wbmm_backward_table_workspace_bytes(x.shape, wl.w, tdt)
-        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+        ws = W.new_workspace(need, dev)  # counters start at zero, stay zero
         sets.append((x, t, dy, y, dx, dtab, ws))
 
     passes = wl.passes

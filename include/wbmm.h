@@ -91,10 +91,22 @@ size_t wbmm_backward_table_workspace_bytes(int64_t B, int64_t C, int64_t H,
  *                  I[i, j] = k of x[.., i] * dy[.., j]
  * (the scatter-add of the per-window products X^T dY over the relative-offset
  * index).  x, dy: [B,C,H,W] in dtype; dtable: float32 [C,(2w-1)^2],
- * overwritten.  workspace: device buffer of at least
- * wbmm_backward_table_workspace_bytes(...) bytes (may be NULL when that is 0);
- * its contents on entry do not matter.  The reduction has a fixed order: the
- * result is bitwise reproducible for a given shape. */
+ * overwritten.
+ *
+ * workspace: device buffer of at least wbmm_backward_table_workspace_bytes()
+ * bytes (may be NULL when that is 0).  It starts with one 32-bit counter per
+ * channel (the first ceil(4C/256)*256 bytes), followed by per-slab partial
+ * sums.  The counters must be ZERO when a call starts: zero-fill the
+ * workspace before its first use.  Every call that completes leaves its
+ * counters at zero again, so repeated calls with the same shape (or with fewer
+ * channels) reuse the workspace as it is; before a call with more channels,
+ * zero the first ceil(4C/256)*256 bytes again (they may hold partial sums of
+ * earlier calls).  Calls that run concurrently must not share a workspace.
+ * The partial-sum area may hold anything on entry.
+ *
+ * The reduction has a fixed order (slab partials are summed in slab order by
+ * the last workgroup of each channel): the result is bitwise reproducible for
+ * a given shape. */
 wbmm_status wbmm_backward_table(const void *x, const void *dy, float *dtable,
                                 void *workspace, size_t workspace_bytes,
                                 int64_t B, int64_t C, int64_t H, int64_t W,

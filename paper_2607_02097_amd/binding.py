@@ -136,9 +136,35 @@ def wbmm_backward_table_workspace_bytes(shape, w: int, dtype) -> int:
     return int(load_library().wbmm_backward_table_workspace_bytes(B, C, H, W, int(w), _code(dtype)))
 
 
+_WS_CACHE = {}
+
+
+def _cached_workspace(device, nbytes, stream, shape_key):
+    """A zero-filled workspace kept per (device, stream, call shape).  The
+    library leaves its counters at zero after every call, so a workspace is
+    zero-filled once, when it is created for a new shape."""
+    st = torch.cuda.current_stream(device).cuda_stream if stream is None else \
+        int(getattr(stream, "cuda_stream", stream))
+    key = (str(device), st, shape_key)
+    ws = _WS_CACHE.get(key)
+    if ws is None:
+        ws = torch.zeros(nbytes, dtype=torch.uint8, device=device)
+        _WS_CACHE[key] = ws
+    return ws
+
+
+def new_workspace(nbytes: int, device="cuda") -> torch.Tensor:
+    """A zero-filled workspace for wbmm_backward_table (see include/wbmm.h)."""
+    return torch.zeros(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
 def wbmm_backward_table(x: torch.Tensor, dy: torch.Tensor, w: int, out=None, workspace=None,
                         stream=None):
-    """dtable (float32 [C,(2w-1)^2], overwritten) for input x and gradient dy."""
+    """dtable (float32 [C,(2w-1)^2], overwritten) for input x and gradient dy.
+
+    ``workspace``: a uint8 device tensor whose counter area is zero (see
+    include/wbmm.h; ``new_workspace`` makes one).  When omitted, a zeroed
+    workspace cached per (device, stream, shape) is used."""
     _check_tensor(x, "x")
     _check_tensor(dy, "dy")
     if dy.shape != x.shape or dy.dtype != x.dtype or dy.device != x.device:
@@ -153,7 +179,7 @@ def wbmm_backward_table(x: torch.Tensor, dy: torch.Tensor, w: int, out=None, wor
             raise ValueError("out must be float32 [C, (2w-1)^2] on x's device")
     need = wbmm_backward_table_workspace_bytes(x.shape, w, x.dtype)
     if workspace is None and need > 0:
-        workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
+        workspace = _cached_workspace(x.device, need, stream, (tuple(x.shape), int(w), x.dtype))
     ws_ptr = ctypes.c_void_p(workspace.data_ptr() if workspace is not None else 0)
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     with torch.cuda.device(x.device):

@@ -43,8 +43,9 @@
 // pi - po, so all pairs with equal pi - po share one accumulator (27 16x16
 // fp32 tiles at w = 14), split across the four waves.  The next stage's rows
 // are loaded into registers while the current stage computes.  Diagonal sums
-// of the tiles give dT; slabs are combined by a second kernel in a fixed
-// order (no atomics anywhere, bitwise reproducible).
+// of the tiles give dT.  Slabs of one channel are summed in slab order by
+// the channel's last workgroup, found with one atomic ticket per workgroup;
+// the result is bitwise reproducible.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -308,139 +309,213 @@ struct FwdCfg {
   static constexpr int TB_LEN = Tag::W16 ? K1 * RP * RP : 0;
 };
 
+// The forward kernel runs two waves per workgroup.  Each wave owns a run of
+// 16-window sub-tiles and pipelines them through one private LDS buffer: the
+// rows of sub-tile j+1 are loaded into registers while sub-tile j is
+// multiplied and its rows are stored, so reads and writes of the whole grid
+// stay interleaved (a grid that reads everything first and writes everything
+// afterwards moves data at about half the rate).
+constexpr int kFwdWaves = 4;
+constexpr int kFwdThreads = 64 * kFwdWaves;
+
 template <class Tag, int WIN>
-__host__ __device__ constexpr size_t fwd_lds_bytes(int tile) {
+__host__ __device__ constexpr size_t fwd_lds_bytes() {
   typedef FwdCfg<Tag, WIN> G;
-  return (size_t)tile * G::LDSW * Tag::ES + (size_t)(G::TS_LEN + G::TB_LEN) * Tag::ES;
+  return (size_t)kFwdWaves * 16 * G::LDSW * Tag::ES + (size_t)(G::TS_LEN + G::TB_LEN) * Tag::ES;
+}
+
+// Row copies of one sub-tile (16 windows x KR padded rows) spread over the 64
+// lanes of a wave; rows of one window are consecutive.
+template <class Tag, int WIN>
+struct SubRows {
+  static constexpr int N = 16 * FwdCfg<Tag, WIN>::KR;
+  static constexpr int PER_LANE = cdiv(N, 64);
+  RowData<WIN, Tag::ES> rd[PER_LANE];
+};
+
+template <class Tag, int WIN>
+__device__ inline void load_sub(const KArgs &a, const void *x, int64_t c, int64_t m0, int nwin, int lane,
+                                SubRows<Tag, WIN> &o) {
+  constexpr int KR = FwdCfg<Tag, WIN>::KR;
+#pragma unroll
+  for (int k = 0; k < SubRows<Tag, WIN>::PER_LANE; ++k) {
+    const int q = lane + 64 * k;
+    const int v = q / KR;
+    const int hi = q - v * KR;
+    Row<WIN, Tag::ES> r;
+    r.cols = 0; r.eoff = 0; r.mode = kNone; r.odd = 0;
+    if (q < SubRows<Tag, WIN>::N && v < nwin) r = row_of<WIN, Tag::ES>(a, x, c, m0 + v, hi);
+    load_row<WIN, Tag::ES>(x, r, o.rd[k]);
+  }
+}
+
+template <class Tag, int WIN>
+__device__ inline void write_sub(unsigned char *buf, int lane, const SubRows<Tag, WIN> &o) {
+  typedef FwdCfg<Tag, WIN> G;
+  typedef RowData<WIN, Tag::ES> RD;
+#pragma unroll
+  for (int k = 0; k < SubRows<Tag, WIN>::PER_LANE; ++k) {
+    const int q = lane + 64 * k;
+    if (q >= SubRows<Tag, WIN>::N) continue;
+    const int v = q / G::KR;
+    const int hi = q - v * G::KR;
+    uint32_t *l4 = reinterpret_cast<uint32_t *>(buf + (v * G::LDSW + hi * G::RP) * Tag::ES);
+#pragma unroll
+    for (int i = 0; i < RD::ND; i += 4)
+      *reinterpret_cast<uint4 *>(l4 + i) = make_uint4(o.rd[k].d[i], o.rd[k].d[i + 1], o.rd[k].d[i + 2], o.rd[k].d[i + 3]);
+  }
+}
+
+template <class Tag, int WIN>
+__device__ inline void store_sub(const KArgs &a, void *y, int64_t c, int64_t m0, int nwin, int lane,
+                                 const unsigned char *buf) {
+  typedef FwdCfg<Tag, WIN> G;
+  typedef RowData<WIN, Tag::ES> RD;
+  for (int q = lane; q < 16 * WIN; q += 64) {
+    const int v = q / WIN;
+    const int hi = q - v * WIN;
+    if (v >= nwin) break;
+    const Row<WIN, Tag::ES> r = row_of<WIN, Tag::ES>(a, y, c, m0 + v, hi);
+    if (r.mode == kNone) continue;
+    const uint32_t *l4 = reinterpret_cast<const uint32_t *>(buf + (v * G::LDSW + hi * G::RP) * Tag::ES);
+    uint32_t d[RD::ND];
+#pragma unroll
+    for (int i = 0; i < RD::ND; i += 4) {
+      const uint4 u = *reinterpret_cast<const uint4 *>(l4 + i);
+      d[i] = u.x; d[i + 1] = u.y; d[i + 2] = u.z; d[i + 3] = u.w;
+    }
+    store_row<WIN, Tag::ES>(y, r, d);
+  }
 }
 
 template <class Tag, int WIN, bool REV>
-__global__ __launch_bounds__(kThreads) void wbmm_fwd_kernel(const typename Tag::S *__restrict__ x,
-                                                            const typename Tag::S *__restrict__ tab,
-                                                            typename Tag::S *__restrict__ y, KArgs a) {
+__global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename Tag::S *__restrict__ x,
+                                                                  const typename Tag::S *__restrict__ tab,
+                                                                  typename Tag::S *__restrict__ y, KArgs a) {
   typedef typename Tag::S S;
   typedef typename Tag::Frag Frag;
   typedef FwdCfg<Tag, WIN> G;
-  typedef RowData<WIN, Tag::ES> RD;
-  constexpr int RP = G::RP, KR = G::KR, LDSW = G::LDSW, K1 = G::K1, K2 = G::K2, ES = Tag::ES;
+  constexpr int RP = G::RP, LDSW = G::LDSW, K1 = G::K1, K2 = G::K2;
 
   extern __shared__ __align__(16) unsigned char smem[];
-  S *tile = reinterpret_cast<S *>(smem);
-  S *Ts = tile + a.tile * LDSW;
+  S *Ts = reinterpret_cast<S *>(smem + kFwdWaves * 16 * LDSW * Tag::ES);
   S *TB = Ts + G::TS_LEN;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
+  unsigned char *buf = smem + wave * 16 * LDSW * Tag::ES;  // this wave's sub-tile
+  S *rowp = reinterpret_cast<S *>(buf);
+
   const int64_t c = blockIdx.x / a.tiles_per_ch;
   const int64_t n0 = (int64_t)(blockIdx.x - c * a.tiles_per_ch) * a.tile;
   const int nwin = (int)((n0 + a.tile <= a.N) ? a.tile : a.N - n0);
+  const int spw = a.tile / (16 * kFwdWaves);  // sub-tiles per wave
+  const int first = wave * spw;               // this wave's first sub-tile
+  int nsub = (nwin - first * 16 + 15) / 16;   // its sub-tiles holding windows
+  nsub = nsub < 0 ? 0 : (nsub > spw ? spw : nsub);
 
-  // ---- 1. rows -> window-major LDS tile (padding included); while the first
-  //         rows are in flight, the Toeplitz blocks of M_c are built straight
-  //         from the table in global memory: TB[dh][x_out][x_in] (16-bit
-  //         path), or the table itself goes to LDS (float32 path).
+  // ---- 1. first sub-tile's rows in flight; the table (Toeplitz blocks of
+  //         M_c for 16-bit, the table itself for float32) -> LDS
+  SubRows<Tag, WIN> nxt;
+  if (nsub > 0) load_sub<Tag, WIN>(a, x, c, n0 + first * 16, nwin - first * 16, lane, nxt);
   {
-    const int nrows = nwin * KR;
-    constexpr int U = 4;
-    for (int q0 = tid; q0 < nrows || q0 == tid; q0 += kThreads * U) {
-      RD rd[U];
-      int dst[U];
+    const S *tc = tab + c * K2;
+    if constexpr (Tag::W16) {
+      constexpr int CPR = RP / 8;               // 8-element chunks per TB row
+      constexpr int NCH = K1 * RP * CPR;
+      for (int ch = tid; ch < NCH; ch += kFwdThreads) {
+        const int row = ch / CPR;               // = dhi * RP + x_out
+        const int xi0 = (ch - row * CPR) * 8;
+        const int dhi = row / RP;
+        const int xo = row - dhi * RP;
+        u16x8 v = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+        if (xo < WIN) {
+          const int k0 = dhi * K1 - xo + WIN - 1;  // table index of x_in = 0
 #pragma unroll
-      for (int k = 0; k < U; ++k) {
-        const int q = q0 + k * kThreads;
-        dst[k] = -1;
-        if (q < nrows) {
-          const int v = q / KR;  // rows of one window are consecutive
-          const int hi = q - v * KR;
-          const Row<WIN, ES> r = row_of<WIN, ES>(a, x, c, n0 + v, hi);
-          load_row<WIN, ES>(x, r, rd[k]);
-          dst[k] = (v * LDSW + hi * RP) * ES;
-        }
-      }
-      if (q0 == tid) {
-        const S *tc = tab + c * K2;
-        if constexpr (Tag::W16) {
-          constexpr int CPR = RP / 8;               // 8-element chunks per TB row
-          constexpr int NCH = K1 * RP * CPR;
-          for (int ch = tid; ch < NCH; ch += kThreads) {
-            const int row = ch / CPR;               // = dhi * RP + xo
-            const int xi0 = (ch - row * CPR) * 8;
-            const int dhi = row / RP;
-            const int xo = row - dhi * RP;
-            u16x8 v = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
-            if (xo < WIN) {
-              const int k0 = dhi * K1 - xo + WIN - 1;  // table index of x_in = 0
-#pragma unroll
-              for (int e = 0; e < 8; ++e) {
-                const int xi = xi0 + e < WIN ? xi0 + e : WIN - 1;
-                const int k = k0 + xi;
-                const u16 t = tc[REV ? K2 - 1 - k : k];
-                v[e] = xi0 + e < WIN ? t : (u16)0;
-              }
-            }
-            *reinterpret_cast<u16x8 *>(&TB[row * RP + xi0]) = v;
+          for (int e = 0; e < 8; ++e) {
+            const int xi = xi0 + e < WIN ? xi0 + e : WIN - 1;
+            const int k = k0 + xi;
+            const u16 t = tc[REV ? K2 - 1 - k : k];
+            v[e] = xi0 + e < WIN ? t : (u16)0;
           }
-        } else {
-          for (int k = tid; k < K2; k += kThreads) Ts[k] = tc[REV ? K2 - 1 - k : k];
         }
+        *reinterpret_cast<u16x8 *>(&TB[row * RP + xi0]) = v;
       }
-#pragma unroll
-      for (int k = 0; k < U; ++k) {
-        if (dst[k] < 0) continue;
-        uint32_t *l4 = reinterpret_cast<uint32_t *>(smem + dst[k]);
-#pragma unroll
-        for (int i = 0; i < RD::ND; i += 4)
-          *reinterpret_cast<uint4 *>(l4 + i) = make_uint4(rd[k].d[i], rd[k].d[i + 1], rd[k].d[i + 2], rd[k].d[i + 3]);
-      }
+    } else {
+      for (int k = tid; k < K2; k += kFwdThreads) Ts[k] = tc[REV ? K2 - 1 - k : k];
     }
   }
   __syncthreads();
 
   const int g = lane >> 4;   // lane group
   const int ln = lane & 15;  // row (A) / column (B, C) inside a 16x16 tile
-  const int nsub = (nwin + 15) >> 4;
   if constexpr (Tag::W16) {
     constexpr int S_ = G::S, NT = G::NT, NB = G::NB;
-    // ---- 3. the distinct B fragments, in registers
-    Frag bf[NB];
-#pragma unroll
-    for (int q = 0; q < NB; ++q) {
-      const int d0 = q - (NT - 1);  // = 2*kstep - ntile
+    // ---- 2. B fragment q (= 2*kstep - ntile + NT - 1) for this lane
+    auto load_bf = [&](int q) -> Frag {
+      const int d0 = q - (NT - 1);
       int dh, xi0;
       if (RP == 16) { dh = d0 + (g >> 1); xi0 = 8 * (g & 1); }
       else { dh = 2 * d0 + g - (ln >> 3); xi0 = 0; }
       const int xo = ln & (RP - 1);
       if (dh >= -(WIN - 1) && dh <= WIN - 1)
-        bf[q] = *reinterpret_cast<const Frag *>(&TB[((dh + WIN - 1) * RP + xo) * RP + xi0]);
-      else
-        bf[q] = Frag{0, 0, 0, 0, 0, 0, 0, 0};
-    }
-    // ---- 4. 16-window sub-tiles: A fragments, products, rounded results
-    for (int sub = wave; sub < nsub; sub += kWaves) {
-      S *rowp = tile + (sub * 16) * LDSW;
+        return *reinterpret_cast<const Frag *>(&TB[((dh + WIN - 1) * RP + xo) * RP + xi0]);
+      return Frag{0, 0, 0, 0, 0, 0, 0, 0};
+    };
+    // ---- 3. pipeline over this wave's sub-tiles
+    for (int j = 0; j < nsub; ++j) {
+      const int64_t m0 = n0 + (first + j) * 16;
+      const int mw = nwin - (first + j) * 16;  // windows left from m0
+      write_sub<Tag, WIN>(buf, lane, nxt);
+      if (j + 1 < nsub) load_sub<Tag, WIN>(a, x, c, m0 + 16, mw - 16, lane, nxt);
       Frag af[S_];
 #pragma unroll
       for (int s = 0; s < S_; ++s)
         af[s] = *reinterpret_cast<const Frag *>(&rowp[ln * LDSW + s * 32 + 8 * g]);
       S *outp = rowp + (4 * g) * LDSW + ln;
+      // Output tiles t and t+1 use the even and the odd fragments: two
+      // independent accumulation chains.  Walking t upwards, fragment q is
+      // first needed at t = max(0, NT-1-q) (same parity) and last at
+      // 2(S-1) + NT-1-q: it is read from LDS when first needed, so only about
+      // 2S fragments are live at once.
+      Frag bf[NB];
 #pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      for (int t0 = 0; t0 < NT; t0 += 2) {
 #pragma unroll
-        for (int s = 0; s < S_; ++s) acc = mma<Tag>(af[s], bf[2 * s - t + NT - 1], acc);
-        const uint32_t lo = pack2<Tag>(acc[0], acc[1]);
-        const uint32_t hi = pack2<Tag>(acc[2], acc[3]);
-        outp[0 * LDSW + 16 * t] = (u16)(lo & 0xffffu);
-        outp[1 * LDSW + 16 * t] = (u16)(lo >> 16);
-        outp[2 * LDSW + 16 * t] = (u16)(hi & 0xffffu);
-        outp[3 * LDSW + 16 * t] = (u16)(hi >> 16);
+        for (int q = 0; q < NB; ++q) {
+          const int tf = NT - 1 - q;  // smallest t with this parity using q
+          const int first_t = tf >= 0 ? tf : (((-tf) & 1) ? 1 : 0);
+          if (first_t == t0 || first_t == t0 + 1) bf[q] = load_bf(q);
+        }
+        f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < S_; ++s) {
+          acc0 = mma<Tag>(af[s], bf[2 * s - t0 + NT - 1], acc0);
+          if (t0 + 1 < NT) acc1 = mma<Tag>(af[s], bf[2 * s - t0 - 1 + NT - 1], acc1);
+        }
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int t = t0 + h;
+          if (t >= NT) continue;
+          const f32x4 acc = h ? acc1 : acc0;
+          const uint32_t lo = pack2<Tag>(acc[0], acc[1]);
+          const uint32_t hi = pack2<Tag>(acc[2], acc[3]);
+          outp[0 * LDSW + 16 * t] = (u16)(lo & 0xffffu);
+          outp[1 * LDSW + 16 * t] = (u16)(lo >> 16);
+          outp[2 * LDSW + 16 * t] = (u16)(hi & 0xffffu);
+          outp[3 * LDSW + 16 * t] = (u16)(hi >> 16);
+        }
       }
+      store_sub<Tag, WIN>(a, y, c, m0, mw, lane, buf);
     }
   } else {
     constexpr int S_ = G::S, NT = G::NT;
-    for (int sub = wave; sub < nsub; sub += kWaves) {
-      S *rowp = tile + (sub * 16) * LDSW;
+    for (int j = 0; j < nsub; ++j) {
+      const int64_t m0 = n0 + (first + j) * 16;
+      const int mw = nwin - (first + j) * 16;
+      write_sub<Tag, WIN>(buf, lane, nxt);
+      if (j + 1 < nsub) load_sub<Tag, WIN>(a, x, c, m0 + 16, mw - 16, lane, nxt);
       float af[S_];
 #pragma unroll
       for (int s = 0; s < S_; ++s) af[s] = rowp[ln * LDSW + 4 * s + g];
@@ -463,26 +538,7 @@ __global__ __launch_bounds__(kThreads) void wbmm_fwd_kernel(const typename Tag::
 #pragma unroll
         for (int rr = 0; rr < 4; ++rr) outp[rr * LDSW + 16 * t] = acc[rr];
       }
-    }
-  }
-  __syncthreads();
-
-  // ---- 5. window-major LDS tile -> global rows
-  {
-    const int nrows = nwin * WIN;
-    for (int q = tid; q < nrows; q += kThreads) {
-      const int v = q / WIN;
-      const int hi = q - v * WIN;
-      const Row<WIN, ES> r = row_of<WIN, ES>(a, y, c, n0 + v, hi);
-      if (r.mode == kNone) continue;
-      const uint32_t *l4 = reinterpret_cast<const uint32_t *>(smem + (v * LDSW + hi * RP) * ES);
-      uint32_t d[RD::ND];
-#pragma unroll
-      for (int i = 0; i < RD::ND; i += 4) {
-        const uint4 u = *reinterpret_cast<const uint4 *>(l4 + i);
-        d[i] = u.x; d[i + 1] = u.y; d[i + 2] = u.z; d[i + 3] = u.w;
-      }
-      store_row<WIN, ES>(y, r, d);
+      store_sub<Tag, WIN>(a, y, c, m0, mw, lane, buf);
     }
   }
 }
@@ -629,7 +685,8 @@ __device__ inline u16x8 dt_frag16(const unsigned char *buf, int pt, int lane) {
 
 template <class Tag, int WIN, int WAVE>
 __device__ __attribute__((always_inline)) void dt_wave(const typename Tag::S *__restrict__ x, const typename Tag::S *__restrict__ dy,
-                        float *__restrict__ out, const KArgs &a, unsigned char *smem) {
+                        float *__restrict__ dt, float *__restrict__ part, unsigned *__restrict__ cnt,
+                        const KArgs &a, unsigned char *smem) {
   typedef typename Tag::Frag Frag;
   typedef DtCfg<Tag, WIN> G;
   constexpr int NPT = G::NPT, CW = G::CW, RP = G::RP, R = G::R;
@@ -753,6 +810,9 @@ __device__ __attribute__((always_inline)) void dt_wave(const typename Tag::S *__
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
   __syncthreads();
+  // this slab's table gradient: combine the (P, sub-row offset) bins of each
+  // offset (dh, dw) in a fixed order
+  const bool single = a.tiles_per_ch == 1;
   for (int k = tid; k < K2; k += kThreads) {
     const int dhi = k / K1;
     const int dwi = k - dhi * K1;
@@ -763,33 +823,50 @@ __device__ __attribute__((always_inline)) void dt_wave(const typename Tag::S *__
       if (da < -(R - 1) || da > R - 1) continue;
       s += binsum[(P + NPT - 1) * NBT + (da + R - 1) * K1 + dwi];
     }
-    out[(slab * a.C + c) * K2 + k] = s;
+    if (single) {
+      dt[c * K2 + k] = s;
+    } else {
+      // device-coherent store: written through to where every XCD reads it
+      __hip_atomic_store(&part[(slab * a.C + c) * K2 + k], s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
+  if (single) return;
+  // Several slabs per channel: the last workgroup of the channel to finish
+  // (ticket from the channel's counter) sums the slabs' partials in slab
+  // order and resets the counter, so the result does not depend on timing.
+  // The partial stores are device-coherent; waiting for their completion
+  // before the barrier orders them before the ticket without a cache
+  // write-back.
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  int *flag = reinterpret_cast<int *>(smem);
+  if (tid == 0) {
+    const unsigned ticket = __hip_atomic_fetch_add(&cnt[c], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    *flag = ticket == (unsigned)(a.tiles_per_ch - 1);
+  }
+  __syncthreads();
+  if (*flag == 0) return;
+  for (int k = tid; k < K2; k += kThreads) {
+    float s = 0.f;
+    for (int j = 0; j < a.tiles_per_ch; ++j)
+      s += __hip_atomic_load(&part[((int64_t)j * a.C + c) * K2 + k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    dt[c * K2 + k] = s;
+  }
+  if (tid == 0) __hip_atomic_store(&cnt[c], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 template <class Tag, int WIN>
 __global__ __launch_bounds__(kThreads, 3) void wbmm_dt_kernel(const typename Tag::S *__restrict__ x,
-                                                           const typename Tag::S *__restrict__ dy,
-                                                           float *__restrict__ out, KArgs a) {
+                                                              const typename Tag::S *__restrict__ dy,
+                                                              float *__restrict__ dt, float *__restrict__ part,
+                                                              unsigned *__restrict__ cnt, KArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   switch (threadIdx.x >> 6) {
-    case 0: dt_wave<Tag, WIN, 0>(x, dy, out, a, smem); break;
-    case 1: dt_wave<Tag, WIN, 1>(x, dy, out, a, smem); break;
-    case 2: dt_wave<Tag, WIN, 2>(x, dy, out, a, smem); break;
-    default: dt_wave<Tag, WIN, 3>(x, dy, out, a, smem); break;
+    case 0: dt_wave<Tag, WIN, 0>(x, dy, dt, part, cnt, a, smem); break;
+    case 1: dt_wave<Tag, WIN, 1>(x, dy, dt, part, cnt, a, smem); break;
+    case 2: dt_wave<Tag, WIN, 2>(x, dy, dt, part, cnt, a, smem); break;
+    default: dt_wave<Tag, WIN, 3>(x, dy, dt, part, cnt, a, smem); break;
   }
-}
-
-// Sum of the per-slab partials in slab order: dt[i] = sum_s ws[s][i].
-template <class Tag>
-__global__ __launch_bounds__(kThreads) void wbmm_dt_reduce_kernel(const float *__restrict__ ws,
-                                                                  float *__restrict__ dt,
-                                                                  int64_t slabs, int64_t len) {
-  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  if (i >= len) return;
-  float s = 0.f;
-  for (int64_t k = 0; k < slabs; ++k) s += ws[k * len + i];
-  dt[i] = s;
 }
 
 // ============================================================ host side
@@ -807,14 +884,14 @@ static KArgs make_args(const Geom &g) {
   return a;
 }
 
-static constexpr size_t kLdsBudget = 64 * 1024;
-
+// Windows per forward workgroup: kFwdWaves waves x sub-tiles per wave x 16.
+// More sub-tiles per wave pipeline better; small problems keep enough
+// workgroups to cover the 256 compute units.
 template <class Tag, int WIN>
 static int pick_fwd_tile(const Geom &g) {
-  int tile = rp_of(WIN) == 8 ? 128 : 64;
-  while (tile > 16 && fwd_lds_bytes<Tag, WIN>(tile) > kLdsBudget) tile /= 2;
-  while (tile > 64 && g.C * cdiv64(g.N, tile) < 1024) tile /= 2;
-  return tile;
+  int spw = rp_of(WIN) == 8 ? 4 : 2;
+  while (spw > 1 && g.C * cdiv64(g.N, 16 * kFwdWaves * spw) < 1024) spw /= 2;
+  return 16 * kFwdWaves * spw;
 }
 
 template <class Tag, int WIN>
@@ -825,11 +902,11 @@ static hipError_t run_forward(const void *x, const void *t, void *y, const Geom 
   a.tile = pick_fwd_tile<Tag, WIN>(g);
   a.tiles_per_ch = (int)cdiv64(g.N, a.tile);
   const dim3 grid((unsigned)(g.C * a.tiles_per_ch));
-  const size_t lds = fwd_lds_bytes<Tag, WIN>(a.tile);
+  const size_t lds = fwd_lds_bytes<Tag, WIN>();
   if (rev)
-    wbmm_fwd_kernel<Tag, WIN, true><<<grid, dim3(kThreads), lds, st>>>((const S *)x, (const S *)t, (S *)y, a);
+    wbmm_fwd_kernel<Tag, WIN, true><<<grid, dim3(kFwdThreads), lds, st>>>((const S *)x, (const S *)t, (S *)y, a);
   else
-    wbmm_fwd_kernel<Tag, WIN, false><<<grid, dim3(kThreads), lds, st>>>((const S *)x, (const S *)t, (S *)y, a);
+    wbmm_fwd_kernel<Tag, WIN, false><<<grid, dim3(kFwdThreads), lds, st>>>((const S *)x, (const S *)t, (S *)y, a);
   return hipGetLastError();
 }
 
@@ -846,24 +923,23 @@ static DtPlan plan_dt(const Geom &g) {
   return p;
 }
 
+// Workspace of the table gradient: per-channel counters (zero between calls)
+// followed by the per-slab partial sums.
+static size_t counter_bytes(int64_t C) { return (size_t)((C * 4 + 255) / 256 * 256); }
+
 template <class Tag, int WIN>
 static hipError_t run_dtable(const void *x, const void *dy, float *dt, void *ws, const Geom &g,
                              hipStream_t st) {
   typedef typename Tag::S S;
-  typedef DtCfg<Tag, WIN> G;
   KArgs a = make_args(g);
   const DtPlan p = plan_dt<Tag, WIN>(g);
   a.tile = (int)p.slab_windows;
   a.tiles_per_ch = (int)p.slabs;
-  float *out = p.slabs > 1 ? (float *)ws : dt;
+  unsigned *cnt = p.slabs > 1 ? (unsigned *)ws : nullptr;
+  float *part = p.slabs > 1 ? (float *)((char *)ws + counter_bytes(g.C)) : nullptr;
   const size_t lds = dt_lds_bytes<Tag, WIN>();
   wbmm_dt_kernel<Tag, WIN><<<dim3((unsigned)(g.C * p.slabs)), dim3(kThreads), lds, st>>>(
-      (const S *)x, (const S *)dy, out, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || p.slabs == 1) return e;
-  const int64_t len = g.C * G::K2;
-  wbmm_dt_reduce_kernel<Tag><<<dim3((unsigned)cdiv64(len, kThreads)), dim3(kThreads), 0, st>>>(
-      (const float *)ws, dt, p.slabs, len);
+      (const S *)x, (const S *)dy, dt, part, cnt, a);
   return hipGetLastError();
 }
 

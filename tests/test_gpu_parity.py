@@ -207,7 +207,7 @@ def test_gpu_error_paths():
         W.wbmm_forward(x, t, 7, out=x)  # output aliases the input
     big = torch.zeros((64, 192, 28, 28), dtype=torch.bfloat16, device="cuda")
     need = W.wbmm_backward_table_workspace_bytes(big.shape, 14, big.dtype)
-    ws = torch.empty(need - 4, dtype=torch.uint8, device="cuda")
+    ws = W.new_workspace(need - 4)
     with pytest.raises(W.WbmmError):
         W.wbmm_backward_table(big, big.clone(), 14, workspace=ws)
 
@@ -220,7 +220,7 @@ def test_hip_graph_replay_matches_eager():
     d = synth.draw_workload(wl, seed=2)
     x, t, dy = (to_device(d[k], "bf16") for k in ("x", "t", "dy"))
     need = W.wbmm_backward_table_workspace_bytes(x.shape, 14, x.dtype)
-    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    ws = W.new_workspace(need)
     y, dx = torch.empty_like(x), torch.empty_like(dy)
     dt = torch.empty((wl.C, wl.table_len), dtype=torch.float32, device="cuda")
     ref = (W.wbmm_forward(x, t, 14), W.wbmm_backward_input(dy, t, 14),
@@ -241,3 +241,24 @@ def test_hip_graph_replay_matches_eager():
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(y, ref[0]) and torch.equal(dx, ref[1]) and torch.equal(dt, ref[2]), rep
+
+
+def test_workspace_counters_reset_between_calls():
+    """The table gradient leaves its per-channel counters at zero: one zeroed
+    workspace serves repeated calls and smaller shapes, bit for bit."""
+    big = synth.WORKLOADS["bf16_b16_c64_112_w14"]
+    d = synth.draw_workload(big, seed=5)
+    x, dy = (to_device(d[k], "bf16") for k in ("x", "dy"))
+    need = W.wbmm_backward_table_workspace_bytes(x.shape, 14, x.dtype)
+    ws = W.new_workspace(need)
+    ref = W.wbmm_backward_table(x, dy, 14, workspace=W.new_workspace(need))
+    for _ in range(3):
+        got = W.wbmm_backward_table(x, dy, 14, workspace=ws)
+        torch.cuda.synchronize()
+        assert torch.equal(got, ref)
+    counters = ws[: 4 * big.C].view(torch.int32)
+    assert int(counters.abs().sum()) == 0
+    xs, dys = x[:, :48].contiguous(), dy[:, :48].contiguous()
+    small = W.wbmm_backward_table(xs, dys, 14, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(small, ref[:48])
