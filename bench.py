@@ -40,7 +40,41 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cold", action="store_true",
                    help="rotate through enough input sets to defeat the 256 MB Infinity Cache")
+    p.add_argument("--eager", action="store_true",
+                   help="launch without HIP graphs (for hardware-counter runs)")
+    p.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
+                   help="only run a plain device copy of BYTES bytes (counter calibration)")
     return p.parse_args()
+
+
+# HBM traffic of the dominant kernel, from two rocprofv3 --pmc runs (FETCH_SIZE,
+# WRITE_SIZE; KiB per dispatch) scaled by what the same counters read for a
+# plain copy of known size.  Valid only for the kernel source it was measured
+# on (sha256 of the kernel header); otherwise reported as null.
+TRAFFIC = {
+    # (workload, pass): measured bytes per dispatch (profiles/wbmm_traffic_*.txt)
+    ("bf16_b64_c192_28_w14", "dt"): {"source": "493257aa57539cd7", "bytes": 47474908},
+    ("bf16_b64_c192_28_w14", "fwd"): {"source": "493257aa57539cd7", "bytes": 41097714},
+    ("bf16_b64_c192_28_w14", "dx"): {"source": "493257aa57539cd7", "bytes": 41109816},
+}
+
+
+def kernel_source_hash():
+    import hashlib
+    path = os.path.join(ROOT, "paper_2607_02097_amd", "csrc", "wbmm_kernels.h")
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def calibrate_copy(nbytes, steps):
+    import torch
+    dev = torch.device("cuda:0")
+    a = torch.ones(nbytes // 2, dtype=torch.bfloat16, device=dev)
+    b = torch.empty_like(a)
+    for _ in range(steps):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration": "copy", "bytes_read": a.numel() * 2,
+                      "bytes_written": b.numel() * 2, "launches": steps}))
 
 
 def pass_bytes(wl, p, es):
@@ -60,6 +94,10 @@ def main():
               "with no collective, so there is no multi-GPU step to time "
               "(asked for --gpus %d, WORLD_SIZE=%d)" % (args.gpus, world), file=sys.stderr)
         sys.exit(2)
+
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy, max(args.steps, 1))
+        return
 
     import numpy as np
     import torch
@@ -136,50 +174,71 @@ def main():
 
     # HIP graphs: R consecutive steps per graph (and R launches per pass graph)
     R = 10
-
-    def capture(seq):
-        g = torch.cuda.CUDAGraph()
-        cs = torch.cuda.Stream(dev)
-        cs.wait_stream(stream)
-        with torch.cuda.graph(g, stream=cs):
-            for i, p in enumerate(seq):
-                launch(p, i // len(passes) if len(seq) > R else i)
-        stream.wait_stream(cs)
-        torch.cuda.synchronize()
-        return g
-
-    g_step = capture([p for _ in range(R) for p in passes])
-    g_pass = {p: capture([p] * R) for p in passes}
-    for _ in range(3):
-        g_step.replay()
-        for p in passes:
-            g_pass[p].replay()
-    torch.cuda.synchronize()
-
-    # timed region: K steps = K/R replays of the step graph, bracketed by
-    # synchronisation; then each pass graph timed with HIP events on the
-    # same stream to get the average duration of each kernel launch
     reps = max(1, args.steps // R)
     steps = reps * R
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_start.record(stream)
-    for _ in range(reps):
-        g_step.replay()
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    total_ms = t_start.elapsed_time(t_end)
-    ms_step = total_ms / steps
-    per_pass = {}
-    for p in passes:
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        for _ in range(reps):
-            g_pass[p].replay()
-        b.record(stream)
+
+    if args.eager:
+        # plain stream launches (hardware-counter runs serialise dispatches)
+        t_start = torch.cuda.Event(enable_timing=True)
+        t_end = torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
-        per_pass[p] = a.elapsed_time(b) / (reps * R)
+        t_start.record(stream)
+        for i in range(steps):
+            for p in passes:
+                launch(p, i)
+        t_end.record(stream)
+        torch.cuda.synchronize()
+        ms_step = t_start.elapsed_time(t_end) / steps
+        per_pass = {}
+        for p in passes:
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for i in range(steps):
+                launch(p, i)
+            b.record(stream)
+            torch.cuda.synchronize()
+            per_pass[p] = a.elapsed_time(b) / steps
+    else:
+        def capture(seq, per_step):
+            g = torch.cuda.CUDAGraph()
+            cs = torch.cuda.Stream(dev)
+            cs.wait_stream(stream)
+            with torch.cuda.graph(g, stream=cs):
+                for i, p in enumerate(seq):
+                    launch(p, i // per_step)
+            stream.wait_stream(cs)
+            torch.cuda.synchronize()
+            return g
+
+        g_step = capture([p for _ in range(R) for p in passes], len(passes))
+        g_pass = {p: capture([p] * R, 1) for p in passes}
+        for _ in range(3):
+            g_step.replay()
+            for p in passes:
+                g_pass[p].replay()
+        torch.cuda.synchronize()
+
+        # timed region: K steps = K/R replays of the step graph, bracketed by
+        # synchronisation; then each pass graph timed with HIP events on the
+        # same stream to get the average duration of each kernel launch
+        t_start = torch.cuda.Event(enable_timing=True)
+        t_end = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t_start.record(stream)
+        for _ in range(reps):
+            g_step.replay()
+        t_end.record(stream)
+        torch.cuda.synchronize()
+        ms_step = t_start.elapsed_time(t_end) / steps
+        per_pass = {}
+        for p in passes:
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for _ in range(reps):
+                g_pass[p].replay()
+            b.record(stream)
+            torch.cuda.synchronize()
+            per_pass[p] = a.elapsed_time(b) / (reps * R)
     args.steps = steps
 
     flops = wl.flops()
@@ -193,8 +252,9 @@ def main():
     dom_flops = wl.flops((dom,))
     ai = dom_flops / dom_bytes
     ridge = peak * 1e12 / (HBM_PEAK_GBS * 1e9)
-    kernel_name = {"fwd": "wbmm_fwd_kernel", "dx": "wbmm_fwd_kernel(reversed table)",
-                   "dt": "wbmm_dt_kernel+wbmm_dt_reduce_kernel"}[dom]
+    kernel_name = {"fwd": "wbmm_fwd_kernel<%s,%d,false>", "dx": "wbmm_fwd_kernel<%s,%d,true>",
+                   "dt": "wbmm_dt_kernel<%s,%d>"}[dom] % ({"bf16": "TagBF16", "f16": "TagF16",
+                                                          "f32": "TagF32"}[wl.dtype], wl.w)
     if ai < ridge:
         achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
@@ -203,7 +263,11 @@ def main():
         achieved = dom_flops / (dom_ms * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
                 "unit": "TFLOP/s", "frac": round(achieved / peak, 4)}
-    roof.update({"traffic": None, "kernel": kernel_name, "pass": dom,
+    tr = TRAFFIC.get((wl.name, dom))
+    traffic = None
+    if tr is not None and tr["source"] == kernel_source_hash():
+        traffic = tr["bytes"]
+    roof.update({"traffic": traffic, "kernel": kernel_name, "pass": dom,
                  "avg_ms": round(dom_ms, 5), "algorithmic_bytes": dom_bytes,
                  "algorithmic_flops": dom_flops})
 
@@ -239,7 +303,7 @@ def main():
                    "passes": list(passes), "cold_cache": bool(args.cold), "input_sets": nsets},
         "pct_bf16_mfma_peak": round(100 * tflops / peak, 3),
         "per_pass_ms": {k: round(v, 5) for k, v in per_pass.items()},
-        "launch": "HIP graph replay, %d steps per graph" % R,
+        "launch": "eager stream launches" if args.eager else "HIP graph replay, %d steps per graph" % R,
         "eager_ms_per_step": round(eager_ms, 5),
         "roofline": roof,
         "cpu_baseline": cpu,
