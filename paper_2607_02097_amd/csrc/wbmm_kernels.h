@@ -160,7 +160,7 @@ struct Row {
 };
 
 template <int WIN, int ES>
-__device__ inline Row<WIN, ES> row_of(const KArgs &a, const void *base, int64_t c, int64_t n, int hi) {
+__device__ __attribute__((always_inline)) inline Row<WIN, ES> row_of(const KArgs &a, const void *base, int64_t c, int64_t n, int hi) {
   Row<WIN, ES> r;
   r.eoff = 0;
   r.cols = 0;
@@ -203,7 +203,7 @@ struct RowData {
 
 // Load a window row: columns >= cols and padded columns read as zero.
 template <int WIN, int ES>
-__device__ inline void load_row(const void *base, const Row<WIN, ES> &r, RowData<WIN, ES> &o) {
+__device__ __attribute__((always_inline)) inline void load_row(const void *base, const Row<WIN, ES> &r, RowData<WIN, ES> &o) {
   constexpr int ND = RowData<WIN, ES>::ND;
   constexpr int NDV = (WIN * ES) / 4;  // data dwords of a whole aligned row
 #pragma unroll
@@ -251,7 +251,7 @@ __device__ inline void load_row(const void *base, const Row<WIN, ES> &r, RowData
 
 // Store the first cols elements of a padded row held as dwords.
 template <int WIN, int ES>
-__device__ inline void store_row(void *base, const Row<WIN, ES> &r, const uint32_t *d) {
+__device__ __attribute__((always_inline)) inline void store_row(void *base, const Row<WIN, ES> &r, const uint32_t *d) {
   constexpr int NDV = (WIN * ES) / 4;
   if (r.mode == kNone) return;
   char *p = reinterpret_cast<char *>(base) + r.eoff * ES;
@@ -309,7 +309,7 @@ struct FwdCfg {
   static constexpr int TB_LEN = Tag::W16 ? K1 * RP * RP : 0;
 };
 
-// The forward kernel runs two waves per workgroup.  Each wave owns a run of
+// The forward kernel runs four waves per workgroup.  Each wave owns a run of
 // 16-window sub-tiles and pipelines them through one private LDS buffer: the
 // rows of sub-tile j+1 are loaded into registers while sub-tile j is
 // multiplied and its rows are stored, so reads and writes of the whole grid
@@ -324,6 +324,13 @@ __host__ __device__ constexpr size_t fwd_lds_bytes() {
   return (size_t)kFwdWaves * 16 * G::LDSW * Tag::ES + (size_t)(G::TS_LEN + G::TB_LEN) * Tag::ES;
 }
 
+// Wave-level ordering of LDS accesses made by different lanes of one wave.
+__device__ __attribute__((always_inline)) inline void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // Row copies of one sub-tile (16 windows x KR padded rows) spread over the 64
 // lanes of a wave; rows of one window are consecutive.
 template <class Tag, int WIN>
@@ -334,7 +341,7 @@ struct SubRows {
 };
 
 template <class Tag, int WIN>
-__device__ inline void load_sub(const KArgs &a, const void *x, int64_t c, int64_t m0, int nwin, int lane,
+__device__ __attribute__((always_inline)) inline void load_sub(const KArgs &a, const void *x, int64_t c, int64_t m0, int nwin, int lane,
                                 SubRows<Tag, WIN> &o) {
   constexpr int KR = FwdCfg<Tag, WIN>::KR;
 #pragma unroll
@@ -350,7 +357,7 @@ __device__ inline void load_sub(const KArgs &a, const void *x, int64_t c, int64_
 }
 
 template <class Tag, int WIN>
-__device__ inline void write_sub(unsigned char *buf, int lane, const SubRows<Tag, WIN> &o) {
+__device__ __attribute__((always_inline)) inline void write_sub(unsigned char *buf, int lane, const SubRows<Tag, WIN> &o) {
   typedef FwdCfg<Tag, WIN> G;
   typedef RowData<WIN, Tag::ES> RD;
 #pragma unroll
@@ -367,7 +374,7 @@ __device__ inline void write_sub(unsigned char *buf, int lane, const SubRows<Tag
 }
 
 template <class Tag, int WIN>
-__device__ inline void store_sub(const KArgs &a, void *y, int64_t c, int64_t m0, int nwin, int lane,
+__device__ __attribute__((always_inline)) inline void store_sub(const KArgs &a, void *y, int64_t c, int64_t m0, int nwin, int lane,
                                  const unsigned char *buf) {
   typedef FwdCfg<Tag, WIN> G;
   typedef RowData<WIN, Tag::ES> RD;
@@ -420,8 +427,12 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
   SubRows<Tag, WIN> nxt;
   if (nsub > 0) load_sub<Tag, WIN>(a, x, c, n0 + first * 16, nwin - first * 16, lane, nxt);
   {
+    // the table row moves with coalesced loads; the Toeplitz blocks are then
+    // gathered from its LDS copy
     const S *tc = tab + c * K2;
+    for (int k = tid; k < K2; k += kFwdThreads) Ts[k] = tc[REV ? K2 - 1 - k : k];
     if constexpr (Tag::W16) {
+      __syncthreads();
       constexpr int CPR = RP / 8;               // 8-element chunks per TB row
       constexpr int NCH = K1 * RP * CPR;
       for (int ch = tid; ch < NCH; ch += kFwdThreads) {
@@ -435,15 +446,12 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
             const int xi = xi0 + e < WIN ? xi0 + e : WIN - 1;
-            const int k = k0 + xi;
-            const u16 t = tc[REV ? K2 - 1 - k : k];
+            const u16 t = Ts[k0 + xi];
             v[e] = xi0 + e < WIN ? t : (u16)0;
           }
         }
         *reinterpret_cast<u16x8 *>(&TB[row * RP + xi0]) = v;
       }
-    } else {
-      for (int k = tid; k < K2; k += kFwdThreads) Ts[k] = tc[REV ? K2 - 1 - k : k];
     }
   }
   __syncthreads();
@@ -506,8 +514,31 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
           outp[2 * LDSW + 16 * t] = (u16)(hi & 0xffffu);
           outp[3 * LDSW + 16 * t] = (u16)(hi >> 16);
         }
+        // small windows: the window rows of output tiles t0 and t0+1 are
+        // final; storing them now overlaps the stores with the products of
+        // the next tiles (large windows store the sub-tile at the end, which
+        // keeps their registers within three waves per SIMD)
+        if constexpr (RP == 8) {
+          wave_lds_sync();
+          constexpr int RPT = 16 / RP;  // window rows per output tile
+          const int v = lane & 15;
+          const int hr = t0 * RPT + (lane >> 4);
+          if ((lane >> 4) < 2 * RPT && hr < WIN && v < mw) {
+            const Row<WIN, Tag::ES> r = row_of<WIN, Tag::ES>(a, y, c, m0 + v, hr);
+            if (r.mode != kNone) {
+              const uint32_t *l4 = reinterpret_cast<const uint32_t *>(buf + (v * LDSW + hr * RP) * Tag::ES);
+              uint32_t dd[RowData<WIN, Tag::ES>::ND];
+#pragma unroll
+              for (int i = 0; i < RowData<WIN, Tag::ES>::ND; i += 4) {
+                const uint4 u4 = *reinterpret_cast<const uint4 *>(l4 + i);
+                dd[i] = u4.x; dd[i + 1] = u4.y; dd[i + 2] = u4.z; dd[i + 3] = u4.w;
+              }
+              store_row<WIN, Tag::ES>(y, r, dd);
+            }
+          }
+        }
       }
-      store_sub<Tag, WIN>(a, y, c, m0, mw, lane, buf);
+      if constexpr (RP != 8) store_sub<Tag, WIN>(a, y, c, m0, mw, lane, buf);
     }
   } else {
     constexpr int S_ = G::S, NT = G::NT;
@@ -605,11 +636,21 @@ __host__ __device__ constexpr PRange make_prange() {
   return r;
 }
 
+// Largest number of accumulator tiles a wave owns.
+template <int NPT>
+__host__ __device__ constexpr int max_tiles_per_wave() {
+  constexpr PRange r = make_prange<NPT>();
+  int m = 1;
+  for (int w = 0; w < kWaves; ++w)
+    if (r.hi[w] - r.lo[w] + 1 > m) m = r.hi[w] - r.lo[w] + 1;
+  return m;
+}
+
 template <class Tag, int WIN>
 __host__ __device__ constexpr size_t dt_lds_bytes() {
   typedef DtCfg<Tag, WIN> G;
   const size_t ops = 2 * (size_t)G::BUF;
-  const size_t bins = (size_t)(kWaves * 2 * 16 * 17 + G::NACC * G::NBT) * 4;
+  const size_t bins = (size_t)(kWaves * max_tiles_per_wave<G::NPT>() * 16 * 17 + G::NACC * G::NBT) * 4;
   return ops > bins ? ops : bins;
 }
 
@@ -622,7 +663,7 @@ struct DtStage {
 };
 
 template <class Tag, int WIN>
-__device__ inline void dt_load_stage(const KArgs &a, const void *x, const void *dy, int64_t c, int64_t m0,
+__device__ __attribute__((always_inline)) inline void dt_load_stage(const KArgs &a, const void *x, const void *dy, int64_t c, int64_t m0,
                                      int64_t m1, int tid, DtStage<Tag, WIN> &st) {
   typedef DtCfg<Tag, WIN> G;
 #pragma unroll
@@ -642,7 +683,7 @@ __device__ inline void dt_load_stage(const KArgs &a, const void *x, const void *
 
 // Write a loaded stage window-major (padded rows, as in the forward tile).
 template <class Tag, int WIN>
-__device__ inline void dt_write_stage(unsigned char *smem, int tid, const DtStage<Tag, WIN> &st) {
+__device__ __attribute__((always_inline)) inline void dt_write_stage(unsigned char *smem, int tid, const DtStage<Tag, WIN> &st) {
   typedef DtCfg<Tag, WIN> G;
   typedef RowData<WIN, Tag::ES> RD;
 #pragma unroll
@@ -670,7 +711,7 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 // row r is the 4-element chunks of lanes 4r .. 4r + 3; lane 4r + q points at
 // window 8g + r (+4), positions 16 * pt + 4q .. + 3.
 template <class Tag, int WIN>
-__device__ inline u16x8 dt_frag16(const unsigned char *buf, int pt, int lane) {
+__device__ __attribute__((always_inline)) inline u16x8 dt_frag16(const unsigned char *buf, int pt, int lane) {
   typedef DtCfg<Tag, WIN> G;
   const int g = lane >> 4;
   const int i = lane & 15;
@@ -765,31 +806,29 @@ __device__ __attribute__((always_inline)) void dt_wave(const typename Tag::S *__
   }
   __syncthreads();
 
-  // ---- diagonal binning, two accumulator tiles per round, fixed order.
-  // Bin (da, dw) of tile P sums the elements (ra*RP + xo + dw, rb*RP + xo)
-  // with ra - rb = da over xo; every lane issues all its reads at once
-  // (out-of-range terms read a valid slot and are masked to zero).
-  float *scr = reinterpret_cast<float *>(smem) + WAVE * 2 * 16 * 17;
-  float *binsum = reinterpret_cast<float *>(smem) + kWaves * 2 * 16 * 17;
+  // ---- diagonal binning, fixed order.  Every tile of the wave goes to LDS
+  // at once; bin (da, dw) of tile P sums the elements
+  // (ra*RP + xo + dw, rb*RP + xo) with ra - rb = da over xo, and every lane
+  // issues the reads of all its bins at once (out-of-range terms read a valid
+  // slot and are masked to zero).
+  constexpr int NPM = max_tiles_per_wave<NPT>();
+  float *scr = reinterpret_cast<float *>(smem) + WAVE * NPM * 272;
+  float *binsum = reinterpret_cast<float *>(smem) + kWaves * NPM * 272;
 #pragma unroll
-  for (int j0 = 0; j0 < NP; j0 += 2) {
+  for (int j = 0; j < NP; ++j) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      if (j0 + h < NP) {
+    for (int rr = 0; rr < 4; ++rr) scr[j * 272 + (4 * g + rr) * 17 + ln] = acc[j][rr];
+  }
+  wave_lds_sync();
 #pragma unroll
-        for (int rr = 0; rr < 4; ++rr) scr[h * 272 + (4 * g + rr) * 17 + ln] = acc[j0 + h][rr];
-      }
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    const int nb2 = (j0 + 1 < NP ? 2 : 1) * NBT;
-    for (int b2 = lane; b2 < nb2; b2 += 64) {
-      const int h = b2 >= NBT ? 1 : 0;
-      const int bin = b2 - h * NBT;
+  for (int it = 0; it < cdiv(NP * NBT, 64); ++it) {
+    const int b2 = lane + 64 * it;
+    if (b2 < NP * NBT) {
+      const int j = b2 / NBT;
+      const int bin = b2 - j * NBT;
       const int da = bin / K1 - (R - 1);  // input sub-row minus output sub-row
       const int dw = bin - (bin / K1) * K1 - (WIN - 1);
-      const float *t = scr + h * 272;
+      const float *t = scr + j * 272;
       float sum = 0.f;
 #pragma unroll
       for (int ra = 0; ra < R; ++ra) {
@@ -803,11 +842,8 @@ __device__ __attribute__((always_inline)) void dt_wave(const typename Tag::S *__
           sum += ok ? v : 0.f;
         }
       }
-      binsum[(PLO + j0 + h + NPT - 1) * NBT + bin] = sum;
+      binsum[(PLO + j + NPT - 1) * NBT + bin] = sum;
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
   __syncthreads();
   // this slab's table gradient: combine the (P, sub-row offset) bins of each
@@ -846,11 +882,35 @@ __device__ __attribute__((always_inline)) void dt_wave(const typename Tag::S *__
   }
   __syncthreads();
   if (*flag == 0) return;
-  for (int k = tid; k < K2; k += kThreads) {
-    float s = 0.f;
-    for (int j = 0; j < a.tiles_per_ch; ++j)
-      s += __hip_atomic_load(&part[((int64_t)j * a.C + c) * K2 + k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    dt[c * K2 + k] = s;
+  // all loads of a group of slabs are issued before the sums, which keep
+  // the slab order
+  constexpr int KPT = cdiv(K2, kThreads);
+  constexpr int SG = 8;
+  float s[KPT];
+#pragma unroll
+  for (int i = 0; i < KPT; ++i) s[i] = 0.f;
+  for (int j0 = 0; j0 < a.tiles_per_ch; j0 += SG) {
+    float v[KPT][SG];
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int k = tid + i * kThreads;
+#pragma unroll
+      for (int j = 0; j < SG; ++j)
+        v[i][j] = (k < K2 && j0 + j < a.tiles_per_ch)
+                      ? __hip_atomic_load(&part[((int64_t)(j0 + j) * a.C + c) * K2 + k], __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT)
+                      : 0.f;
+    }
+#pragma unroll
+    for (int i = 0; i < KPT; ++i)
+#pragma unroll
+      for (int j = 0; j < SG; ++j)
+        if (j0 + j < a.tiles_per_ch) s[i] += v[i][j];
+  }
+#pragma unroll
+  for (int i = 0; i < KPT; ++i) {
+    const int k = tid + i * kThreads;
+    if (k < K2) dt[c * K2 + k] = s[i];
   }
   if (tid == 0) __hip_atomic_store(&cnt[c], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
