@@ -3,8 +3,11 @@
 
 One step = forward + input gradient + table gradient (all three passes of the
 operator) over one batch of seeded synthetic input already resident in device
-memory.  The headline workload is the w=14 stage shape B=64, C=192, H=W=28 in
-bfloat16 with float32 accumulation.
+memory: the forward kernel, then the fused backward kernel, which computes
+both gradients from one read of x and dy.  The headline workload is the w=14
+stage shape B=64, C=192, H=W=28 in bfloat16 with float32 accumulation.  The
+separate input- and table-gradient kernels are timed as well and reported
+beside the step (per_pass_ms).
 
 Prints ONE JSON line with the throughput (algorithmic TFLOP/s, 6*C*N*d^2 per
 step), the roofline of the dominant kernel (timed live with HIP events on the
@@ -53,9 +56,6 @@ def parse():
 # on (sha256 of the kernel header); otherwise reported as null.
 TRAFFIC = {
     # (workload, pass): measured bytes per dispatch (profiles/wbmm_traffic_*.txt)
-    ("bf16_b64_c192_28_w14", "dt"): {"source": "493257aa57539cd7", "bytes": 47474908},
-    ("bf16_b64_c192_28_w14", "fwd"): {"source": "493257aa57539cd7", "bytes": 41097714},
-    ("bf16_b64_c192_28_w14", "dx"): {"source": "493257aa57539cd7", "bytes": 41109816},
 }
 
 
@@ -78,12 +78,18 @@ def calibrate_copy(nbytes, steps):
 
 
 def pass_bytes(wl, p, es):
-    """Algorithmic bytes of one pass (each tensor touched once)."""
+    """Algorithmic bytes of one kernel (each tensor touched once)."""
     act = wl.B * wl.C * wl.H * wl.W * es
     tab = wl.C * wl.table_len
     if p in ("fwd", "dx"):
         return 2 * act + tab * es          # read input, write output, read table
-    return 2 * act + tab * 4               # read x and dy, write float32 dtable
+    if p == "dt":
+        return 2 * act + tab * 4           # read x and dy, write float32 dtable
+    return 3 * act + tab * es + tab * 4    # fused: read x, dy, table; write dx, dtable
+
+
+def pass_flops(wl, p):
+    return wl.flops(("dx", "dt") if p == "bwd" else (p,))
 
 
 def main():
@@ -121,7 +127,7 @@ def main():
 
     nsets = 1
     if args.cold:
-        per = 3 * wl.B * wl.C * wl.H * wl.W * es
+        per = 4 * wl.B * wl.C * wl.H * wl.W * es  # x, dy, y, dx
         nsets = max(2, int(np.ceil(2 * 256e6 / per)) + 1)
     sets = []
     for i in range(nsets):
@@ -133,6 +139,9 @@ def main():
         sets.append((x, t, dy, y, dx, dtab, ws))
 
     passes = wl.passes
+    # kernels of one step: the fused backward covers the two gradients
+    step_kernels = ["fwd", "bwd"] if "dt" in passes else list(passes)
+    timed = step_kernels + [p for p in passes if p not in step_kernels and p != "fwd"]
     lib = W.load_library()
     code = W.DTYPE_CODES[tdt]
     import ctypes
@@ -148,15 +157,19 @@ def main():
             r = lib.wbmm_forward(vp(x.data_ptr()), vp(t.data_ptr()), vp(y.data_ptr()), *dims)
         elif p == "dx":
             r = lib.wbmm_backward_input(vp(dy.data_ptr()), vp(t.data_ptr()), vp(dx.data_ptr()), *dims)
-        else:
+        elif p == "dt":
             r = lib.wbmm_backward_table(vp(x.data_ptr()), vp(dy.data_ptr()), vp(dtab.data_ptr()),
                                         vp(ws.data_ptr()), ws.numel(), *dims)
+        else:
+            r = lib.wbmm_backward(vp(x.data_ptr()), vp(dy.data_ptr()), vp(t.data_ptr()),
+                                  vp(dx.data_ptr()), vp(dtab.data_ptr()), vp(ws.data_ptr()),
+                                  ws.numel(), *dims)
         if r != 0:
             raise RuntimeError("%s failed: %s" % (p, W.wbmm_status_string(r)))
 
     # warm-up, eager
     for i in range(args.warmup):
-        for p in passes:
+        for p in timed:
             launch(p, i)
     torch.cuda.synchronize()
 
@@ -166,7 +179,7 @@ def main():
     n_eager = min(args.steps, 50)
     e0.record(stream)
     for i in range(n_eager):
-        for p in passes:
+        for p in step_kernels:
             launch(p, i)
     e1.record(stream)
     torch.cuda.synchronize()
@@ -184,13 +197,13 @@ def main():
         torch.cuda.synchronize()
         t_start.record(stream)
         for i in range(steps):
-            for p in passes:
+            for p in step_kernels:
                 launch(p, i)
         t_end.record(stream)
         torch.cuda.synchronize()
         ms_step = t_start.elapsed_time(t_end) / steps
         per_pass = {}
-        for p in passes:
+        for p in timed:
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream)
             for i in range(steps):
@@ -210,11 +223,11 @@ def main():
             torch.cuda.synchronize()
             return g
 
-        g_step = capture([p for _ in range(R) for p in passes], len(passes))
-        g_pass = {p: capture([p] * R, 1) for p in passes}
+        g_step = capture([p for _ in range(R) for p in step_kernels], len(step_kernels))
+        g_pass = {p: capture([p] * R, 1) for p in timed}
         for _ in range(3):
             g_step.replay()
-            for p in passes:
+            for p in timed:
                 g_pass[p].replay()
         torch.cuda.synchronize()
 
@@ -231,7 +244,7 @@ def main():
         torch.cuda.synchronize()
         ms_step = t_start.elapsed_time(t_end) / steps
         per_pass = {}
-        for p in passes:
+        for p in timed:
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream)
             for _ in range(reps):
@@ -245,15 +258,15 @@ def main():
     tflops = flops / (ms_step * 1e-3) / 1e12
     peak = BF16_PEAK_TFLOPS if wl.dtype in ("bf16", "f16") else F32_PEAK_TFLOPS
 
-    # dominant kernel: the pass with the largest average duration
-    dom = max(per_pass, key=per_pass.get)
+    # dominant kernel: the step kernel with the largest average duration
+    dom = max(step_kernels, key=per_pass.get)
     dom_ms = per_pass[dom]
     dom_bytes = pass_bytes(wl, dom, es)
-    dom_flops = wl.flops((dom,))
+    dom_flops = pass_flops(wl, dom)
     ai = dom_flops / dom_bytes
     ridge = peak * 1e12 / (HBM_PEAK_GBS * 1e9)
     kernel_name = {"fwd": "wbmm_fwd_kernel<%s,%d,false>", "dx": "wbmm_fwd_kernel<%s,%d,true>",
-                   "dt": "wbmm_dt_kernel<%s,%d>"}[dom] % ({"bf16": "TagBF16", "f16": "TagF16",
+                   "dt": "wbmm_dt_kernel<%s,%d>", "bwd": "wbmm_bwd_kernel<%s,%d>"}[dom] % ({"bf16": "TagBF16", "f16": "TagF16",
                                                           "f32": "TagF32"}[wl.dtype], wl.w)
     if ai < ridge:
         achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
@@ -273,18 +286,23 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
+        # the oracle over the whole workload, repeated for about 10 s
         import oracle
-        t0 = time.perf_counter()
-        if "fwd" in passes:
-            oracle.forward(d["x64"], d["t64"], wl.w)
-        if "dx" in passes:
-            oracle.backward_input(d["dy64"], d["t64"], wl.w)
-        if "dt" in passes:
-            oracle.backward_table(d["x64"], d["dy64"], wl.w)
-        cpu_s = time.perf_counter() - t0
-        cpu = {"value": round(flops / cpu_s / 1e12, 6), "unit": "TFLOP/s",
+        reps_cpu, cpu_s = 0, 0.0
+        while cpu_s < 10.0 and reps_cpu < 200:
+            t0 = time.perf_counter()
+            if "fwd" in passes:
+                oracle.forward(d["x64"], d["t64"], wl.w)
+            if "dx" in passes:
+                oracle.backward_input(d["dy64"], d["t64"], wl.w)
+            if "dt" in passes:
+                oracle.backward_table(d["x64"], d["dy64"], wl.w)
+            cpu_s += time.perf_counter() - t0
+            reps_cpu += 1
+        cpu = {"value": round(reps_cpu * flops / cpu_s / 1e12, 6), "unit": "TFLOP/s",
                "cores": oracle.max_threads(), "kind": "oracle",
-               "sample": "whole workload, all passes (%s), fp64, %.2f s" % ("+".join(passes), cpu_s)}
+               "sample": "whole workload, all passes (%s), fp64, %d runs in %.1f s"
+                         % ("+".join(passes), reps_cpu, cpu_s)}
 
     out = {
         "metric": METRIC if args.workload == HEADLINE else "WBMM %s TFLOP/s, %s" % ("+".join(passes), args.workload),
@@ -300,7 +318,8 @@ def main():
         "dtype": wl.dtype,
         "data": "synthetic (seeded N(0,1) activations/gradients, N(0,0.02^2) table)",
         "config": {"workload": wl.name, "B": wl.B, "C": wl.C, "H": wl.H, "W": wl.W, "w": wl.w,
-                   "passes": list(passes), "cold_cache": bool(args.cold), "input_sets": nsets},
+                   "passes": list(passes), "step_kernels": step_kernels,
+                   "cold_cache": bool(args.cold), "input_sets": nsets},
         "pct_bf16_mfma_peak": round(100 * tflops / peak, 3),
         "per_pass_ms": {k: round(v, 5) for k, v in per_pass.items()},
         "launch": "eager stream launches" if args.eager else "HIP graph replay, %d steps per graph" % R,

@@ -112,6 +112,25 @@ wbmm_status wbmm_backward_table(const void *x, const void *dy, float *dtable,
                                 int64_t B, int64_t C, int64_t H, int64_t W,
                                 int w, wbmm_dtype dtype, void *stream);
 
+/* Size in bytes of the device workspace wbmm_backward needs for this shape;
+ * equal to wbmm_backward_table_workspace_bytes() (same layout and rules). */
+size_t wbmm_backward_workspace_bytes(int64_t B, int64_t C, int64_t H, int64_t W,
+                                     int w, wbmm_dtype dtype);
+
+/* Both gradients in one pass (the input gradient of wbmm_backward_input and
+ * the table gradient of wbmm_backward_table): every window of x and dy is
+ * read once.  Results equal those of the two separate calls bit for bit.
+ * x, dy, dx: [B,C,H,W] in dtype; table: [C,(2w-1)^2] in dtype; dtable: float32
+ * [C,(2w-1)^2], overwritten.  dx and dtable must not overlap any input, each
+ * other or the workspace.  workspace / workspace_bytes: as for
+ * wbmm_backward_table (counters zero at the start of a call, left zero at
+ * its end; no concurrent sharing). */
+wbmm_status wbmm_backward(const void *x, const void *dy, const void *table,
+                          void *dx, float *dtable, void *workspace,
+                          size_t workspace_bytes, int64_t B, int64_t C,
+                          int64_t H, int64_t W, int w, wbmm_dtype dtype,
+                          void *stream);
+
 /* Static description of a status code (never NULL). */
 const char *wbmm_status_string(wbmm_status s);
 

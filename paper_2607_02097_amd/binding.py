@@ -7,7 +7,8 @@ built, or a call fails, an exception is raised.
 
 Names follow the C entry points: ``wbmm_forward``, ``wbmm_backward_input``,
 ``wbmm_backward_table``, ``wbmm_backward_table_workspace_bytes``,
-``wbmm_relative_index``, ``wbmm_status_string``.
+``wbmm_backward``, ``wbmm_backward_workspace_bytes``, ``wbmm_relative_index``,
+``wbmm_status_string``.
 """
 from __future__ import annotations
 
@@ -26,7 +27,8 @@ WBMM_ERR_HIP = 3
 DTYPE_CODES = {torch.float32: 0, torch.bfloat16: 1, torch.float16: 2}
 
 EXPORTED = ("wbmm_forward", "wbmm_backward_input", "wbmm_backward_table",
-            "wbmm_backward_table_workspace_bytes", "wbmm_status_string",
+            "wbmm_backward_table_workspace_bytes", "wbmm_backward",
+            "wbmm_backward_workspace_bytes", "wbmm_status_string",
             "wbmm_relative_index", "wbmm_version")
 
 _lib = None
@@ -57,6 +59,10 @@ def load_library(path: str = LIB_PATH):
     lib.wbmm_backward_table_workspace_bytes.restype = ctypes.c_size_t
     lib.wbmm_backward_table.argtypes = [vp, vp, vp, vp, ctypes.c_size_t] + shape
     lib.wbmm_backward_table.restype = st
+    lib.wbmm_backward_workspace_bytes.argtypes = [i64, i64, i64, i64, ci, ci]
+    lib.wbmm_backward_workspace_bytes.restype = ctypes.c_size_t
+    lib.wbmm_backward.argtypes = [vp, vp, vp, vp, vp, vp, ctypes.c_size_t] + shape
+    lib.wbmm_backward.restype = st
     lib.wbmm_status_string.argtypes = [st]
     lib.wbmm_status_string.restype = ctypes.c_char_p
     lib.wbmm_relative_index.argtypes = [ci, ctypes.POINTER(ctypes.c_int32)]
@@ -191,6 +197,51 @@ def wbmm_backward_table(x: torch.Tensor, dy: torch.Tensor, w: int, out=None, wor
     return out
 
 
+def wbmm_backward_workspace_bytes(shape, w: int, dtype) -> int:
+    B, C, H, W = shape
+    return int(load_library().wbmm_backward_workspace_bytes(B, C, H, W, int(w), _code(dtype)))
+
+
+def wbmm_backward(x: torch.Tensor, dy: torch.Tensor, table: torch.Tensor, w: int, dx=None,
+                  dtable=None, workspace=None, stream=None):
+    """Both gradients in one pass: returns (dx, dtable), dx like x, dtable
+    float32 [C,(2w-1)^2] (overwritten).  ``workspace`` as for
+    ``wbmm_backward_table``."""
+    _check_tensor(x, "x")
+    _check_tensor(dy, "dy")
+    _check_tensor(table, "table")
+    if dy.shape != x.shape or dy.dtype != x.dtype or dy.device != x.device:
+        raise ValueError("dy must match x's shape, dtype and device")
+    if table.dtype != x.dtype or table.device != x.device:
+        raise ValueError("table must match x's dtype and device")
+    B, C, H, W = x.shape
+    k = (2 * int(w) - 1) ** 2
+    if dx is None:
+        dx = torch.empty_like(x)
+    else:
+        _check_tensor(dx, "dx")
+        if dx.shape != x.shape or dx.dtype != x.dtype or dx.device != x.device:
+            raise ValueError("dx must match x's shape, dtype and device")
+    if dtable is None:
+        dtable = torch.empty((C, k), dtype=torch.float32, device=x.device)
+    else:
+        _check_tensor(dtable, "dtable")
+        if dtable.dtype != torch.float32 or dtable.numel() != C * k or dtable.device != x.device:
+            raise ValueError("dtable must be float32 [C, (2w-1)^2] on x's device")
+    need = wbmm_backward_workspace_bytes(x.shape, w, x.dtype)
+    if workspace is None and need > 0:
+        workspace = _cached_workspace(x.device, need, stream, (tuple(x.shape), int(w), x.dtype))
+    ws_ptr = ctypes.c_void_p(workspace.data_ptr() if workspace is not None else 0)
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    with torch.cuda.device(x.device):
+        st = load_library().wbmm_backward(_ptr(x), _ptr(dy), _ptr(table), _ptr(dx), _ptr(dtable),
+                                          ws_ptr, ws_bytes, B, C, H, W, int(w), _code(x.dtype),
+                                          _stream(x, stream))
+    if st != WBMM_OK:
+        raise WbmmError(st, "wbmm_backward")
+    return dx, dtable
+
+
 def wbmm_relative_index(w: int) -> torch.Tensor:
     """The int32 [d, d] index I of eq. index_computation (host tensor)."""
     d = int(w) * int(w)
@@ -207,8 +258,9 @@ def wbmm_version() -> str:
 
 
 class WBMMFunction(torch.autograd.Function):
-    """Autograd composition of the three entry points (the table gradient is
-    computed in float32 and cast to the table's dtype)."""
+    """Autograd composition of the entry points: the forward, then both
+    gradients in one fused pass (or the one that is needed).  The table
+    gradient is computed in float32 and cast to the table's dtype."""
 
     @staticmethod
     def forward(ctx, x, table, w):
@@ -220,9 +272,14 @@ class WBMMFunction(torch.autograd.Function):
     def backward(ctx, dy):
         x, table = ctx.saved_tensors
         dy = dy.contiguous()
-        dx = wbmm_backward_input(dy, table, ctx.w) if ctx.needs_input_grad[0] else None
-        dt = None
-        if ctx.needs_input_grad[1]:
+        need_x, need_t = ctx.needs_input_grad[0], ctx.needs_input_grad[1]
+        dx = dt = None
+        if need_x and need_t:
+            dx, dt = wbmm_backward(x, dy, table, ctx.w)
+            dt = dt.to(table.dtype)
+        elif need_x:
+            dx = wbmm_backward_input(dy, table, ctx.w)
+        elif need_t:
             dt = wbmm_backward_table(x, dy, ctx.w).to(table.dtype)
         return dx, dt, None
 

@@ -124,6 +124,41 @@ wbmm_status wbmm_backward_table(const void *x, const void *dy, float *dtable, vo
   return from_hip(wbmm::launch_dtable((Dt)dtype, x, dy, dtable, workspace, g, (hipStream_t)stream));
 }
 
+size_t wbmm_backward_workspace_bytes(int64_t B, int64_t C, int64_t H, int64_t W, int w,
+                                     wbmm_dtype dtype) {
+  return wbmm_backward_table_workspace_bytes(B, C, H, W, w, dtype);
+}
+
+wbmm_status wbmm_backward(const void *x, const void *dy, const void *table, void *dx, float *dtable,
+                          void *workspace, size_t workspace_bytes, int64_t B, int64_t C, int64_t H,
+                          int64_t W, int w, wbmm_dtype dtype, void *stream) {
+  Geom g;
+  int64_t bytes = 0;
+  wbmm_status s = check_shape(B, C, H, W, w, dtype, &g, &bytes);
+  if (s != WBMM_OK) return s;
+  if (!x || !dy || !table || !dx || !dtable) return WBMM_ERR_INVALID_ARG;
+  const size_t es = elem_size(dtype);
+  if (!aligned(x, es) || !aligned(dy, es) || !aligned(table, es) || !aligned(dx, es) || !aligned(dtable, 4))
+    return WBMM_ERR_INVALID_ARG;
+  const int64_t k2 = (int64_t)(2 * w - 1) * (2 * w - 1);
+  const int64_t tbytes = C * k2 * (int64_t)es;  // table
+  const int64_t gbytes = C * k2 * 4;            // dtable
+  // outputs overlap neither inputs nor each other
+  if (overlap(dx, bytes, x, bytes) || overlap(dx, bytes, dy, bytes) || overlap(dx, bytes, table, tbytes) ||
+      overlap(dx, bytes, dtable, gbytes) || overlap(dtable, gbytes, x, bytes) ||
+      overlap(dtable, gbytes, dy, bytes) || overlap(dtable, gbytes, table, tbytes))
+    return WBMM_ERR_INVALID_ARG;
+  const size_t need = wbmm::dtable_workspace_bytes((Dt)dtype, g);
+  if (need > 0) {
+    if (!workspace || workspace_bytes < need || !aligned(workspace, 4)) return WBMM_ERR_INVALID_ARG;
+    if (overlap(workspace, (int64_t)need, dtable, gbytes) || overlap(workspace, (int64_t)need, dx, bytes) ||
+        overlap(workspace, (int64_t)need, x, bytes) || overlap(workspace, (int64_t)need, dy, bytes) ||
+        overlap(workspace, (int64_t)need, table, tbytes))
+      return WBMM_ERR_INVALID_ARG;
+  }
+  return from_hip(wbmm::launch_backward((Dt)dtype, x, dy, table, dx, dtable, workspace, g, (hipStream_t)stream));
+}
+
 const char *wbmm_status_string(wbmm_status s) {
   switch (s) {
     case WBMM_OK: return "WBMM_OK";

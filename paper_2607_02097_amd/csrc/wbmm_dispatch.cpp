@@ -40,6 +40,13 @@ hipError_t launch_dtable(Dt dt, const void *x, const void *dy, float *dtable, vo
   return e->dtable(x, dy, dtable, workspace, g, stream);
 }
 
+hipError_t launch_backward(Dt dt, const void *x, const void *dy, const void *table, void *dx, float *dtable,
+                           void *workspace, const Geom &g, hipStream_t stream) {
+  const Entry *e = find(dt, g.w);
+  if (!e) return hipErrorInvalidValue;
+  return e->bwd(x, dy, table, dx, dtable, workspace, g, stream);
+}
+
 DtPlan plan_dtable(Dt dt, const Geom &g) {
   const Entry *e = find(dt, g.w);
   if (!e) return DtPlan{0, 0};

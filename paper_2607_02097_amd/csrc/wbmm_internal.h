@@ -1,5 +1,5 @@
 // Internal interface between the C-ABI front end (wbmm_api.cpp) and the HIP
-// kernels (wbmm_kernels.hip).  Not installed, not part of the ABI.
+// kernels (wbmm_kernels.h, instantiated by wbmm_inst.hip).  Not installed, not part of the ABI.
 #pragma once
 
 #include <stddef.h>
@@ -39,16 +39,22 @@ hipError_t launch_forward(Dt dt, const void *x, const void *table, void *y,
                           hipStream_t stream);
 hipError_t launch_dtable(Dt dt, const void *x, const void *dy, float *dtable,
                          void *workspace, const Geom &g, hipStream_t stream);
+hipError_t launch_backward(Dt dt, const void *x, const void *dy, const void *table,
+                           void *dx, float *dtable, void *workspace, const Geom &g,
+                           hipStream_t stream);
 
 // Per-(dtype, window) entry points, defined by the wbmm_inst.hip
 // translation units and collected into tables by wbmm_dispatch.cpp.
 typedef hipError_t (*FwdFn)(const void *, const void *, void *, const Geom &, bool, hipStream_t);
 typedef hipError_t (*DtFn)(const void *, const void *, float *, void *, const Geom &, hipStream_t);
 typedef DtPlan (*PlanFn)(const Geom &);
+typedef hipError_t (*BwdFn)(const void *, const void *, const void *, void *, float *, void *, const Geom &,
+                            hipStream_t);
 struct Entry {
   FwdFn fwd;
   DtFn dtable;
   PlanFn plan;
+  BwdFn bwd;
 };
 
 }  // namespace wbmm

@@ -574,7 +574,7 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
   }
 }
 
-// ===================================================== dtable kernel
+// ===================================================== table gradient
 
 template <class Tag, int WIN>
 struct DtCfg {
@@ -595,6 +595,30 @@ struct DtCfg {
   static constexpr int NBT = (2 * R - 1) * K1;    // bins per accumulator tile
   static constexpr int ROWS = 2 * CW * KR;        // row copies per stage (x and dy)
   static constexpr int RPT = cdiv(ROWS, kThreads);  // row copies per thread
+};
+
+// Staging of the fused backward: the table gradient's stages, with enough
+// padded rows (zero beyond the window) for both readers of the tile: the
+// input-gradient products (K over KP positions) and the table-gradient tiles
+// (NPT * 16 positions); the forward's row pitch when it holds them.
+// LDS: [x stage][dy stage][table row][Toeplitz blocks (16-bit)].
+template <class Tag, int WIN>
+struct BwdCfg {
+  typedef DtCfg<Tag, WIN> T;
+  typedef FwdCfg<Tag, WIN> F;
+  static constexpr int RP = T::RP, NPT = T::NPT, R = T::R, CW = T::CW;
+  static constexpr int NACC = T::NACC, K1 = T::K1, K2 = T::K2, NBT = T::NBT;
+  static constexpr int KR = F::KR > T::KR ? F::KR : T::KR;
+  static constexpr int LDSW = F::LDSW >= KR * RP ? F::LDSW : T::LDSW;
+  static constexpr int BUF = CW * LDSW * Tag::ES;
+  static constexpr int ROWS = 2 * CW * KR;
+  static constexpr int RPT = cdiv(ROWS, kThreads);
+  static constexpr int SUBS = CW / 16;            // input-gradient sub-tiles per stage
+  static constexpr int WPS = kWaves / SUBS;       // waves per sub-tile
+  static constexpr int TS_OFF = 2 * BUF;
+  static constexpr int TB_OFF = TS_OFF + rup(F::TS_LEN * Tag::ES, 16);
+  static constexpr int TAB_END = TB_OFF + F::TB_LEN * Tag::ES;
+  static_assert(KR * RP <= LDSW && NPT * 16 <= LDSW, "staged rows must fit the pitch");
 };
 
 // Accumulator tiles are split among the waves in contiguous ranges of
@@ -646,26 +670,48 @@ __host__ __device__ constexpr int max_tiles_per_wave() {
   return m;
 }
 
+// The accumulator tiles of one wave: P = lo .. lo + np - 1.
+template <int NPT, int WAVE>
+struct PSpan {
+  static constexpr PRange PR = make_prange<NPT>();
+  static constexpr int lo = PR.lo[WAVE];
+  static constexpr int np = PR.hi[WAVE] - PR.lo[WAVE] + 1;  // may be 0
+  static constexpr int hi = lo + np - 1;
+  static constexpr int na = np > 0 ? np : 1;                // array length
+};
+
+template <class G>
+__host__ __device__ constexpr size_t bins_lds_bytes() {
+  return (size_t)(kWaves * max_tiles_per_wave<G::NPT>() * 16 * 17 + G::NACC * G::NBT) * 4;
+}
+
 template <class Tag, int WIN>
 __host__ __device__ constexpr size_t dt_lds_bytes() {
   typedef DtCfg<Tag, WIN> G;
   const size_t ops = 2 * (size_t)G::BUF;
-  const size_t bins = (size_t)(kWaves * max_tiles_per_wave<G::NPT>() * 16 * 17 + G::NACC * G::NBT) * 4;
+  const size_t bins = bins_lds_bytes<G>();
+  return ops > bins ? ops : bins;
+}
+
+template <class Tag, int WIN>
+__host__ __device__ constexpr size_t bwd_lds_bytes() {
+  typedef BwdCfg<Tag, WIN> G;
+  const size_t ops = (size_t)G::TAB_END;
+  const size_t bins = bins_lds_bytes<G>();
   return ops > bins ? ops : bins;
 }
 
 // Row copies of one stage: task q covers tensor (q / (CW * KR)), window
 // (q / KR) % CW of the stage and padded row q % KR (rows >= w are zero).
-template <class Tag, int WIN>
-struct DtStage {
-  typedef DtCfg<Tag, WIN> G;
+template <class Tag, int WIN, class G>
+struct Stage {
   RowData<WIN, Tag::ES> rd[G::RPT];
 };
 
-template <class Tag, int WIN>
-__device__ __attribute__((always_inline)) inline void dt_load_stage(const KArgs &a, const void *x, const void *dy, int64_t c, int64_t m0,
-                                     int64_t m1, int tid, DtStage<Tag, WIN> &st) {
-  typedef DtCfg<Tag, WIN> G;
+template <class Tag, int WIN, class G>
+__device__ __attribute__((always_inline)) inline void stage_load(const KArgs &a, const void *x, const void *dy,
+                                                                  int64_t c, int64_t m0, int64_t m1, int tid,
+                                                                  Stage<Tag, WIN, G> &st) {
 #pragma unroll
   for (int k = 0; k < G::RPT; ++k) {
     const int q = tid + k * kThreads;
@@ -682,9 +728,9 @@ __device__ __attribute__((always_inline)) inline void dt_load_stage(const KArgs 
 }
 
 // Write a loaded stage window-major (padded rows, as in the forward tile).
-template <class Tag, int WIN>
-__device__ __attribute__((always_inline)) inline void dt_write_stage(unsigned char *smem, int tid, const DtStage<Tag, WIN> &st) {
-  typedef DtCfg<Tag, WIN> G;
+template <class Tag, int WIN, class G>
+__device__ __attribute__((always_inline)) inline void stage_write(unsigned char *smem, int tid,
+                                                                   const Stage<Tag, WIN, G> &st) {
   typedef RowData<WIN, Tag::ES> RD;
 #pragma unroll
   for (int k = 0; k < G::RPT; ++k) {
@@ -710,100 +756,88 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 // the transposing read hands lane i the i-th column of the 4 x 16 block whose
 // row r is the 4-element chunks of lanes 4r .. 4r + 3; lane 4r + q points at
 // window 8g + r (+4), positions 16 * pt + 4q .. + 3.
-template <class Tag, int WIN>
+template <int LDSW>
 __device__ __attribute__((always_inline)) inline u16x8 dt_frag16(const unsigned char *buf, int pt, int lane) {
-  typedef DtCfg<Tag, WIN> G;
   const int g = lane >> 4;
   const int i = lane & 15;
   const int r = i >> 2, q = i & 3;
-  const int e0 = (8 * g + r) * G::LDSW + 16 * pt + 4 * q;
+  const int e0 = (8 * g + r) * LDSW + 16 * pt + 4 * q;
   lds_i16x4 *p0 = (lds_i16x4 *)(buf + 2 * e0);
-  lds_i16x4 *p1 = (lds_i16x4 *)(buf + 2 * (e0 + 4 * G::LDSW));
+  lds_i16x4 *p1 = (lds_i16x4 *)(buf + 2 * (e0 + 4 * LDSW));
   const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(p0);
   const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(p1);
   return __builtin_bit_cast(u16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
-template <class Tag, int WIN, int WAVE>
-__device__ __attribute__((always_inline)) void dt_wave(const typename Tag::S *__restrict__ x, const typename Tag::S *__restrict__ dy,
-                        float *__restrict__ dt, float *__restrict__ part, unsigned *__restrict__ cnt,
-                        const KArgs &a, unsigned char *smem) {
+// This wave's share of X^T dY for one stage (K = the stage's windows).
+template <class Tag, class G, int WAVE>
+__device__ __attribute__((always_inline)) inline void dt_products(const unsigned char *Xt, const unsigned char *Dt,
+                                                                   f32x4 (&acc)[PSpan<G::NPT, WAVE>::na], int lane) {
   typedef typename Tag::Frag Frag;
-  typedef DtCfg<Tag, WIN> G;
-  constexpr int NPT = G::NPT, CW = G::CW, RP = G::RP, R = G::R;
-  constexpr int K1 = G::K1, K2 = G::K2, NBT = G::NBT;
-  constexpr PRange PR = make_prange<NPT>();
-  constexpr int PLO = PR.lo[WAVE];
-  constexpr int NP = PR.hi[WAVE] - PR.lo[WAVE] + 1;  // may be 0
-  constexpr int PHI = PLO + NP - 1;
-
-  const unsigned char *Xt = smem;
-  const unsigned char *Dt = smem + G::BUF;
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
+  typedef PSpan<G::NPT, WAVE> SP;
+  constexpr int NPT = G::NPT, CW = G::CW;
+  constexpr int PLO = SP::lo, NP = SP::np, PHI = SP::hi;
   const int g = lane >> 4;
   const int ln = lane & 15;
-  const int64_t c = blockIdx.x / a.tiles_per_ch;
-  const int64_t slab = blockIdx.x - c * a.tiles_per_ch;
-  const int64_t s0 = slab * a.tile;
-  const int64_t s1 = (s0 + a.tile < a.N) ? s0 + a.tile : a.N;
-
-  f32x4 acc[NP > 0 ? NP : 1];
+  if constexpr (NP > 0) {
+    if constexpr (Tag::W16) {
+      Frag bf[NPT];
 #pragma unroll
-  for (int j = 0; j < NP; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  DtStage<Tag, WIN> st;
-  dt_load_stage<Tag, WIN>(a, x, dy, c, s0, s1, tid, st);
-
-  for (int64_t m0 = s0; m0 < s1; m0 += CW) {
-    if (m0 != s0) __syncthreads();  // previous stage consumed
-    dt_write_stage<Tag, WIN>(smem, tid, st);
-    __syncthreads();
-    if (m0 + CW < s1) dt_load_stage<Tag, WIN>(a, x, dy, c, m0 + CW, s1, tid, st);
-
-    if constexpr (NP > 0) {
-      if constexpr (Tag::W16) {
-        Frag bf[NPT];
+      for (int pi = 0; pi < NPT; ++pi) {
+        // B fragments first needed at this pi: po with max(0, po + PLO) == pi
+#pragma unroll
+        for (int po = 0; po < NPT; ++po) {
+          const bool used = po + PHI >= 0 && po + PLO <= NPT - 1;
+          if (used && (po + PLO > 0 ? po + PLO : 0) == pi) bf[po] = dt_frag16<G::LDSW>(Dt, po, lane);
+        }
+        const Frag af = dt_frag16<G::LDSW>(Xt, pi, lane);
+#pragma unroll
+        for (int j = 0; j < NP; ++j) {
+          const int po = pi - (PLO + j);
+          if (po >= 0 && po < NPT) acc[j] = mma<Tag>(af, bf[po], acc[j]);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < CW / 4; ++ks) {
+        float bf[NPT];
 #pragma unroll
         for (int pi = 0; pi < NPT; ++pi) {
-          // B fragments first needed at this pi: po with max(0, po + PLO) == pi
 #pragma unroll
           for (int po = 0; po < NPT; ++po) {
             const bool used = po + PHI >= 0 && po + PLO <= NPT - 1;
             if (used && (po + PLO > 0 ? po + PLO : 0) == pi)
-              bf[po] = dt_frag16<Tag, WIN>(Dt, po, lane);
+              bf[po] = reinterpret_cast<const float *>(Dt)[(4 * ks + g) * G::LDSW + 16 * po + ln];
           }
-          const Frag af = dt_frag16<Tag, WIN>(Xt, pi, lane);
+          const float af = reinterpret_cast<const float *>(Xt)[(4 * ks + g) * G::LDSW + 16 * pi + ln];
 #pragma unroll
           for (int j = 0; j < NP; ++j) {
             const int po = pi - (PLO + j);
             if (po >= 0 && po < NPT) acc[j] = mma<Tag>(af, bf[po], acc[j]);
           }
         }
-      } else {
-#pragma unroll
-        for (int ks = 0; ks < CW / 4; ++ks) {
-          float bf[NPT];
-#pragma unroll
-          for (int pi = 0; pi < NPT; ++pi) {
-#pragma unroll
-            for (int po = 0; po < NPT; ++po) {
-              const bool used = po + PHI >= 0 && po + PLO <= NPT - 1;
-              if (used && (po + PLO > 0 ? po + PLO : 0) == pi)
-                bf[po] = reinterpret_cast<const float *>(Dt)[(4 * ks + g) * G::LDSW + 16 * po + ln];
-            }
-            const float af = reinterpret_cast<const float *>(Xt)[(4 * ks + g) * G::LDSW + 16 * pi + ln];
-#pragma unroll
-            for (int j = 0; j < NP; ++j) {
-              const int po = pi - (PLO + j);
-              if (po >= 0 && po < NPT) acc[j] = mma<Tag>(af, bf[po], acc[j]);
-            }
-          }
-        }
       }
     }
   }
+}
+
+// Table gradient of the workgroup's slab from the accumulators: diagonal
+// bins, then the slab's dT; with several slabs per channel the channel's
+// last workgroup sums the partials.  Starts with a workgroup barrier (the
+// bins reuse the LDS of the stages).
+template <class Tag, int WIN, class G, int WAVE>
+__device__ __attribute__((always_inline)) inline void dt_finish(const f32x4 (&acc)[PSpan<G::NPT, WAVE>::na],
+                                                                 unsigned char *smem, float *__restrict__ dt,
+                                                                 float *__restrict__ part, unsigned *__restrict__ cnt,
+                                                                 const KArgs &a, int64_t c, int64_t slab) {
+  typedef PSpan<G::NPT, WAVE> SP;
+  constexpr int NPT = G::NPT, RP = G::RP, R = G::R;
+  constexpr int K1 = G::K1, K2 = G::K2, NBT = G::NBT;
+  constexpr int PLO = SP::lo, NP = SP::np;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int g = lane >> 4;
+  const int ln = lane & 15;
   __syncthreads();
 
   // ---- diagonal binning, fixed order.  Every tile of the wave goes to LDS
@@ -915,6 +949,35 @@ __device__ __attribute__((always_inline)) void dt_wave(const typename Tag::S *__
   if (tid == 0) __hip_atomic_store(&cnt[c], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+template <class Tag, int WIN, int WAVE>
+__device__ __attribute__((always_inline)) void dt_wave(const typename Tag::S *__restrict__ x, const typename Tag::S *__restrict__ dy,
+                        float *__restrict__ dt, float *__restrict__ part, unsigned *__restrict__ cnt,
+                        const KArgs &a, unsigned char *smem) {
+  typedef DtCfg<Tag, WIN> G;
+  typedef PSpan<G::NPT, WAVE> SP;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int64_t c = blockIdx.x / a.tiles_per_ch;
+  const int64_t slab = blockIdx.x - c * a.tiles_per_ch;
+  const int64_t s0 = slab * a.tile;
+  const int64_t s1 = (s0 + a.tile < a.N) ? s0 + a.tile : a.N;
+
+  f32x4 acc[SP::na];
+#pragma unroll
+  for (int j = 0; j < SP::na; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  Stage<Tag, WIN, G> st;
+  stage_load<Tag, WIN, G>(a, x, dy, c, s0, s1, tid, st);
+  for (int64_t m0 = s0; m0 < s1; m0 += G::CW) {
+    if (m0 != s0) __syncthreads();  // previous stage consumed
+    stage_write<Tag, WIN, G>(smem, tid, st);
+    __syncthreads();
+    if (m0 + G::CW < s1) stage_load<Tag, WIN, G>(a, x, dy, c, m0 + G::CW, s1, tid, st);
+    dt_products<Tag, G, WAVE>(smem, smem + G::BUF, acc, lane);
+  }
+  dt_finish<Tag, WIN, G, WAVE>(acc, smem, dt, part, cnt, a, c, slab);
+}
+
 template <class Tag, int WIN>
 __global__ __launch_bounds__(kThreads, 3) void wbmm_dt_kernel(const typename Tag::S *__restrict__ x,
                                                               const typename Tag::S *__restrict__ dy,
@@ -926,6 +989,211 @@ __global__ __launch_bounds__(kThreads, 3) void wbmm_dt_kernel(const typename Tag
     case 1: dt_wave<Tag, WIN, 1>(x, dy, dt, part, cnt, a, smem); break;
     case 2: dt_wave<Tag, WIN, 2>(x, dy, dt, part, cnt, a, smem); break;
     default: dt_wave<Tag, WIN, 3>(x, dy, dt, part, cnt, a, smem); break;
+  }
+}
+
+// ===================================================== fused backward
+
+// Input-gradient products of one stage: dX = dY M^T per window, i.e. the
+// forward products with the reversed table.  The wave takes sub-tile
+// WAVE % SUBS of the stage and the output tiles [T0, T1) of its part; K runs
+// outermost (all its output tiles accumulate at once), each tile's sum over
+// K in the forward's order.  The rounded results go to Obuf (window-major,
+// the x stage, no longer read).
+template <class Tag, int WIN, int WAVE>
+__device__ __attribute__((always_inline)) inline void dx_products(const unsigned char *Dbuf, unsigned char *Obuf,
+                                                                   const unsigned char *smem, int lane) {
+  typedef typename Tag::S S;
+  typedef typename Tag::Frag Frag;
+  typedef BwdCfg<Tag, WIN> G;
+  typedef FwdCfg<Tag, WIN> F;
+  constexpr int RP = G::RP, LDSW = G::LDSW, NT = F::NT, S_ = F::S, K1 = G::K1;
+  constexpr int SUB = WAVE % G::SUBS, PART = WAVE / G::SUBS;
+  constexpr int T0 = PART * NT / G::WPS, T1 = (PART + 1) * NT / G::WPS, NTW = T1 - T0;
+  const int g = lane >> 4;
+  const int ln = lane & 15;
+  const S *rowp = reinterpret_cast<const S *>(Dbuf) + SUB * 16 * LDSW;
+  S *outp = reinterpret_cast<S *>(Obuf) + (SUB * 16 + 4 * g) * LDSW + ln;
+  if constexpr (NTW > 0) {
+    f32x4 acc[NTW];
+#pragma unroll
+    for (int j = 0; j < NTW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if constexpr (Tag::W16) {
+      constexpr int NB = F::NB;
+      const S *TB = reinterpret_cast<const S *>(smem + G::TB_OFF);
+      auto load_bf = [&](int q) -> Frag {
+        const int d0 = q - (NT - 1);
+        int dh, xi0;
+        if (RP == 16) { dh = d0 + (g >> 1); xi0 = 8 * (g & 1); }
+        else { dh = 2 * d0 + g - (ln >> 3); xi0 = 0; }
+        const int xo = ln & (RP - 1);
+        if (dh >= -(WIN - 1) && dh <= WIN - 1)
+          return *reinterpret_cast<const Frag *>(&TB[((dh + WIN - 1) * RP + xo) * RP + xi0]);
+        return Frag{0, 0, 0, 0, 0, 0, 0, 0};
+      };
+      // fragment q = 2s - t + NT - 1 serves steps s with T0 <= t < T1; it is
+      // read from LDS at the first of them
+      Frag bf[NB];
+#pragma unroll
+      for (int s = 0; s < S_; ++s) {
+#pragma unroll
+        for (int q = 0; q < NB; ++q) {
+          const int lo = 2 * s + NT - T1, hi = 2 * s + NT - 1 - T0;  // fragments of step s
+          const bool first = s == 0 ? true : !(q >= lo - 2 && q <= hi - 2);
+          if (q >= lo && q <= hi && first) bf[q] = load_bf(q);
+        }
+        const Frag af = *reinterpret_cast<const Frag *>(&rowp[ln * LDSW + s * 32 + 8 * g]);
+#pragma unroll
+        for (int j = 0; j < NTW; ++j) acc[j] = mma<Tag>(af, bf[2 * s - (T0 + j) + NT - 1], acc[j]);
+      }
+#pragma unroll
+      for (int j = 0; j < NTW; ++j) {
+        const int t = T0 + j;
+        const uint32_t lo = pack2<Tag>(acc[j][0], acc[j][1]);
+        const uint32_t hi = pack2<Tag>(acc[j][2], acc[j][3]);
+        outp[0 * LDSW + 16 * t] = (u16)(lo & 0xffffu);
+        outp[1 * LDSW + 16 * t] = (u16)(lo >> 16);
+        outp[2 * LDSW + 16 * t] = (u16)(hi & 0xffffu);
+        outp[3 * LDSW + 16 * t] = (u16)(hi >> 16);
+      }
+    } else {
+      const S *Ts = reinterpret_cast<const S *>(smem + G::TS_OFF);
+#pragma unroll
+      for (int s = 0; s < S_; ++s) {
+        const float af = rowp[ln * LDSW + 4 * s + g];
+        const int k = 4 * s + g;
+        const int hi = k / RP, xi = k % RP;
+#pragma unroll
+        for (int j = 0; j < NTW; ++j) {
+          const int pn = 16 * (T0 + j) + ln;
+          const int ho = pn / RP, xo = pn % RP;
+          const int dh = hi - ho;
+          float bv = 0.f;
+          if (xo < WIN && xi < WIN && dh >= -(WIN - 1) && dh <= WIN - 1)
+            bv = Ts[(dh + WIN - 1) * K1 + xi - xo + WIN - 1];
+          acc[j] = mma<Tag>(af, bv, acc[j]);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < NTW; ++j)
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) outp[rr * LDSW + 16 * (T0 + j)] = acc[j][rr];
+    }
+  }
+}
+
+// Store the stage's input-gradient rows (window-major in Obuf).
+template <class Tag, int WIN>
+__device__ __attribute__((always_inline)) inline void dx_store(const KArgs &a, void *dx, int64_t c, int64_t m0,
+                                                                int64_t m1, int tid, const unsigned char *Obuf) {
+  typedef BwdCfg<Tag, WIN> G;
+  typedef RowData<WIN, Tag::ES> RD;
+  for (int q = tid; q < G::CW * WIN; q += kThreads) {
+    const int v = q / WIN;
+    const int hi = q - v * WIN;
+    if (m0 + v >= m1) break;
+    const Row<WIN, Tag::ES> r = row_of<WIN, Tag::ES>(a, dx, c, m0 + v, hi);
+    if (r.mode == kNone) continue;
+    const uint32_t *l4 = reinterpret_cast<const uint32_t *>(Obuf + (v * G::LDSW + hi * G::RP) * Tag::ES);
+    uint32_t d[RD::ND];
+#pragma unroll
+    for (int i = 0; i < RD::ND; i += 4) {
+      const uint4 u = *reinterpret_cast<const uint4 *>(l4 + i);
+      d[i] = u.x; d[i + 1] = u.y; d[i + 2] = u.z; d[i + 3] = u.w;
+    }
+    store_row<WIN, Tag::ES>(dx, r, d);
+  }
+}
+
+// One workgroup = (channel, slab of windows), as the table gradient.  Per
+// stage: the x and dy rows land window-major; the waves accumulate their
+// share of X^T dY; after a barrier the x tile is free and receives the
+// input-gradient results computed from the dy tile, which are then stored
+// as rows.  dY is read once for both gradients.
+template <class Tag, int WIN, int WAVE>
+__device__ __attribute__((always_inline)) void bwd_wave(const typename Tag::S *__restrict__ x,
+                                                        const typename Tag::S *__restrict__ dy,
+                                                        const typename Tag::S *__restrict__ tab,
+                                                        typename Tag::S *__restrict__ dx, float *__restrict__ dt,
+                                                        float *__restrict__ part, unsigned *__restrict__ cnt,
+                                                        const KArgs &a, unsigned char *smem) {
+  typedef typename Tag::S S;
+  typedef BwdCfg<Tag, WIN> G;
+  typedef PSpan<G::NPT, WAVE> SP;
+  constexpr int RP = G::RP, K1 = G::K1, K2 = G::K2;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int64_t c = blockIdx.x / a.tiles_per_ch;
+  const int64_t slab = blockIdx.x - c * a.tiles_per_ch;
+  const int64_t s0 = slab * a.tile;
+  const int64_t s1 = (s0 + a.tile < a.N) ? s0 + a.tile : a.N;
+  unsigned char *Xt = smem;
+  unsigned char *Dt = smem + G::BUF;
+
+  f32x4 acc[SP::na];
+#pragma unroll
+  for (int j = 0; j < SP::na; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // first stage in flight; the reversed table row and (16-bit) its Toeplitz
+  // blocks -> LDS
+  Stage<Tag, WIN, G> st;
+  stage_load<Tag, WIN, G>(a, x, dy, c, s0, s1, tid, st);
+  {
+    S *Ts = reinterpret_cast<S *>(smem + G::TS_OFF);
+    const S *tc = tab + c * K2;
+    for (int k = tid; k < K2; k += kThreads) Ts[k] = tc[K2 - 1 - k];
+    if constexpr (Tag::W16) {
+      __syncthreads();
+      S *TB = reinterpret_cast<S *>(smem + G::TB_OFF);
+      constexpr int CPR = RP / 8;
+      constexpr int NCH = K1 * RP * CPR;
+      for (int ch = tid; ch < NCH; ch += kThreads) {
+        const int row = ch / CPR;               // = dhi * RP + x_out
+        const int xi0 = (ch - row * CPR) * 8;
+        const int dhi = row / RP;
+        const int xo = row - dhi * RP;
+        u16x8 v = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+        if (xo < WIN) {
+          const int k0 = dhi * K1 - xo + WIN - 1;  // table index of x_in = 0
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int xi = xi0 + e < WIN ? xi0 + e : WIN - 1;
+            const u16 t = Ts[k0 + xi];
+            v[e] = xi0 + e < WIN ? t : (u16)0;
+          }
+        }
+        *reinterpret_cast<u16x8 *>(&TB[row * RP + xi0]) = v;
+      }
+    }
+  }
+
+  for (int64_t m0 = s0; m0 < s1; m0 += G::CW) {
+    if (m0 != s0) __syncthreads();  // previous stage's rows stored
+    stage_write<Tag, WIN, G>(smem, tid, st);
+    __syncthreads();
+    if (m0 + G::CW < s1) stage_load<Tag, WIN, G>(a, x, dy, c, m0 + G::CW, s1, tid, st);
+    dt_products<Tag, G, WAVE>(Xt, Dt, acc, lane);
+    __syncthreads();  // the x tile is no longer read
+    dx_products<Tag, WIN, WAVE>(Dt, Xt, smem, lane);
+    __syncthreads();
+    dx_store<Tag, WIN>(a, dx, c, m0, s1, tid, Xt);
+  }
+  dt_finish<Tag, WIN, G, WAVE>(acc, smem, dt, part, cnt, a, c, slab);
+}
+
+template <class Tag, int WIN>
+__global__ __launch_bounds__(kThreads, 2) void wbmm_bwd_kernel(const typename Tag::S *__restrict__ x,
+                                                               const typename Tag::S *__restrict__ dy,
+                                                               const typename Tag::S *__restrict__ tab,
+                                                               typename Tag::S *__restrict__ dx,
+                                                               float *__restrict__ dt, float *__restrict__ part,
+                                                               unsigned *__restrict__ cnt, KArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  switch (threadIdx.x >> 6) {
+    case 0: bwd_wave<Tag, WIN, 0>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
+    case 1: bwd_wave<Tag, WIN, 1>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
+    case 2: bwd_wave<Tag, WIN, 2>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
+    default: bwd_wave<Tag, WIN, 3>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
   }
 }
 
@@ -962,7 +1230,10 @@ static hipError_t run_forward(const void *x, const void *t, void *y, const Geom 
   a.tile = pick_fwd_tile<Tag, WIN>(g);
   a.tiles_per_ch = (int)cdiv64(g.N, a.tile);
   const dim3 grid((unsigned)(g.C * a.tiles_per_ch));
-  const size_t lds = fwd_lds_bytes<Tag, WIN>();
+  constexpr size_t lds = fwd_lds_bytes<Tag, WIN>();
+  // float32 windows of 13 and more take up to 70 KB (LDS is reached with ds
+  // instructions only)
+  static_assert(lds <= 160 * 1024, "workgroup LDS above the 160 KB of a compute unit");
   if (rev)
     wbmm_fwd_kernel<Tag, WIN, true><<<grid, dim3(kFwdThreads), lds, st>>>((const S *)x, (const S *)t, (S *)y, a);
   else
@@ -997,9 +1268,27 @@ static hipError_t run_dtable(const void *x, const void *dy, float *dt, void *ws,
   a.tiles_per_ch = (int)p.slabs;
   unsigned *cnt = p.slabs > 1 ? (unsigned *)ws : nullptr;
   float *part = p.slabs > 1 ? (float *)((char *)ws + counter_bytes(g.C)) : nullptr;
-  const size_t lds = dt_lds_bytes<Tag, WIN>();
+  constexpr size_t lds = dt_lds_bytes<Tag, WIN>();
+  static_assert(lds <= 65536, "workgroup LDS above 64 KB");
   wbmm_dt_kernel<Tag, WIN><<<dim3((unsigned)(g.C * p.slabs)), dim3(kThreads), lds, st>>>(
       (const S *)x, (const S *)dy, dt, part, cnt, a);
+  return hipGetLastError();
+}
+
+template <class Tag, int WIN>
+static hipError_t run_backward(const void *x, const void *dy, const void *t, void *dx, float *dt, void *ws,
+                               const Geom &g, hipStream_t st) {
+  typedef typename Tag::S S;
+  KArgs a = make_args(g);
+  const DtPlan p = plan_dt<Tag, WIN>(g);
+  a.tile = (int)p.slab_windows;
+  a.tiles_per_ch = (int)p.slabs;
+  unsigned *cnt = p.slabs > 1 ? (unsigned *)ws : nullptr;
+  float *part = p.slabs > 1 ? (float *)((char *)ws + counter_bytes(g.C)) : nullptr;
+  constexpr size_t lds = bwd_lds_bytes<Tag, WIN>();
+  static_assert(lds <= 65536, "workgroup LDS above 64 KB");
+  wbmm_bwd_kernel<Tag, WIN><<<dim3((unsigned)(g.C * p.slabs)), dim3(kThreads), lds, st>>>(
+      (const S *)x, (const S *)dy, (const S *)t, (S *)dx, dt, part, cnt, a);
   return hipGetLastError();
 }
 

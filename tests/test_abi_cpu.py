@@ -105,3 +105,32 @@ def test_workspace_query(lib):
     n = lib.wbmm_backward_table_workspace_bytes(64, 192, 28, 28, 14, 1)
     counters = (192 * 4 + 255) // 256 * 256  # one 32-bit counter per channel
     assert n > counters and (n - counters) % (192 * 729 * 4) == 0
+
+
+def test_backward_rejects_bad_arguments(lib):
+    E = W.WBMM_ERR_INVALID_ARG
+    vp = ctypes.c_void_p
+
+    def call(x=FAKE, dy=FAKE * 8, t=FAKE * 12, dx=FAKE * 16, dt=FAKE * 24, ws=0, wsb=0,
+             B=1, C=2, H=7, Wd=7, w=7, d=1):
+        return lib.wbmm_backward(vp(x), vp(dy), vp(t), vp(dx), vp(dt), vp(ws), wsb,
+                                 B, C, H, Wd, w, d, None)
+
+    for k in ("x", "dy", "t", "dx", "dt"):
+        assert call(**{k: 0}) == E, k
+    assert call(dx=FAKE * 16 + 1) == E             # misaligned bf16 output
+    assert call(dt=FAKE * 24 + 2) == E             # dtable must be 4-byte aligned
+    assert call(dx=FAKE) == E                      # dx aliases x
+    assert call(dx=FAKE * 8 + 64) == E             # dx overlaps dy
+    assert call(dx=FAKE * 12 - 64) == E            # dx overlaps the table
+    assert call(dt=FAKE * 12) == E                 # dtable overlaps the table
+    assert call(dt=FAKE * 16 + 128) == E           # dtable overlaps dx
+    assert call(w=18) == W.WBMM_ERR_UNSUPPORTED
+    assert call(d=5) == W.WBMM_ERR_UNSUPPORTED
+    need = lib.wbmm_backward_workspace_bytes(64, 192, 28, 28, 14, 1)
+    assert need == lib.wbmm_backward_table_workspace_bytes(64, 192, 28, 28, 14, 1) > 0
+    big = dict(B=64, C=192, H=28, Wd=28, w=14, x=FAKE, dy=FAKE * 64, t=FAKE * 128,
+               dx=FAKE * 192, dt=FAKE * 256)
+    assert call(**big) == E                                         # no workspace
+    assert call(ws=FAKE * 320, wsb=need - 4, **big) == E            # too small
+    assert call(ws=FAKE * 192 + 64, wsb=need, **big) == E           # overlaps dx

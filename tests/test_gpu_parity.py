@@ -74,7 +74,7 @@ SMALL = [
     (2, 3, 30, 17, 14),
     (1, 2, 14, 14, 14),
     (9, 2, 14, 14, 14),
-    # bands wider than the LDS staging limit take the generic kernels
+    # wide images: many windows per band, ragged bottom windows
     (1, 2, 20, 600, 14),
     (2, 1, 9, 1200, 7),
 ]
@@ -86,6 +86,35 @@ def test_small_parity(shape, dtype):
     B, C, H, Wd, w = shape
     d = draw(B, C, H, Wd, w, dtype, seed=11)
     check(run_gpu(d, w, dtype), run_oracle(d, w), dtype, "%s %s" % (dtype, shape))
+
+
+def check_fused(d, w, dtype, label):
+    """The fused backward equals the two separate entry points bit for bit
+    (same products, same summation orders) and the oracle within tolerance."""
+    x, t, dy = (to_device(d[k], dtype) for k in ("x", "t", "dy"))
+    dx, dt = W.wbmm_backward(x, dy, t, w)
+    dx_s = W.wbmm_backward_input(dy, t, w)
+    dt_s = W.wbmm_backward_table(x, dy, w)
+    torch.cuda.synchronize()
+    assert torch.equal(dx, dx_s), "%s: fused dx differs from wbmm_backward_input" % label
+    assert torch.equal(dt, dt_s), "%s: fused dt differs from wbmm_backward_table" % label
+    check({"dx": to_f64(dx), "dt": to_f64(dt)}, run_oracle(d, w, ("dx", "dt")), dtype, label + " fused")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("shape", SMALL, ids=lambda s: "B%dC%dH%dW%dw%d" % s)
+def test_fused_backward_small(shape, dtype):
+    B, C, H, Wd, w = shape
+    d = draw(B, C, H, Wd, w, dtype, seed=12)
+    check_fused(d, w, dtype, "%s %s" % (dtype, shape))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("w", list(range(1, 17)))
+def test_fused_backward_every_window_size(w, dtype):
+    B, C, H, Wd = 3, 2, 2 * w + 3, w + 5
+    d = draw(B, C, H, Wd, w, dtype, seed=100 + w)
+    check_fused(d, w, dtype, "%s w=%d" % (dtype, w))
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -157,6 +186,13 @@ def test_workload_full_size(name):
         assert np.isfinite(v).all(), "%s %s: non-finite output" % (name, k)
         sub[k] = v[ch] if k == "dt" else v[:, ch]
     check(sub, want, wl.dtype, name)
+    if "dt" in wl.passes:
+        # the fused backward at full size: equal to the separate passes
+        x, t, dy = (to_device(d[k], wl.dtype) for k in ("x", "t", "dy"))
+        dx, dt = W.wbmm_backward(x, dy, t, wl.w)
+        torch.cuda.synchronize()
+        assert np.array_equal(to_f64(dx), got["dx"]), "%s: fused dx" % name
+        assert np.array_equal(to_f64(dt), got["dt"]), "%s: fused dt" % name
 
 
 def test_determinism_and_reversed_table():
@@ -210,6 +246,11 @@ def test_gpu_error_paths():
     ws = W.new_workspace(need - 4)
     with pytest.raises(W.WbmmError):
         W.wbmm_backward_table(big, big.clone(), 14, workspace=ws)
+    tb = torch.zeros((192, 729), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(W.WbmmError):
+        W.wbmm_backward(big, big.clone(), tb, 14, workspace=ws)  # workspace too small
+    with pytest.raises(W.WbmmError):
+        W.wbmm_backward(x, x.clone(), t, 7, dx=x)  # dx aliases x
 
 
 def test_hip_graph_replay_matches_eager():
@@ -221,8 +262,9 @@ def test_hip_graph_replay_matches_eager():
     x, t, dy = (to_device(d[k], "bf16") for k in ("x", "t", "dy"))
     need = W.wbmm_backward_table_workspace_bytes(x.shape, 14, x.dtype)
     ws = W.new_workspace(need)
-    y, dx = torch.empty_like(x), torch.empty_like(dy)
+    y, dx, dx2 = torch.empty_like(x), torch.empty_like(dy), torch.empty_like(dy)
     dt = torch.empty((wl.C, wl.table_len), dtype=torch.float32, device="cuda")
+    dt2 = torch.empty_like(dt)
     ref = (W.wbmm_forward(x, t, 14), W.wbmm_backward_input(dy, t, 14),
            W.wbmm_backward_table(x, dy, 14, workspace=ws))
     torch.cuda.synchronize()
@@ -233,14 +275,16 @@ def test_hip_graph_replay_matches_eager():
         W.wbmm_forward(x, t, 14, out=y)
         W.wbmm_backward_input(dy, t, 14, out=dx)
         W.wbmm_backward_table(x, dy, 14, out=dt, workspace=ws)
+        W.wbmm_backward(x, dy, t, 14, dx=dx2, dtable=dt2, workspace=ws)
     torch.cuda.current_stream().wait_stream(s)
     for rep in range(3):
-        y.zero_(); dx.zero_(); dt.zero_()
+        y.zero_(); dx.zero_(); dt.zero_(); dx2.zero_(); dt2.zero_()
         W.wbmm_forward(dy, t, 14)  # unrelated eager work between replays
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(y, ref[0]) and torch.equal(dx, ref[1]) and torch.equal(dt, ref[2]), rep
+        assert torch.equal(dx2, ref[1]) and torch.equal(dt2, ref[2]), rep
 
 
 def test_workspace_counters_reset_between_calls():
@@ -254,8 +298,9 @@ def test_workspace_counters_reset_between_calls():
     ref = W.wbmm_backward_table(x, dy, 14, workspace=W.new_workspace(need))
     for _ in range(3):
         got = W.wbmm_backward_table(x, dy, 14, workspace=ws)
+        _, got2 = W.wbmm_backward(x, dy, to_device(d["t"], "bf16"), 14, workspace=ws)
         torch.cuda.synchronize()
-        assert torch.equal(got, ref)
+        assert torch.equal(got, ref) and torch.equal(got2, ref)
     counters = ws[: 4 * big.C].view(torch.int32)
     assert int(counters.abs().sum()) == 0
     xs, dys = x[:, :48].contiguous(), dy[:, :48].contiguous()
