@@ -395,6 +395,59 @@ __device__ __attribute__((always_inline)) inline void store_sub(const KArgs &a, 
   }
 }
 
+// The table row of channel c (read back to front for the input gradient)
+// -> Ts with coalesced loads; for 16-bit, the Toeplitz blocks
+// TB[dh][x_out][x_in] of M_c gathered from it.  Ends with a workgroup barrier.
+template <class Tag, int WIN, bool REV>
+__device__ __attribute__((always_inline)) inline void fwd_tables(const typename Tag::S *__restrict__ tab, int64_t c,
+                                                                  typename Tag::S *Ts, typename Tag::S *TB, int tid) {
+  typedef typename Tag::S S;
+  typedef FwdCfg<Tag, WIN> G;
+  constexpr int RP = G::RP, K1 = G::K1, K2 = G::K2;
+  const S *tc = tab + c * K2;
+  for (int k = tid; k < K2; k += kFwdThreads) Ts[k] = tc[REV ? K2 - 1 - k : k];
+  if constexpr (Tag::W16) {
+    __syncthreads();
+    constexpr int CPR = RP / 8;               // 8-element chunks per TB row
+    constexpr int NCH = K1 * RP * CPR;
+    for (int ch = tid; ch < NCH; ch += kFwdThreads) {
+      const int row = ch / CPR;               // = dhi * RP + x_out
+      const int xi0 = (ch - row * CPR) * 8;
+      const int dhi = row / RP;
+      const int xo = row - dhi * RP;
+      u16x8 v = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+      if (xo < WIN) {
+        const int k0 = dhi * K1 - xo + WIN - 1;  // table index of x_in = 0
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int xi = xi0 + e < WIN ? xi0 + e : WIN - 1;
+          const u16 t = Ts[k0 + xi];
+          v[e] = xi0 + e < WIN ? t : (u16)0;
+        }
+      }
+      *reinterpret_cast<u16x8 *>(&TB[row * RP + xi0]) = v;
+    }
+  }
+  __syncthreads();
+}
+
+// B fragment q (= 2 * kstep - ntile + NT - 1) of M_c for lane (g, ln), from
+// the Toeplitz blocks.
+template <class Tag, int WIN>
+__device__ __attribute__((always_inline)) inline typename Tag::Frag fwd_bfrag(const typename Tag::S *TB, int q,
+                                                                               int g, int ln) {
+  typedef FwdCfg<Tag, WIN> G;
+  constexpr int RP = G::RP, NT = G::NT;
+  const int d0 = q - (NT - 1);
+  int dh, xi0;
+  if (RP == 16) { dh = d0 + (g >> 1); xi0 = 8 * (g & 1); }
+  else { dh = 2 * d0 + g - (ln >> 3); xi0 = 0; }
+  const int xo = ln & (RP - 1);
+  if (dh >= -(WIN - 1) && dh <= WIN - 1)
+    return *reinterpret_cast<const typename Tag::Frag *>(&TB[((dh + WIN - 1) * RP + xo) * RP + xi0]);
+  return typename Tag::Frag{0, 0, 0, 0, 0, 0, 0, 0};
+}
+
 template <class Tag, int WIN, bool REV>
 __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename Tag::S *__restrict__ x,
                                                                   const typename Tag::S *__restrict__ tab,
@@ -426,51 +479,13 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
   //         M_c for 16-bit, the table itself for float32) -> LDS
   SubRows<Tag, WIN> nxt;
   if (nsub > 0) load_sub<Tag, WIN>(a, x, c, n0 + first * 16, nwin - first * 16, lane, nxt);
-  {
-    // the table row moves with coalesced loads; the Toeplitz blocks are then
-    // gathered from its LDS copy
-    const S *tc = tab + c * K2;
-    for (int k = tid; k < K2; k += kFwdThreads) Ts[k] = tc[REV ? K2 - 1 - k : k];
-    if constexpr (Tag::W16) {
-      __syncthreads();
-      constexpr int CPR = RP / 8;               // 8-element chunks per TB row
-      constexpr int NCH = K1 * RP * CPR;
-      for (int ch = tid; ch < NCH; ch += kFwdThreads) {
-        const int row = ch / CPR;               // = dhi * RP + x_out
-        const int xi0 = (ch - row * CPR) * 8;
-        const int dhi = row / RP;
-        const int xo = row - dhi * RP;
-        u16x8 v = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
-        if (xo < WIN) {
-          const int k0 = dhi * K1 - xo + WIN - 1;  // table index of x_in = 0
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const int xi = xi0 + e < WIN ? xi0 + e : WIN - 1;
-            const u16 t = Ts[k0 + xi];
-            v[e] = xi0 + e < WIN ? t : (u16)0;
-          }
-        }
-        *reinterpret_cast<u16x8 *>(&TB[row * RP + xi0]) = v;
-      }
-    }
-  }
-  __syncthreads();
+  fwd_tables<Tag, WIN, REV>(tab, c, Ts, TB, tid);
 
   const int g = lane >> 4;   // lane group
   const int ln = lane & 15;  // row (A) / column (B, C) inside a 16x16 tile
   if constexpr (Tag::W16) {
     constexpr int S_ = G::S, NT = G::NT, NB = G::NB;
-    // ---- 2. B fragment q (= 2*kstep - ntile + NT - 1) for this lane
-    auto load_bf = [&](int q) -> Frag {
-      const int d0 = q - (NT - 1);
-      int dh, xi0;
-      if (RP == 16) { dh = d0 + (g >> 1); xi0 = 8 * (g & 1); }
-      else { dh = 2 * d0 + g - (ln >> 3); xi0 = 0; }
-      const int xo = ln & (RP - 1);
-      if (dh >= -(WIN - 1) && dh <= WIN - 1)
-        return *reinterpret_cast<const Frag *>(&TB[((dh + WIN - 1) * RP + xo) * RP + xi0]);
-      return Frag{0, 0, 0, 0, 0, 0, 0, 0};
-    };
+    auto load_bf = [&](int q) -> Frag { return fwd_bfrag<Tag, WIN>(TB, q, g, ln); };
     // ---- 3. pipeline over this wave's sub-tiles
     for (int j = 0; j < nsub; ++j) {
       const int64_t m0 = n0 + (first + j) * 16;
@@ -570,6 +585,181 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
         for (int rr = 0; rr < 4; ++rr) outp[rr * LDSW + 16 * t] = acc[rr];
       }
       store_sub<Tag, WIN>(a, y, c, m0, mw, lane, buf);
+    }
+  }
+}
+
+// ------------------------------------------------ forward, band layout
+// Small 16-bit windows (w <= 8) on maps whose windows tile the image, whose
+// windows per band (NW) divide 16 and whose image rows start 16-byte
+// aligned: a sub-tile of 16 consecutive windows is then 16 / NW whole bands,
+// each band w image rows that are contiguous in memory.  The band moves with
+// 16-byte loads and stores at consecutive addresses (a window row of w < 8
+// elements would otherwise take several narrow accesses) and keeps its image
+// layout in LDS; the matrix-core A operands are gathered from it element by
+// element, and the rounded results are written back into it.  The rows of
+// each finished output-tile pair are stored while the next pair is
+// multiplied.
+template <int WIN>
+struct BandCfg {
+  static constexpr int ELEMS = 16 * WIN * WIN;  // elements of one sub-tile
+  static constexpr int CH = ELEMS / 8;          // its 16-byte chunks
+  static constexpr int KC = cdiv(CH, 64);       // chunks per lane
+  static constexpr int BUF_BYTES = rup(ELEMS * 2, 16);
+};
+
+template <class Tag, int WIN>
+__host__ __device__ constexpr size_t fwd_band_lds_bytes() {
+  typedef FwdCfg<Tag, WIN> G;
+  return (size_t)kFwdWaves * BandCfg<WIN>::BUF_BYTES + (size_t)(G::TS_LEN + G::TB_LEN) * Tag::ES;
+}
+
+// Element offset of the first element of the band holding window n.
+__device__ __attribute__((always_inline)) inline int64_t band_offset(const KArgs &a, int64_t c, int64_t n, int win) {
+  const int nhw = a.NH * a.NW;
+  const int b = fdiv((int)n, nhw, a.inv_nhw);
+  const int wy = fdiv((int)n - b * nhw, a.NW, a.inv_nw);
+  return (((int64_t)b * a.C + c) * a.H + (int64_t)wy * win) * a.W;
+}
+
+// The 16-byte chunks of the bands of one sub-tile (window m0 and on, nb
+// bands), lane + 64 k; chunk q of the sub-tile is element 8 q of its LDS copy.
+template <int WIN>
+__device__ __attribute__((always_inline)) inline void band_load(const KArgs &a, const void *x, int64_t c, int64_t m0,
+                                                                 int nb, int lane, uint4 (&v)[BandCfg<WIN>::KC]) {
+  const int cpb = WIN * (int)a.W / 8;  // chunks per band
+#pragma unroll
+  for (int k = 0; k < BandCfg<WIN>::KC; ++k) {
+    const int q = lane + 64 * k;
+    v[k] = make_uint4(0, 0, 0, 0);
+    if (q < nb * cpb) {
+      const int j = q / cpb;
+      const int64_t e = band_offset(a, c, m0 + (int64_t)j * a.NW, WIN) + 8 * (int64_t)(q - j * cpb);
+      v[k] = *reinterpret_cast<const uint4 *>(reinterpret_cast<const char *>(x) + 2 * e);
+    }
+  }
+}
+
+template <class Tag, int WIN, bool REV>
+__global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_band_kernel(const typename Tag::S *__restrict__ x,
+                                                                       const typename Tag::S *__restrict__ tab,
+                                                                       typename Tag::S *__restrict__ y, KArgs a) {
+  typedef typename Tag::S S;
+  typedef typename Tag::Frag Frag;
+  typedef FwdCfg<Tag, WIN> G;
+  typedef BandCfg<WIN> BC;
+  static_assert(Tag::W16 && G::RP == 8, "band layout: 16-bit windows up to 8");
+  constexpr int S_ = G::S, NT = G::NT, NB = G::NB, KC = BC::KC;
+
+  extern __shared__ __align__(16) unsigned char smem[];
+  S *Ts = reinterpret_cast<S *>(smem + kFwdWaves * BC::BUF_BYTES);
+  S *TB = Ts + G::TS_LEN;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  u16 *raw = reinterpret_cast<u16 *>(smem + wave * BC::BUF_BYTES);  // this wave's bands
+
+  const int64_t c = blockIdx.x / a.tiles_per_ch;
+  const int64_t n0 = (int64_t)(blockIdx.x - c * a.tiles_per_ch) * a.tile;
+  const int nwin = (int)((n0 + a.tile <= a.N) ? a.tile : a.N - n0);
+  const int spw = a.tile / (16 * kFwdWaves);  // sub-tiles per wave
+  const int first = wave * spw;
+  int nsub = (nwin - first * 16 + 15) / 16;
+  nsub = nsub < 0 ? 0 : (nsub > spw ? spw : nsub);
+  const int W = (int)a.W;
+  const int NWb = a.NW;            // windows per band
+  const int BE = WIN * W;          // elements per band
+  auto bands_of = [&](int j) -> int {  // bands of sub-tile j
+    const int mw = nwin - (first + j) * 16;
+    return (mw < 16 ? mw : 16) / NWb;
+  };
+
+  uint4 nxt[KC];
+  if (nsub > 0) band_load<WIN>(a, x, c, n0 + first * 16, bands_of(0), lane, nxt);
+  fwd_tables<Tag, WIN, REV>(tab, c, Ts, TB, tid);
+
+  const int g = lane >> 4;
+  const int ln = lane & 15;
+  for (int j = 0; j < nsub; ++j) {
+    const int64_t m0 = n0 + (first + j) * 16;
+    const int nb = bands_of(j);
+    const int nw16 = nb * NWb;  // windows of this sub-tile
+    wave_lds_sync();
+#pragma unroll
+    for (int k = 0; k < KC; ++k) {
+      const int q = lane + 64 * k;
+      if (q < BC::CH) *reinterpret_cast<uint4 *>(raw + 8 * q) = nxt[k];
+    }
+    if (j + 1 < nsub) band_load<WIN>(a, x, c, m0 + 16, bands_of(j + 1), lane, nxt);
+    wave_lds_sync();
+    // A fragment of K step s: window ln, its row 4s + g, columns 0..7
+    const int jb = ln / NWb, wx = ln - jb * NWb;
+    const int abase = jb * BE + wx * WIN;
+    Frag af[S_];
+#pragma unroll
+    for (int s = 0; s < S_; ++s) {
+      const int r = 4 * s + g;
+      Frag f = Frag{0, 0, 0, 0, 0, 0, 0, 0};
+      if (r < WIN && ln < nw16) {
+#pragma unroll
+        for (int e = 0; e < WIN; ++e) f[e] = raw[abase + r * W + e];
+      }
+      af[s] = f;
+    }
+    // the four windows 4g .. 4g+3 this lane's results belong to
+    int obase[4];
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      const int m = 4 * g + rr;
+      const int jo = m / NWb;
+      obase[rr] = m < nw16 ? jo * BE + (m - jo * NWb) * WIN : -1;
+    }
+    Frag bf[NB];
+#pragma unroll
+    for (int t0 = 0; t0 < NT; t0 += 2) {
+#pragma unroll
+      for (int q = 0; q < NB; ++q) {
+        const int tf = NT - 1 - q;  // smallest t with this parity using q
+        const int first_t = tf >= 0 ? tf : (((-tf) & 1) ? 1 : 0);
+        if (first_t == t0 || first_t == t0 + 1) bf[q] = fwd_bfrag<Tag, WIN>(TB, q, g, ln);
+      }
+      f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < S_; ++s) {
+        acc0 = mma<Tag>(af[s], bf[2 * s - t0 + NT - 1], acc0);
+        if (t0 + 1 < NT) acc1 = mma<Tag>(af[s], bf[2 * s - t0 - 1 + NT - 1], acc1);
+      }
+      // results: output position ln of tile t = row 2t + ln / 8, column ln % 8
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int t = t0 + h;
+        if (t >= NT) continue;
+        const f32x4 acc = h ? acc1 : acc0;
+        const int ho = 2 * t + (ln >> 3), xo = ln & 7;
+        if (ho < WIN && xo < WIN) {
+          const uint32_t lo = pack2<Tag>(acc[0], acc[1]);
+          const uint32_t hi = pack2<Tag>(acc[2], acc[3]);
+          const u16 vals[4] = {(u16)(lo & 0xffffu), (u16)(lo >> 16), (u16)(hi & 0xffffu), (u16)(hi >> 16)};
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr)
+            if (obase[rr] >= 0) raw[obase[rr] + ho * W + xo] = vals[rr];
+        }
+      }
+      // image rows [2 t0, 2 t0 + 4) of every band are final: store them
+      wave_lds_sync();
+      {
+        const int r0 = 2 * t0;
+        const int r1 = r0 + 4 < WIN ? r0 + 4 : WIN;
+        const int cpr = (r1 - r0) * W / 8;  // chunks per band in these rows
+        if (lane < nb * cpr) {
+          const int jj = lane / cpr;
+          const int i = r0 * W / 8 + (lane - jj * cpr);
+          const uint4 val = *reinterpret_cast<const uint4 *>(raw + jj * BE + 8 * i);
+          const int64_t e = band_offset(a, c, m0 + (int64_t)jj * NWb, WIN) + 8 * (int64_t)i;
+          *reinterpret_cast<uint4 *>(reinterpret_cast<char *>(y) + 2 * e) = val;
+        }
+      }
     }
   }
 }
@@ -1230,6 +1420,21 @@ static hipError_t run_forward(const void *x, const void *t, void *y, const Geom 
   a.tile = pick_fwd_tile<Tag, WIN>(g);
   a.tiles_per_ch = (int)cdiv64(g.N, a.tile);
   const dim3 grid((unsigned)(g.C * a.tiles_per_ch));
+  if constexpr (Tag::W16 && rp_of(WIN) == 8) {
+    // band layout: windows tile the map, NW divides 16, image rows and both
+    // tensors 16-byte aligned
+    const bool band = g.H % WIN == 0 && g.W % WIN == 0 && 16 % g.NW == 0 && g.W % 8 == 0 &&
+                      (reinterpret_cast<uintptr_t>(x) & 15) == 0 && (reinterpret_cast<uintptr_t>(y) & 15) == 0;
+    if (band) {
+      constexpr size_t blds = fwd_band_lds_bytes<Tag, WIN>();
+      static_assert(blds <= 65536, "workgroup LDS above 64 KB");
+      if (rev)
+        wbmm_fwd_band_kernel<Tag, WIN, true><<<grid, dim3(kFwdThreads), blds, st>>>((const S *)x, (const S *)t, (S *)y, a);
+      else
+        wbmm_fwd_band_kernel<Tag, WIN, false><<<grid, dim3(kFwdThreads), blds, st>>>((const S *)x, (const S *)t, (S *)y, a);
+      return hipGetLastError();
+    }
+  }
   constexpr size_t lds = fwd_lds_bytes<Tag, WIN>();
   // float32 windows of 13 and more take up to 70 KB (LDS is reached with ds
   // instructions only)

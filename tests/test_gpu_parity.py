@@ -166,6 +166,64 @@ def test_integer_data_bit_exact(w, dtype):
         assert np.array_equal(got[k], want[k]), k
 
 
+# shapes for the band-layout forward (16-bit, w <= 8, windows tile the map,
+# windows per band divide 16, rows 16-byte aligned)
+BAND = [
+    (5, 3, 56, 56, 7),
+    (3, 2, 14, 56, 7),     # 48 windows per channel: a ragged last tile
+    (2, 3, 16, 16, 4),     # 4 windows per band
+    (1, 2, 24, 64, 8),     # 8 windows per band
+    (2, 2, 8, 32, 2),      # 16 windows per band
+    (3, 2, 5, 40, 5),      # one band per image
+    (1, 4, 16, 16, 1),
+]
+
+
+def misaligned_like(t):
+    """A contiguous copy of t whose data starts 2 bytes past a 16-byte boundary
+    (the forward then takes the row path)."""
+    buf = torch.empty(t.numel() + 8, dtype=t.dtype, device=t.device)
+    v = buf[1:1 + t.numel()].view(t.shape)
+    v.copy_(t)
+    return v
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("shape", BAND, ids=lambda s: "B%dC%dH%dW%dw%d" % s)
+def test_band_layout_forward(shape, dtype):
+    """The band-layout forward and input gradient match the oracle and equal
+    the row-path results bit for bit (same products, same order)."""
+    B, C, H, Wd, w = shape
+    d = draw(B, C, H, Wd, w, dtype, seed=21)
+    x, t, dy = (to_device(d[k], dtype) for k in ("x", "t", "dy"))
+    y, dx = W.wbmm_forward(x, t, w), W.wbmm_backward_input(dy, t, w)
+    xm, dym = misaligned_like(x), misaligned_like(dy)
+    ym, dxm = misaligned_like(torch.zeros_like(x)), misaligned_like(torch.zeros_like(dy))
+    W.wbmm_forward(xm, t, w, out=ym)
+    W.wbmm_backward_input(dym, t, w, out=dxm)
+    torch.cuda.synchronize()
+    assert torch.equal(y, ym) and torch.equal(dx, dxm)
+    check({"fwd": to_f64(y), "dx": to_f64(dx)}, run_oracle(d, w, ("fwd", "dx")), dtype, "band %s" % (shape,))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+def test_band_layout_one_hot_bit_exact(dtype):
+    w = 7
+    B, C, H, Wd = 2, 6, 14, 56
+    d = draw(B, C, H, Wd, w, dtype, seed=6)
+    K = 2 * w - 1
+    t64 = np.zeros((C, K * K))
+    offs = [(0, 0), (1, -2), (-(w - 1), w - 1), (w - 1, -(w - 1)), (-3, 0), (2, 5)]
+    for c in range(C):
+        dh, dw = offs[c]
+        t64[c, (dh + w - 1) * K + (dw + w - 1)] = 1.0
+    d["t"], d["t64"] = synth.round_to(t64, dtype)
+    got = run_gpu(d, w, dtype, ("fwd", "dx"))
+    want = run_oracle(d, w, ("fwd", "dx"))
+    for k in want:
+        assert np.array_equal(got[k], want[k]), k
+
+
 def sampled_channels(C):
     return sorted({0, 1, C // 3, C // 2, C - 1})
 
