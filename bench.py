@@ -55,7 +55,12 @@ def parse():
 # plain copy of known size.  Valid only for the kernel source it was measured
 # on (sha256 of the kernel header); otherwise reported as null.
 TRAFFIC = {
-    # (workload, pass): measured bytes per dispatch (profiles/wbmm_traffic_*.txt)
+    # (workload, kernel): measured bytes per dispatch (profiles/wbmm_traffic_*.txt)
+    ("bf16_b64_c192_28_w14", "bwd"): {"source": "049fd9639fe78f01", "bytes": 68180689},
+    ("bf16_b64_c192_28_w14", "fwd"): {"source": "049fd9639fe78f01", "bytes": 41098384},
+    ("bf16_b64_c192_28_w14", "dx"): {"source": "049fd9639fe78f01", "bytes": 41108509},
+    ("bf16_b64_c192_28_w14", "dt"): {"source": "049fd9639fe78f01", "bytes": 47624850},
+    ("bf16_b64_c96_56_w7", "fwd"): {"source": "049fd9639fe78f01", "bytes": 77438873},
 }
 
 
