@@ -170,5 +170,23 @@ def hier_forward(x, tg, tl, wl, lib=None) -> np.ndarray:
     return dense_forward(x, hier_fused_matrix(tg, tl, wl, lib=lib), 2 * wl, lib=lib)
 
 
+def dense_backward_input(dy, m, wg, lib=None) -> np.ndarray:
+    """dX = dY_w M^T per window for an explicit per-channel matrix M."""
+    return dense_forward(dy, np.ascontiguousarray(np.transpose(_f64(m), (0, 2, 1))), wg, lib=lib)
+
+
+def hier_backward_input(dy, tg, tl, wl, lib=None) -> np.ndarray:
+    """dX of the hierarchical form: dY_w M_fused^T per global window."""
+    return dense_backward_input(dy, hier_fused_matrix(tg, tl, wl, lib=lib), 2 * wl, lib=lib)
+
+
+def hier_backward_tables(x, dy, wl, lib=None):
+    """(dT_g, dT_l) of the hierarchical form.  By the training form
+    Y = WBMM(X; T_g, 2 wl) + WBMM(X; T_l, wl) + 2 X (the local sub-windows of
+    the zero-padded global windows are the wl windows of the map), each table
+    gradient is that of its own scale."""
+    return backward_table(x, dy, 2 * wl, lib=lib), backward_table(x, dy, wl, lib=lib)
+
+
 if __name__ == "__main__":  # pragma: no cover - manual build hook
     print(build(int(sys.argv[1]) if len(sys.argv) > 1 else 0))

@@ -321,6 +321,35 @@ def test_hierarchical_fused_equals_training_form(olib, shape, wl):
     assert np.array_equal(z, 2 * x)
 
 
+@pytest.mark.parametrize("shape,wl", [((2, 2, 12, 12), 3), ((1, 3, 10, 7), 2)])
+def test_hierarchical_gradients(olib, shape, wl):
+    """Gradients of the hierarchical form, pinned to its dense inference form
+    (explicit M_fused, a separate code path): exact finite differences in
+    both tables on integer data (the loss is bilinear), the adjoint identity
+    for dX, and dX as the forward with both tables reversed."""
+    r = rng(14)
+    C = shape[1]
+    x = r.integers(-3, 4, size=shape).astype(np.float64)
+    dy = r.integers(-3, 4, size=shape).astype(np.float64)
+    tg = r.integers(-3, 4, size=(C, (4 * wl - 1) ** 2)).astype(np.float64)
+    tl = r.integers(-3, 4, size=(C, (2 * wl - 1) ** 2)).astype(np.float64)
+    loss = lambda g, l: float(np.sum(dy * oracle.hier_forward(x, g, l, wl, lib=olib)))
+    dtg, dtl = oracle.hier_backward_tables(x, dy, wl, lib=olib)
+    base = loss(tg, tl)
+    for c, k in [(0, 0), (C - 1, (4 * wl - 1) ** 2 // 2), (C // 2, 5)]:
+        e = np.zeros_like(tg)
+        e[c, k] = 1.0
+        assert loss(tg + e, tl) - base == dtg[c, k]
+    for c, k in [(0, 0), (C - 1, (2 * wl - 1) ** 2 // 2), (C // 2, 2)]:
+        e = np.zeros_like(tl)
+        e[c, k] = 1.0
+        assert loss(tg, tl + e) - base == dtl[c, k]
+    dx = oracle.hier_backward_input(dy, tg, tl, wl, lib=olib)
+    assert float(np.sum(x * dx)) == base
+    rev = oracle.hier_forward(dy, tg[:, ::-1].copy(), tl[:, ::-1].copy(), wl, lib=olib)
+    assert np.array_equal(dx, rev)
+
+
 # ------------------------------------------------ pins reject planted mistakes
 
 def _pin_battery(lib):
