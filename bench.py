@@ -86,6 +86,11 @@ def pass_bytes(wl, p, es):
     """Algorithmic bytes of one kernel (each tensor touched once)."""
     act = wl.B * wl.C * wl.H * wl.W * es
     tab = wl.C * wl.table_len
+    if wl.hier:
+        tabs = tab + wl.C * (wl.w - 1) ** 2  # global and local tables
+        if p == "hfwd":
+            return 2 * act + tabs * es
+        return 3 * act + tabs * es + tabs * 4  # read x, dy, tables; write dx, float32 gradients
     if p in ("fwd", "dx"):
         return 2 * act + tab * es          # read input, write output, read table
     if p == "dt":
@@ -116,7 +121,7 @@ def main():
     from paper_2607_02097_amd import binding as W
     from paper_2607_02097_amd import synth
 
-    wl = synth.WORKLOADS[args.workload]
+    wl = synth.WORKLOADS.get(args.workload) or synth.HIER_WORKLOADS[args.workload]
     es = 4 if wl.dtype == "f32" else 2
     tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[wl.dtype]
     dev = torch.device("cuda:0")
@@ -134,18 +139,29 @@ def main():
     if args.cold:
         per = 4 * wl.B * wl.C * wl.H * wl.W * es  # x, dy, y, dx
         nsets = max(2, int(np.ceil(2 * 256e6 / per)) + 1)
+    wloc = wl.w // 2  # local window of the hierarchical form
+    if wl.hier:
+        d["tl"], d["tl64"] = synth.draw_local_table(wl.C, wloc, wl.dtype, seed=0)
     sets = []
     for i in range(nsets):
         x, t, dy = put(d["x"]), put(d["t"]), put(d["dy"])
         y, dx = torch.empty_like(x), torch.empty_like(dy)
         dtab = torch.empty((wl.C, wl.table_len), dtype=torch.float32, device=dev)
-        need = W.wbmm_backward_table_workspace_bytes(x.shape, wl.w, tdt)
+        if wl.hier:
+            tl = put(d["tl"])
+            dtl = torch.empty((wl.C, (2 * wloc - 1) ** 2), dtype=torch.float32, device=dev)
+            need = W.wbmm_hier_backward_workspace_bytes(x.shape, wloc, tdt)
+        else:
+            tl = dtl = None
+            need = W.wbmm_backward_table_workspace_bytes(x.shape, wl.w, tdt)
         ws = W.new_workspace(need, dev)  # counters start at zero, stay zero
-        sets.append((x, t, dy, y, dx, dtab, ws))
+        sets.append((x, t, dy, y, dx, dtab, ws, tl, dtl))
 
     passes = wl.passes
     # kernels of one step: the fused backward covers the two gradients
     step_kernels = ["fwd", "bwd"] if "dt" in passes else list(passes)
+    if wl.hier:
+        step_kernels = list(passes)
     timed = step_kernels + [p for p in passes if p not in step_kernels and p != "fwd"]
     lib = W.load_library()
     code = W.DTYPE_CODES[tdt]
@@ -155,10 +171,18 @@ def main():
     def launch(p, i):
         """One pass through the C ABI on torch's current stream (raw pointers,
         no per-call Python checks: the shapes were validated above)."""
-        x, t, dy, y, dx, dtab, ws = sets[i % nsets]
+        x, t, dy, y, dx, dtab, ws, tl, dtl = sets[i % nsets]
         st = vp(torch.cuda.current_stream(dev).cuda_stream)
         dims = (wl.B, wl.C, wl.H, wl.W, wl.w, code, st)
-        if p == "fwd":
+        hdims = (wl.B, wl.C, wl.H, wl.W, wloc, code, st)
+        if p == "hfwd":
+            r = lib.wbmm_hier_forward(vp(x.data_ptr()), vp(t.data_ptr()), vp(tl.data_ptr()), vp(y.data_ptr()),
+                                      *hdims)
+        elif p == "hbwd":
+            r = lib.wbmm_hier_backward(vp(x.data_ptr()), vp(dy.data_ptr()), vp(t.data_ptr()), vp(tl.data_ptr()),
+                                       vp(dx.data_ptr()), vp(dtab.data_ptr()), vp(dtl.data_ptr()),
+                                       vp(ws.data_ptr()), ws.numel(), *hdims)
+        elif p == "fwd":
             r = lib.wbmm_forward(vp(x.data_ptr()), vp(t.data_ptr()), vp(y.data_ptr()), *dims)
         elif p == "dx":
             r = lib.wbmm_backward_input(vp(dy.data_ptr()), vp(t.data_ptr()), vp(dx.data_ptr()), *dims)
@@ -271,7 +295,9 @@ def main():
     ai = dom_flops / dom_bytes
     ridge = peak * 1e12 / (HBM_PEAK_GBS * 1e9)
     kernel_name = {"fwd": "wbmm_fwd_kernel<%s,%d,false>", "dx": "wbmm_fwd_kernel<%s,%d,true>",
-                   "dt": "wbmm_dt_kernel<%s,%d>", "bwd": "wbmm_bwd_kernel<%s,%d>"}[dom] % ({"bf16": "TagBF16", "f16": "TagF16",
+                   "dt": "wbmm_dt_kernel<%s,%d>", "bwd": "wbmm_bwd_kernel<%s,%d>",
+                   "hfwd": "wbmm_fwd_kernel<%s,%d,false,true>",
+                   "hbwd": "wbmm_hier_backward (3 launches) <%s,%d>"}[dom] % ({"bf16": "TagBF16", "f16": "TagF16",
                                                           "f32": "TagF32"}[wl.dtype], wl.w)
     if ai < ridge:
         achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
@@ -296,6 +322,10 @@ def main():
         reps_cpu, cpu_s = 0, 0.0
         while cpu_s < 10.0 and reps_cpu < 200:
             t0 = time.perf_counter()
+            if wl.hier:
+                oracle.hier_forward(d["x64"], d["t64"], d["tl64"], wloc)
+                oracle.hier_backward_input(d["dy64"], d["t64"], d["tl64"], wloc)
+                oracle.hier_backward_tables(d["x64"], d["dy64"], wloc)
             if "fwd" in passes:
                 oracle.forward(d["x64"], d["t64"], wl.w)
             if "dx" in passes:

@@ -131,6 +131,46 @@ wbmm_status wbmm_backward(const void *x, const void *dy, const void *table,
                           int64_t H, int64_t W, int w, wbmm_dtype dtype,
                           void *stream);
 
+/* ---- Hierarchical (global + local) form (Sec. "Hierarchical Window
+ * Reparameterization" and the appendix algorithms of its training and
+ * inference modes).  Global windows of w_g = 2 wl, each split into 2 x 2
+ * local sub-windows of wl x wl; two tables: table_g [C,(2 w_g - 1)^2] and
+ * table_l [C,(2 wl - 1)^2], in dtype.  Per global window
+ *   y = x M_fused,  M_fused = M_g + diag_blocks(M_l, M_l, M_l, M_l) + 2 I,
+ * which equals the training form x M_g + x + x_sub M_l + x_sub.  The fused
+ * matrix is never built: the kernel adds the local blocks and the identity
+ * as extra matrix-core products of the w_g kernel.  1 <= wl <= 8.
+ * Same conventions as above (device pointers, NCHW, zero padding at the
+ * bottom/right to multiples of w_g, outputs cropped). */
+wbmm_status wbmm_hier_forward(const void *x, const void *table_g,
+                              const void *table_l, void *y, int64_t B,
+                              int64_t C, int64_t H, int64_t W, int wl,
+                              wbmm_dtype dtype, void *stream);
+
+/* dx = dy M_fused^T (both tables read back to front). */
+wbmm_status wbmm_hier_backward_input(const void *dy, const void *table_g,
+                                     const void *table_l, void *dx, int64_t B,
+                                     int64_t C, int64_t H, int64_t W, int wl,
+                                     wbmm_dtype dtype, void *stream);
+
+/* Workspace for wbmm_hier_backward (the larger of the two table gradients'
+ * needs; same rules as for wbmm_backward_table). */
+size_t wbmm_hier_backward_workspace_bytes(int64_t B, int64_t C, int64_t H,
+                                          int64_t W, int wl, wbmm_dtype dtype);
+
+/* All gradients of the hierarchical form: dx as wbmm_hier_backward_input;
+ * dtable_g = the table gradient with windows 2 wl, dtable_l = the table
+ * gradient with windows wl (the local sub-windows of the padded global
+ * windows are the wl windows of the map); both float32, overwritten.  Three
+ * launches on `stream`, sharing the workspace one after the other.  Outputs
+ * must not overlap inputs, each other or the workspace. */
+wbmm_status wbmm_hier_backward(const void *x, const void *dy,
+                               const void *table_g, const void *table_l,
+                               void *dx, float *dtable_g, float *dtable_l,
+                               void *workspace, size_t workspace_bytes,
+                               int64_t B, int64_t C, int64_t H, int64_t W,
+                               int wl, wbmm_dtype dtype, void *stream);
+
 /* Static description of a status code (never NULL). */
 const char *wbmm_status_string(wbmm_status s);
 

@@ -5,12 +5,16 @@ include/wbmm.h (libwbmm.so, built in-tree by ``python -m
 paper_2607_02097_amd.build``).  This package only marshals torch tensors to
 that library.
 """
-from .binding import (WBMMFunction, WbmmError, load_library, wbmm, wbmm_backward,
-                      wbmm_backward_input, wbmm_backward_table,
+from .binding import (WBMMFunction, WBMMHierFunction, WbmmError, load_library, wbmm,
+                      wbmm_backward, wbmm_backward_input, wbmm_backward_table,
                       wbmm_backward_table_workspace_bytes, wbmm_backward_workspace_bytes,
-                      wbmm_forward, wbmm_relative_index, wbmm_status_string, wbmm_version)
+                      wbmm_forward, wbmm_hier, wbmm_hier_backward, wbmm_hier_backward_input,
+                      wbmm_hier_backward_workspace_bytes, wbmm_hier_forward,
+                      wbmm_relative_index, wbmm_status_string, wbmm_version)
 
-__all__ = ["WBMMFunction", "WbmmError", "load_library", "wbmm", "wbmm_backward",
+__all__ = ["WBMMFunction", "WBMMHierFunction", "WbmmError", "load_library", "wbmm",
+           "wbmm_hier", "wbmm_hier_forward", "wbmm_hier_backward_input", "wbmm_hier_backward",
+           "wbmm_hier_backward_workspace_bytes", "wbmm_backward",
            "wbmm_backward_input", "wbmm_backward_table", "wbmm_backward_table_workspace_bytes",
            "wbmm_backward_workspace_bytes", "wbmm_forward", "wbmm_relative_index",
            "wbmm_status_string", "wbmm_version"]

@@ -7,7 +7,9 @@ built, or a call fails, an exception is raised.
 
 Names follow the C entry points: ``wbmm_forward``, ``wbmm_backward_input``,
 ``wbmm_backward_table``, ``wbmm_backward_table_workspace_bytes``,
-``wbmm_backward``, ``wbmm_backward_workspace_bytes``, ``wbmm_relative_index``,
+``wbmm_backward``, ``wbmm_backward_workspace_bytes``, the hierarchical form
+``wbmm_hier_forward``, ``wbmm_hier_backward_input``, ``wbmm_hier_backward``,
+``wbmm_hier_backward_workspace_bytes``, and ``wbmm_relative_index``,
 ``wbmm_status_string``.
 """
 from __future__ import annotations
@@ -28,7 +30,9 @@ DTYPE_CODES = {torch.float32: 0, torch.bfloat16: 1, torch.float16: 2}
 
 EXPORTED = ("wbmm_forward", "wbmm_backward_input", "wbmm_backward_table",
             "wbmm_backward_table_workspace_bytes", "wbmm_backward",
-            "wbmm_backward_workspace_bytes", "wbmm_status_string",
+            "wbmm_backward_workspace_bytes", "wbmm_hier_forward",
+            "wbmm_hier_backward_input", "wbmm_hier_backward",
+            "wbmm_hier_backward_workspace_bytes", "wbmm_status_string",
             "wbmm_relative_index", "wbmm_version")
 
 _lib = None
@@ -63,6 +67,14 @@ def load_library(path: str = LIB_PATH):
     lib.wbmm_backward_workspace_bytes.restype = ctypes.c_size_t
     lib.wbmm_backward.argtypes = [vp, vp, vp, vp, vp, vp, ctypes.c_size_t] + shape
     lib.wbmm_backward.restype = st
+    lib.wbmm_hier_forward.argtypes = [vp, vp, vp, vp] + shape
+    lib.wbmm_hier_forward.restype = st
+    lib.wbmm_hier_backward_input.argtypes = [vp, vp, vp, vp] + shape
+    lib.wbmm_hier_backward_input.restype = st
+    lib.wbmm_hier_backward_workspace_bytes.argtypes = [i64, i64, i64, i64, ci, ci]
+    lib.wbmm_hier_backward_workspace_bytes.restype = ctypes.c_size_t
+    lib.wbmm_hier_backward.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t] + shape
+    lib.wbmm_hier_backward.restype = st
     lib.wbmm_status_string.argtypes = [st]
     lib.wbmm_status_string.restype = ctypes.c_char_p
     lib.wbmm_relative_index.argtypes = [ci, ctypes.POINTER(ctypes.c_int32)]
@@ -242,6 +254,71 @@ def wbmm_backward(x: torch.Tensor, dy: torch.Tensor, table: torch.Tensor, w: int
     return dx, dtable
 
 
+def _hier_like(fn_name, src, tg, tl, wl, out, stream):
+    _check_tensor(src, "input")
+    _check_tensor(tg, "table_g")
+    _check_tensor(tl, "table_l")
+    if src.dim() != 4:
+        raise ValueError("input must be [B, C, H, W]")
+    B, C, H, W = src.shape
+    for t in (tg, tl):
+        if t.dtype != src.dtype or t.device != src.device:
+            raise ValueError("tables must match the input's dtype and device")
+    if out is None:
+        out = torch.empty_like(src)
+    else:
+        _check_tensor(out, "out")
+        if out.shape != src.shape or out.dtype != src.dtype or out.device != src.device:
+            raise ValueError("out must match the input's shape, dtype and device")
+    with torch.cuda.device(src.device):
+        st = getattr(load_library(), fn_name)(_ptr(src), _ptr(tg), _ptr(tl), _ptr(out), B, C, H, W,
+                                              int(wl), _code(src.dtype), _stream(src, stream))
+    if st != WBMM_OK:
+        raise WbmmError(st, fn_name)
+    return out
+
+
+def wbmm_hier_forward(x, table_g, table_l, wl: int, out=None, stream=None):
+    """Hierarchical form: y = x M_fused per 2wl x 2wl window, table_g
+    [C,(4wl-1)^2], table_l [C,(2wl-1)^2]."""
+    return _hier_like("wbmm_hier_forward", x, table_g, table_l, wl, out, stream)
+
+
+def wbmm_hier_backward_input(dy, table_g, table_l, wl: int, out=None, stream=None):
+    """dx = dy M_fused^T of the hierarchical form."""
+    return _hier_like("wbmm_hier_backward_input", dy, table_g, table_l, wl, out, stream)
+
+
+def wbmm_hier_backward_workspace_bytes(shape, wl: int, dtype) -> int:
+    B, C, H, W = shape
+    return int(load_library().wbmm_hier_backward_workspace_bytes(B, C, H, W, int(wl), _code(dtype)))
+
+
+def wbmm_hier_backward(x, dy, table_g, table_l, wl: int, workspace=None, stream=None):
+    """All gradients of the hierarchical form: (dx, dtable_g, dtable_l), the
+    table gradients float32."""
+    _check_tensor(x, "x")
+    _check_tensor(dy, "dy")
+    if dy.shape != x.shape or dy.dtype != x.dtype or dy.device != x.device:
+        raise ValueError("dy must match x's shape, dtype and device")
+    B, C, H, W = x.shape
+    dx = torch.empty_like(x)
+    dtg = torch.empty((C, (4 * int(wl) - 1) ** 2), dtype=torch.float32, device=x.device)
+    dtl = torch.empty((C, (2 * int(wl) - 1) ** 2), dtype=torch.float32, device=x.device)
+    need = wbmm_hier_backward_workspace_bytes(x.shape, wl, x.dtype)
+    if workspace is None and need > 0:
+        workspace = _cached_workspace(x.device, need, stream, ("hier", tuple(x.shape), int(wl), x.dtype))
+    ws_ptr = ctypes.c_void_p(workspace.data_ptr() if workspace is not None else 0)
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    with torch.cuda.device(x.device):
+        st = load_library().wbmm_hier_backward(_ptr(x), _ptr(dy), _ptr(table_g), _ptr(table_l), _ptr(dx),
+                                               _ptr(dtg), _ptr(dtl), ws_ptr, ws_bytes, B, C, H, W, int(wl),
+                                               _code(x.dtype), _stream(x, stream))
+    if st != WBMM_OK:
+        raise WbmmError(st, "wbmm_hier_backward")
+    return dx, dtg, dtl
+
+
 def wbmm_relative_index(w: int) -> torch.Tensor:
     """The int32 [d, d] index I of eq. index_computation (host tensor)."""
     d = int(w) * int(w)
@@ -287,3 +364,25 @@ class WBMMFunction(torch.autograd.Function):
 def wbmm(x, table, w):
     """Differentiable WBMM: y = WBMM(x; table, w)."""
     return WBMMFunction.apply(x, table, w)
+
+
+class WBMMHierFunction(torch.autograd.Function):
+    """Autograd of the hierarchical form (table gradients cast to the tables'
+    dtype)."""
+
+    @staticmethod
+    def forward(ctx, x, table_g, table_l, wl):
+        ctx.wl = int(wl)
+        ctx.save_for_backward(x, table_g, table_l)
+        return wbmm_hier_forward(x.contiguous(), table_g.contiguous(), table_l.contiguous(), ctx.wl)
+
+    @staticmethod
+    def backward(ctx, dy):
+        x, tg, tl = ctx.saved_tensors
+        dx, dtg, dtl = wbmm_hier_backward(x, dy.contiguous(), tg, tl, ctx.wl)
+        return dx, dtg.to(tg.dtype), dtl.to(tl.dtype), None
+
+
+def wbmm_hier(x, table_g, table_l, wl):
+    """Differentiable hierarchical WBMM (global windows 2 wl, local wl)."""
+    return WBMMHierFunction.apply(x, table_g, table_l, wl)

@@ -159,6 +159,89 @@ wbmm_status wbmm_backward(const void *x, const void *dy, const void *table, void
   return from_hip(wbmm::launch_backward((Dt)dtype, x, dy, table, dx, dtable, workspace, g, (hipStream_t)stream));
 }
 
+// ---- hierarchical (global + local) form: global window 2 wl, local wl
+
+static wbmm_status hier_shapes(int64_t B, int64_t C, int64_t H, int64_t W, int wl, wbmm_dtype dtype, Geom *gg,
+                               Geom *gl, int64_t *bytes) {
+  if (!valid_dtype((int)dtype)) return WBMM_ERR_UNSUPPORTED;
+  if (wl <= 0) return WBMM_ERR_INVALID_ARG;
+  if (2 * wl > wbmm::kMaxWindow) return WBMM_ERR_UNSUPPORTED;
+  wbmm_status s = check_shape(B, C, H, W, 2 * wl, dtype, gg, bytes);
+  if (s != WBMM_OK) return s;
+  return check_shape(B, C, H, W, wl, dtype, gl, bytes);
+}
+
+static wbmm_status hier_forward_like(const void *in, const void *tg, const void *tl, void *out, int64_t B, int64_t C,
+                                     int64_t H, int64_t W, int wl, wbmm_dtype dtype, void *stream, bool rev) {
+  Geom gg, gl;
+  int64_t bytes = 0;
+  wbmm_status s = hier_shapes(B, C, H, W, wl, dtype, &gg, &gl, &bytes);
+  if (s != WBMM_OK) return s;
+  if (!in || !tg || !tl || !out) return WBMM_ERR_INVALID_ARG;
+  const size_t es = elem_size(dtype);
+  if (!aligned(in, es) || !aligned(tg, es) || !aligned(tl, es) || !aligned(out, es)) return WBMM_ERR_INVALID_ARG;
+  const int64_t kg = (int64_t)(4 * wl - 1) * (4 * wl - 1), kl = (int64_t)(2 * wl - 1) * (2 * wl - 1);
+  if (overlap(in, bytes, out, bytes) || overlap(tg, C * kg * (int64_t)es, out, bytes) ||
+      overlap(tl, C * kl * (int64_t)es, out, bytes))
+    return WBMM_ERR_INVALID_ARG;
+  return from_hip(wbmm::launch_hier_forward((Dt)dtype, in, tg, tl, out, gg, rev, (hipStream_t)stream));
+}
+
+wbmm_status wbmm_hier_forward(const void *x, const void *table_g, const void *table_l, void *y, int64_t B,
+                              int64_t C, int64_t H, int64_t W, int wl, wbmm_dtype dtype, void *stream) {
+  return hier_forward_like(x, table_g, table_l, y, B, C, H, W, wl, dtype, stream, false);
+}
+
+wbmm_status wbmm_hier_backward_input(const void *dy, const void *table_g, const void *table_l, void *dx, int64_t B,
+                                     int64_t C, int64_t H, int64_t W, int wl, wbmm_dtype dtype, void *stream) {
+  return hier_forward_like(dy, table_g, table_l, dx, B, C, H, W, wl, dtype, stream, true);
+}
+
+size_t wbmm_hier_backward_workspace_bytes(int64_t B, int64_t C, int64_t H, int64_t W, int wl, wbmm_dtype dtype) {
+  Geom gg, gl;
+  int64_t bytes = 0;
+  if (hier_shapes(B, C, H, W, wl, dtype, &gg, &gl, &bytes) != WBMM_OK) return 0;
+  const size_t a = wbmm::dtable_workspace_bytes((Dt)dtype, gg), b = wbmm::dtable_workspace_bytes((Dt)dtype, gl);
+  return a > b ? a : b;
+}
+
+wbmm_status wbmm_hier_backward(const void *x, const void *dy, const void *table_g, const void *table_l, void *dx,
+                               float *dtable_g, float *dtable_l, void *workspace, size_t workspace_bytes, int64_t B,
+                               int64_t C, int64_t H, int64_t W, int wl, wbmm_dtype dtype, void *stream) {
+  Geom gg, gl;
+  int64_t bytes = 0;
+  wbmm_status s = hier_shapes(B, C, H, W, wl, dtype, &gg, &gl, &bytes);
+  if (s != WBMM_OK) return s;
+  if (!x || !dy || !table_g || !table_l || !dx || !dtable_g || !dtable_l) return WBMM_ERR_INVALID_ARG;
+  const size_t es = elem_size(dtype);
+  if (!aligned(x, es) || !aligned(dy, es) || !aligned(table_g, es) || !aligned(table_l, es) || !aligned(dx, es) ||
+      !aligned(dtable_g, 4) || !aligned(dtable_l, 4))
+    return WBMM_ERR_INVALID_ARG;
+  const int64_t kg = (int64_t)(4 * wl - 1) * (4 * wl - 1), kl = (int64_t)(2 * wl - 1) * (2 * wl - 1);
+  struct Buf { const void *p; int64_t n; };
+  const Buf ins[] = {{x, bytes}, {dy, bytes}, {table_g, C * kg * (int64_t)es}, {table_l, C * kl * (int64_t)es}};
+  const Buf outs[] = {{dx, bytes}, {dtable_g, C * kg * 4}, {dtable_l, C * kl * 4}};
+  for (const Buf &o : outs) {
+    for (const Buf &i : ins)
+      if (overlap(o.p, o.n, i.p, i.n)) return WBMM_ERR_INVALID_ARG;
+    for (const Buf &o2 : outs)
+      if (&o2 != &o && overlap(o.p, o.n, o2.p, o2.n)) return WBMM_ERR_INVALID_ARG;
+  }
+  const size_t need = wbmm_hier_backward_workspace_bytes(B, C, H, W, wl, dtype);
+  if (need > 0) {
+    if (!workspace || workspace_bytes < need || !aligned(workspace, 4)) return WBMM_ERR_INVALID_ARG;
+    for (const Buf &b : ins)
+      if (overlap(workspace, (int64_t)need, b.p, b.n)) return WBMM_ERR_INVALID_ARG;
+    for (const Buf &b : outs)
+      if (overlap(workspace, (int64_t)need, b.p, b.n)) return WBMM_ERR_INVALID_ARG;
+  }
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e = wbmm::launch_hier_forward((Dt)dtype, dy, table_g, table_l, dx, gg, true, st);
+  if (e == hipSuccess) e = wbmm::launch_dtable((Dt)dtype, x, dy, dtable_g, workspace, gg, st);
+  if (e == hipSuccess) e = wbmm::launch_dtable((Dt)dtype, x, dy, dtable_l, workspace, gl, st);
+  return from_hip(e);
+}
+
 const char *wbmm_status_string(wbmm_status s) {
   switch (s) {
     case WBMM_OK: return "WBMM_OK";

@@ -47,6 +47,13 @@ hipError_t launch_backward(Dt dt, const void *x, const void *dy, const void *tab
   return e->bwd(x, dy, table, dx, dtable, workspace, g, stream);
 }
 
+hipError_t launch_hier_forward(Dt dt, const void *x, const void *table_g, const void *table_l, void *y,
+                               const Geom &g, bool reverse_tables, hipStream_t stream) {
+  const Entry *e = find(dt, g.w);
+  if (!e) return hipErrorInvalidValue;
+  return e->hier_fwd(x, table_g, table_l, y, g, reverse_tables, stream);
+}
+
 DtPlan plan_dtable(Dt dt, const Geom &g) {
   const Entry *e = find(dt, g.w);
   if (!e) return DtPlan{0, 0};

@@ -42,6 +42,10 @@ hipError_t launch_dtable(Dt dt, const void *x, const void *dy, float *dtable,
 hipError_t launch_backward(Dt dt, const void *x, const void *dy, const void *table,
                            void *dx, float *dtable, void *workspace, const Geom &g,
                            hipStream_t stream);
+// Hierarchical form: g.w is the global window (2 wl).
+hipError_t launch_hier_forward(Dt dt, const void *x, const void *table_g,
+                               const void *table_l, void *y, const Geom &g,
+                               bool reverse_tables, hipStream_t stream);
 
 // Per-(dtype, window) entry points, defined by the wbmm_inst.hip
 // translation units and collected into tables by wbmm_dispatch.cpp.
@@ -50,11 +54,13 @@ typedef hipError_t (*DtFn)(const void *, const void *, float *, void *, const Ge
 typedef DtPlan (*PlanFn)(const Geom &);
 typedef hipError_t (*BwdFn)(const void *, const void *, const void *, void *, float *, void *, const Geom &,
                             hipStream_t);
+typedef hipError_t (*HierFn)(const void *, const void *, const void *, void *, const Geom &, bool, hipStream_t);
 struct Entry {
   FwdFn fwd;
   DtFn dtable;
   PlanFn plan;
   BwdFn bwd;
+  HierFn hier_fwd;
 };
 
 }  // namespace wbmm

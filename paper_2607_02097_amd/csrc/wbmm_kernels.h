@@ -108,6 +108,11 @@ template <> __device__ inline uint32_t pack2<TagF16>(float a, float b) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
+// One stored 16-bit value as float32 (exact).
+template <class Tag> __device__ inline float to_f32(u16 v);
+template <> __device__ inline float to_f32<TagBF16>(u16 v) { return __builtin_bit_cast(float, (uint32_t)v << 16); }
+template <> __device__ inline float to_f32<TagF16>(u16 v) { return (float)__builtin_bit_cast(_Float16, v); }
+
 template <class Tag> __device__ inline f32x4 mma(typename Tag::Frag a, typename Tag::Frag b, f32x4 c);
 template <> __device__ inline f32x4 mma<TagF32>(float a, float b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
@@ -307,7 +312,30 @@ struct FwdCfg {
   static constexpr int K2 = K1 * K1;
   static constexpr int TS_LEN = rup(K2, 8);
   static constexpr int TB_LEN = Tag::W16 ? K1 * RP * RP : 0;
+  // hierarchical form (WIN = 2 wl): the local table of the wl x wl
+  // sub-windows and its Toeplitz blocks
+  static constexpr int WL = WIN / 2;
+  static constexpr int K1L = WL > 0 ? 2 * WL - 1 : 1;
+  static constexpr int K2L = K1L * K1L;
+  static constexpr int TSL_LEN = rup(K2L, 8);
+  static constexpr int TBL_LEN = Tag::W16 ? K1L * RP * RP : 0;
 };
+
+// Rows of a window touched by the A operand of K step s and by output tile t
+// (row-padded positions: a K step covers 32 / RP rows, a tile 16 / RP rows).
+template <class Tag, int WIN>
+__host__ __device__ constexpr bool fwd_rows_meet(int s, int t, bool same_half_only) {
+  typedef FwdCfg<Tag, WIN> G;
+  constexpr int RK = Tag::KS / G::RP > 0 ? Tag::KS / G::RP : 1;  // rows per K step (16-bit)
+  constexpr int RT = 16 / G::RP;                                 // rows per output tile
+  for (int a = 0; a < RK; ++a)
+    for (int b = 0; b < RT; ++b) {
+      const int hi = RK * s + a, ho = RT * t + b;
+      if (hi >= WIN || ho >= WIN) continue;
+      if (same_half_only ? ((hi < G::WL) == (ho < G::WL)) : hi == ho) return true;
+    }
+  return false;
+}
 
 // The forward kernel runs four waves per workgroup.  Each wave owns a run of
 // 16-window sub-tiles and pipelines them through one private LDS buffer: the
@@ -318,10 +346,11 @@ struct FwdCfg {
 constexpr int kFwdWaves = 4;
 constexpr int kFwdThreads = 64 * kFwdWaves;
 
-template <class Tag, int WIN>
+template <class Tag, int WIN, bool HIER = false>
 __host__ __device__ constexpr size_t fwd_lds_bytes() {
   typedef FwdCfg<Tag, WIN> G;
-  return (size_t)kFwdWaves * 16 * G::LDSW * Tag::ES + (size_t)(G::TS_LEN + G::TB_LEN) * Tag::ES;
+  return (size_t)kFwdWaves * 16 * G::LDSW * Tag::ES + (size_t)(G::TS_LEN + G::TB_LEN) * Tag::ES +
+         (HIER ? (size_t)(G::TSL_LEN + G::TBL_LEN) * Tag::ES : 0);
 }
 
 // Wave-level ordering of LDS accesses made by different lanes of one wave.
@@ -397,15 +426,25 @@ __device__ __attribute__((always_inline)) inline void store_sub(const KArgs &a, 
 
 // The table row of channel c (read back to front for the input gradient)
 // -> Ts with coalesced loads; for 16-bit, the Toeplitz blocks
-// TB[dh][x_out][x_in] of M_c gathered from it.  Ends with a workgroup barrier.
-template <class Tag, int WIN, bool REV>
-__device__ __attribute__((always_inline)) inline void fwd_tables(const typename Tag::S *__restrict__ tab, int64_t c,
-                                                                  typename Tag::S *Ts, typename Tag::S *TB, int tid) {
+// TB[dh][x_out][x_in] of M_c gathered from it.  The hierarchical form also
+// stages the local table (-> Tsl) and, for 16-bit, its blocks
+// TBL[dh][x_out][x_in], zero unless x_in and x_out lie in the same half of the
+// window (the same local sub-window column).  Ends with a workgroup barrier.
+template <class Tag, int WIN, bool REV, bool HIER = false>
+__device__ __attribute__((always_inline)) inline void fwd_tables(const typename Tag::S *__restrict__ tab,
+                                                                  const typename Tag::S *__restrict__ tabl, int64_t c,
+                                                                  typename Tag::S *Ts, typename Tag::S *TB,
+                                                                  typename Tag::S *Tsl, typename Tag::S *TBL, int tid) {
   typedef typename Tag::S S;
   typedef FwdCfg<Tag, WIN> G;
   constexpr int RP = G::RP, K1 = G::K1, K2 = G::K2;
   const S *tc = tab + c * K2;
   for (int k = tid; k < K2; k += kFwdThreads) Ts[k] = tc[REV ? K2 - 1 - k : k];
+  if constexpr (HIER) {
+    constexpr int K2L = G::K2L;
+    const S *tl = tabl + c * K2L;
+    for (int k = tid; k < K2L; k += kFwdThreads) Tsl[k] = tl[REV ? K2L - 1 - k : k];
+  }
   if constexpr (Tag::W16) {
     __syncthreads();
     constexpr int CPR = RP / 8;               // 8-element chunks per TB row
@@ -426,6 +465,28 @@ __device__ __attribute__((always_inline)) inline void fwd_tables(const typename 
         }
       }
       *reinterpret_cast<u16x8 *>(&TB[row * RP + xi0]) = v;
+    }
+    if constexpr (HIER) {
+      constexpr int WL = G::WL, K1L = G::K1L;
+      constexpr int NCHL = K1L * RP * CPR;
+      for (int ch = tid; ch < NCHL; ch += kFwdThreads) {
+        const int row = ch / CPR;               // = dhl * RP + x_out
+        const int xi0 = (ch - row * CPR) * 8;
+        const int dhl = row / RP;
+        const int xo = row - dhl * RP;
+        u16x8 v = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+        if (xo < WIN) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int xi = xi0 + e;
+            const bool same = xi < WIN && (xi < WL) == (xo < WL);
+            const int k = dhl * K1L + (same ? xi - xo + WL - 1 : 0);
+            const u16 t = Tsl[k];
+            v[e] = same ? t : (u16)0;
+          }
+        }
+        *reinterpret_cast<u16x8 *>(&TBL[row * RP + xi0]) = v;
+      }
     }
   }
   __syncthreads();
@@ -448,18 +509,40 @@ __device__ __attribute__((always_inline)) inline typename Tag::Frag fwd_bfrag(co
   return typename Tag::Frag{0, 0, 0, 0, 0, 0, 0, 0};
 }
 
-template <class Tag, int WIN, bool REV>
+// Hierarchical form, 16-bit: the local-table fragment of K step s and output
+// tile t for lane (g, ln) (zero where input and output rows lie in different
+// halves of the window).
+template <class Tag, int WIN>
+__device__ __attribute__((always_inline)) inline typename Tag::Frag fwd_lfrag(const typename Tag::S *TBL, int s, int t,
+                                                                               int g, int ln) {
+  typedef FwdCfg<Tag, WIN> G;
+  constexpr int RP = G::RP, WL = G::WL;
+  int hi, ho, xi0;
+  if (RP == 16) { hi = 2 * s + (g >> 1); ho = t; xi0 = 8 * (g & 1); }
+  else { hi = 4 * s + g; ho = 2 * t + (ln >> 3); xi0 = 0; }
+  const int xo = ln & (RP - 1);
+  const bool same = hi < WIN && ho < WIN && (hi < WL) == (ho < WL);
+  const int dhl = same ? hi - ho + WL - 1 : 0;
+  const typename Tag::Frag f = *reinterpret_cast<const typename Tag::Frag *>(&TBL[(dhl * RP + xo) * RP + xi0]);
+  return same ? f : typename Tag::Frag{0, 0, 0, 0, 0, 0, 0, 0};
+}
+
+template <class Tag, int WIN, bool REV, bool HIER = false>
 __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename Tag::S *__restrict__ x,
                                                                   const typename Tag::S *__restrict__ tab,
+                                                                  const typename Tag::S *__restrict__ tabl,
                                                                   typename Tag::S *__restrict__ y, KArgs a) {
   typedef typename Tag::S S;
   typedef typename Tag::Frag Frag;
   typedef FwdCfg<Tag, WIN> G;
-  constexpr int RP = G::RP, LDSW = G::LDSW, K1 = G::K1, K2 = G::K2;
+  constexpr int RP = G::RP, LDSW = G::LDSW, K1 = G::K1;
+  static_assert(!HIER || WIN % 2 == 0, "the hierarchical form needs an even window");
 
   extern __shared__ __align__(16) unsigned char smem[];
   S *Ts = reinterpret_cast<S *>(smem + kFwdWaves * 16 * LDSW * Tag::ES);
   S *TB = Ts + G::TS_LEN;
+  S *Tsl = TB + G::TB_LEN;  // hierarchical form only
+  S *TBL = Tsl + G::TSL_LEN;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -479,7 +562,7 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
   //         M_c for 16-bit, the table itself for float32) -> LDS
   SubRows<Tag, WIN> nxt;
   if (nsub > 0) load_sub<Tag, WIN>(a, x, c, n0 + first * 16, nwin - first * 16, lane, nxt);
-  fwd_tables<Tag, WIN, REV>(tab, c, Ts, TB, tid);
+  fwd_tables<Tag, WIN, REV, HIER>(tab, tabl, c, Ts, TB, Tsl, TBL, tid);
 
   const int g = lane >> 4;   // lane group
   const int ln = lane & 15;  // row (A) / column (B, C) inside a 16x16 tile
@@ -516,12 +599,24 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
         for (int s = 0; s < S_; ++s) {
           acc0 = mma<Tag>(af[s], bf[2 * s - t0 + NT - 1], acc0);
           if (t0 + 1 < NT) acc1 = mma<Tag>(af[s], bf[2 * s - t0 - 1 + NT - 1], acc1);
+          if constexpr (HIER) {
+            // local sub-window blocks
+            if (fwd_rows_meet<Tag, WIN>(s, t0, true)) acc0 = mma<Tag>(af[s], fwd_lfrag<Tag, WIN>(TBL, s, t0, g, ln), acc0);
+            if (t0 + 1 < NT && fwd_rows_meet<Tag, WIN>(s, t0 + 1, true))
+              acc1 = mma<Tag>(af[s], fwd_lfrag<Tag, WIN>(TBL, s, t0 + 1, g, ln), acc1);
+          }
         }
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
           const int t = t0 + h;
           if (t >= NT) continue;
-          const f32x4 acc = h ? acc1 : acc0;
+          f32x4 acc = h ? acc1 : acc0;
+          if constexpr (HIER) {
+            // the two identity shortcuts: + 2 x at the output's own position,
+            // read before the result overwrites it (pads hold zero)
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr) acc[rr] += 2.f * to_f32<Tag>(outp[rr * LDSW + 16 * t]);
+          }
           const uint32_t lo = pack2<Tag>(acc[0], acc[1]);
           const uint32_t hi = pack2<Tag>(acc[2], acc[3]);
           outp[0 * LDSW + 16 * t] = (u16)(lo & 0xffffu);
@@ -579,6 +674,13 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
           float bv = 0.f;
           if (xo < WIN && xi < WIN && dh >= -(WIN - 1) && dh <= WIN - 1)
             bv = Ts[(dh + WIN - 1) * K1 + xi - xo + WIN - 1];
+          if constexpr (HIER) {
+            // local sub-window entry and the two identity shortcuts
+            constexpr int WL = G::WL, K1L = G::K1L;
+            if (xo < WIN && xi < WIN && hi < WIN && ho < WIN && (hi < WL) == (ho < WL) && (xi < WL) == (xo < WL))
+              bv += Tsl[(dh + WL - 1) * K1L + xi - xo + WL - 1];
+            if (hi == ho && xi == xo && xi < WIN && hi < WIN) bv += 2.f;
+          }
           acc = mma<Tag>(af[s], bv, acc);
         }
 #pragma unroll
@@ -677,7 +779,7 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_band_kernel(const typ
 
   uint4 nxt[KC];
   if (nsub > 0) band_load<WIN>(a, x, c, n0 + first * 16, bands_of(0), lane, nxt);
-  fwd_tables<Tag, WIN, REV>(tab, c, Ts, TB, tid);
+  fwd_tables<Tag, WIN, REV>(tab, nullptr, c, Ts, TB, nullptr, nullptr, tid);
 
   const int g = lane >> 4;
   const int ln = lane & 15;
@@ -1440,10 +1542,35 @@ static hipError_t run_forward(const void *x, const void *t, void *y, const Geom 
   // instructions only)
   static_assert(lds <= 160 * 1024, "workgroup LDS above the 160 KB of a compute unit");
   if (rev)
-    wbmm_fwd_kernel<Tag, WIN, true><<<grid, dim3(kFwdThreads), lds, st>>>((const S *)x, (const S *)t, (S *)y, a);
+    wbmm_fwd_kernel<Tag, WIN, true><<<grid, dim3(kFwdThreads), lds, st>>>((const S *)x, (const S *)t, nullptr, (S *)y, a);
   else
-    wbmm_fwd_kernel<Tag, WIN, false><<<grid, dim3(kFwdThreads), lds, st>>>((const S *)x, (const S *)t, (S *)y, a);
+    wbmm_fwd_kernel<Tag, WIN, false><<<grid, dim3(kFwdThreads), lds, st>>>((const S *)x, (const S *)t, nullptr, (S *)y, a);
   return hipGetLastError();
+}
+
+// Hierarchical form, window WIN = 2 wl: y = x M_fused per window (both tables
+// read back to front for the input gradient).
+template <class Tag, int WIN>
+static hipError_t run_hier_forward(const void *x, const void *tg, const void *tl, void *y, const Geom &g, bool rev,
+                                   hipStream_t st) {
+  if constexpr (WIN % 2 != 0) {
+    return hipErrorInvalidValue;
+  } else {
+    typedef typename Tag::S S;
+    KArgs a = make_args(g);
+    a.tile = pick_fwd_tile<Tag, WIN>(g);
+    a.tiles_per_ch = (int)cdiv64(g.N, a.tile);
+    const dim3 grid((unsigned)(g.C * a.tiles_per_ch));
+    constexpr size_t lds = fwd_lds_bytes<Tag, WIN, true>();
+    static_assert(lds <= 160 * 1024, "workgroup LDS above the 160 KB of a compute unit");
+    if (rev)
+      wbmm_fwd_kernel<Tag, WIN, true, true><<<grid, dim3(kFwdThreads), lds, st>>>((const S *)x, (const S *)tg,
+                                                                                  (const S *)tl, (S *)y, a);
+    else
+      wbmm_fwd_kernel<Tag, WIN, false, true><<<grid, dim3(kFwdThreads), lds, st>>>((const S *)x, (const S *)tg,
+                                                                                   (const S *)tl, (S *)y, a);
+    return hipGetLastError();
+  }
 }
 
 template <class Tag, int WIN>

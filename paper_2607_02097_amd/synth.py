@@ -33,7 +33,8 @@ class Workload:
     H: int
     W: int
     w: int
-    passes: tuple       # subset of ("fwd", "dx", "dt")
+    passes: tuple       # subset of ("fwd", "dx", "dt"); hierarchical: ("hfwd", "hbwd")
+    hier: bool = False  # hierarchical form: global windows w, local w / 2
 
     @property
     def table_len(self) -> int:
@@ -46,10 +47,16 @@ class Workload:
         return self.B * nh * nw
 
     def flops(self, passes=None) -> float:
-        """Algorithmic flops, 2*C*N*d^2 per pass (no padding, no re-reads)."""
+        """Algorithmic flops, 2*C*N*d^2 per pass (no padding, no re-reads).
+        Hierarchical form: the forward and the input gradient are products
+        with the d x d fused matrix; the table gradients are those of the two
+        scales (the local one a quarter of the global one)."""
         d = self.w * self.w
         per = 2.0 * self.C * self.windows_per_channel * d * d
-        return per * len(passes if passes is not None else self.passes)
+        total = 0.0
+        for p in (passes if passes is not None else self.passes):
+            total += per * {"hbwd": 2.25}.get(p, 1.0)
+        return total
 
 
 # The five workloads: parity small case, w=7 memory-bound forward, and three
@@ -61,6 +68,23 @@ WORKLOADS = {
     "bf16_b128_c384_14_w14": Workload("bf16_b128_c384_14_w14", "bf16", 128, 384, 14, 14, 14, ("fwd", "dx", "dt")),
     "bf16_b16_c64_112_w14": Workload("bf16_b16_c64_112_w14", "bf16", 16, 64, 112, 112, 14, ("fwd", "dx", "dt")),
 }
+
+
+# Hierarchical form (global 14 x 14 windows, local 7 x 7 sub-windows): the
+# headline stage shape, and a Pico-width map at dense-prediction resolution.
+HIER_WORKLOADS = {
+    "bf16_b64_c192_28_hier7": Workload("bf16_b64_c192_28_hier7", "bf16", 64, 192, 28, 28, 14,
+                                       ("hfwd", "hbwd"), hier=True),
+    "bf16_b16_c64_112_hier7": Workload("bf16_b16_c64_112_hier7", "bf16", 16, 64, 112, 112, 14,
+                                       ("hfwd", "hbwd"), hier=True),
+}
+
+
+def draw_local_table(C: int, wl: int, dtype: str, seed: int = 0):
+    """Seeded local table of the hierarchical form, N(0, 0.02^2), as
+    (stored, float64) like draw()."""
+    r = np.random.default_rng(seed + 7919)
+    return round_to(0.02 * r.standard_normal((C, (2 * wl - 1) ** 2)), dtype)
 
 
 def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:

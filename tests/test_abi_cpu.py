@@ -134,3 +134,40 @@ def test_backward_rejects_bad_arguments(lib):
     assert call(**big) == E                                         # no workspace
     assert call(ws=FAKE * 320, wsb=need - 4, **big) == E            # too small
     assert call(ws=FAKE * 192 + 64, wsb=need, **big) == E           # overlaps dx
+
+
+def test_hier_rejects_bad_arguments(lib):
+    E, U = W.WBMM_ERR_INVALID_ARG, W.WBMM_ERR_UNSUPPORTED
+    vp = ctypes.c_void_p
+
+    def fwd_call(x=FAKE, tg=FAKE * 4, tl=FAKE * 6, y=FAKE * 8, B=1, C=2, H=14, Wd=14, wl=7, d=1,
+                 fn="wbmm_hier_forward"):
+        return getattr(lib, fn)(vp(x), vp(tg), vp(tl), vp(y), B, C, H, Wd, wl, d, None)
+
+    for fn in ("wbmm_hier_forward", "wbmm_hier_backward_input"):
+        for k in ("x", "tg", "tl", "y"):
+            assert fwd_call(fn=fn, **{k: 0}) == E, (fn, k)
+        assert fwd_call(fn=fn, wl=0) == E
+        assert fwd_call(fn=fn, wl=9) == U
+        assert fwd_call(fn=fn, d=4) == U
+        assert fwd_call(fn=fn, y=FAKE) == E            # output aliases input
+        assert fwd_call(fn=fn, y=FAKE * 6 + 2) == E    # output overlaps the local table
+        assert fwd_call(fn=fn, x=FAKE + 1) == E        # misaligned
+
+    def bwd_call(x=FAKE, dy=FAKE * 8, tg=FAKE * 12, tl=FAKE * 14, dx=FAKE * 16, dtg=FAKE * 20, dtl=FAKE * 24,
+                 ws=0, wsb=0, B=1, C=2, H=14, Wd=14, wl=7, d=1):
+        return lib.wbmm_hier_backward(vp(x), vp(dy), vp(tg), vp(tl), vp(dx), vp(dtg), vp(dtl), vp(ws), wsb,
+                                      B, C, H, Wd, wl, d, None)
+
+    for k in ("x", "dy", "tg", "tl", "dx", "dtg", "dtl"):
+        assert bwd_call(**{k: 0}) == E, k
+    assert bwd_call(dtl=FAKE * 20 + 64) == E          # the two table gradients overlap
+    assert bwd_call(dx=FAKE * 8) == E                 # dx aliases dy
+    assert bwd_call(wl=9) == U
+    need = lib.wbmm_hier_backward_workspace_bytes(64, 192, 28, 28, 7, 1)
+    assert need >= max(lib.wbmm_backward_table_workspace_bytes(64, 192, 28, 28, 14, 1),
+                       lib.wbmm_backward_table_workspace_bytes(64, 192, 28, 28, 7, 1)) > 0
+    big = dict(B=64, C=192, H=28, Wd=28, x=FAKE, dy=FAKE * 64, tg=FAKE * 128, tl=FAKE * 132,
+               dx=FAKE * 192, dtg=FAKE * 256, dtl=FAKE * 260)
+    assert bwd_call(**big) == E                                  # no workspace
+    assert bwd_call(ws=FAKE * 320, wsb=need - 4, **big) == E     # too small

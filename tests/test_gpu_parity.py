@@ -365,3 +365,86 @@ def test_workspace_counters_reset_between_calls():
     small = W.wbmm_backward_table(xs, dys, 14, workspace=ws)
     torch.cuda.synchronize()
     assert torch.equal(small, ref[:48])
+
+
+# ------------------------------------------------------------- hierarchical
+
+HIER = [
+    # (B, C, H, W, wl): global windows 2 wl, ragged and padded maps
+    (2, 3, 28, 28, 7),
+    (1, 2, 30, 17, 7),
+    (2, 2, 16, 16, 4),
+    (1, 2, 21, 35, 5),
+    (2, 1, 32, 32, 8),
+    (2, 2, 12, 20, 3),
+    (3, 2, 8, 12, 2),
+    (2, 2, 6, 6, 1),
+    (1, 2, 12, 12, 6),
+]
+
+
+def draw_hier(B, C, H, Wd, wl, dtype, seed):
+    d = draw(B, C, H, Wd, 2 * wl, dtype, seed=seed)
+    r = np.random.default_rng(seed + 1000)
+    d["tl"], d["tl64"] = synth.round_to(0.02 * r.standard_normal((C, (2 * wl - 1) ** 2)), dtype)
+    return d
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("shape", HIER, ids=lambda s: "B%dC%dH%dW%dwl%d" % s)
+def test_hier_parity(shape, dtype):
+    B, C, H, Wd, wl = shape
+    d = draw_hier(B, C, H, Wd, wl, dtype, seed=31)
+    x, tg, tl, dy = (to_device(d[k], dtype) for k in ("x", "t", "tl", "dy"))
+    y = W.wbmm_hier_forward(x, tg, tl, wl)
+    dx, dtg, dtl = W.wbmm_hier_backward(x, dy, tg, tl, wl)
+    dx2 = W.wbmm_hier_backward_input(dy, tg, tl, wl)
+    torch.cuda.synchronize()
+    assert torch.equal(dx, dx2)
+    want = {"fwd": oracle.hier_forward(d["x64"], d["t64"], d["tl64"], wl),
+            "dx": oracle.hier_backward_input(d["dy64"], d["t64"], d["tl64"], wl)}
+    want["dtg"], want["dtl"] = oracle.hier_backward_tables(d["x64"], d["dy64"], wl)
+    got = {"fwd": to_f64(y), "dx": to_f64(dx), "dtg": to_f64(dtg), "dtl": to_f64(dtl)}
+    check(got, want, dtype, "hier %s %s" % (dtype, shape))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("wl", [2, 3])
+def test_hier_integer_data_bit_exact(wl, dtype):
+    """Small integers in both tables and the data: every sum is exact in fp32
+    and below 256 in magnitude, so the GPU must equal the oracle exactly."""
+    B, C, H, Wd = 3, 2, 5 * wl, 4 * wl + 1
+    r = np.random.default_rng(40 + wl)
+    d = {}
+    for k, shp in (("x", (B, C, H, Wd)), ("dy", (B, C, H, Wd)), ("t", (C, (4 * wl - 1) ** 2)),
+                   ("tl", (C, (2 * wl - 1) ** 2))):
+        d[k], d[k + "64"] = synth.round_to(r.integers(-1, 2, size=shp).astype(np.float64), dtype)
+    x, tg, tl, dy = (to_device(d[k], dtype) for k in ("x", "t", "tl", "dy"))
+    y = W.wbmm_hier_forward(x, tg, tl, wl)
+    dx, dtg, dtl = W.wbmm_hier_backward(x, dy, tg, tl, wl)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_f64(y), oracle.hier_forward(d["x64"], d["t64"], d["tl64"], wl))
+    assert np.array_equal(to_f64(dx), oracle.hier_backward_input(d["dy64"], d["t64"], d["tl64"], wl))
+    wg_, wl_ = oracle.hier_backward_tables(d["x64"], d["dy64"], wl)
+    assert np.array_equal(to_f64(dtg), wg_) and np.array_equal(to_f64(dtl), wl_)
+
+
+def test_hier_autograd_and_zero_tables():
+    d = draw_hier(2, 3, 14, 21, 7, "f32", seed=33)
+    x = to_device(d["x"], "f32").requires_grad_(True)
+    tg = to_device(d["t"], "f32").requires_grad_(True)
+    tl = to_device(d["tl"], "f32").requires_grad_(True)
+    dy = to_device(d["dy"], "f32")
+    y = W.wbmm_hier(x, tg, tl, 7)
+    y.backward(dy)
+    torch.cuda.synchronize()
+    want = {"fwd": oracle.hier_forward(d["x64"], d["t64"], d["tl64"], 7),
+            "dx": oracle.hier_backward_input(d["dy64"], d["t64"], d["tl64"], 7)}
+    want["dtg"], want["dtl"] = oracle.hier_backward_tables(d["x64"], d["dy64"], 7)
+    check({"fwd": to_f64(y), "dx": to_f64(x.grad), "dtg": to_f64(tg.grad), "dtl": to_f64(tl.grad)},
+          want, "f32", "hier autograd")
+    # zero tables: the two identity shortcuts alone, y = 2 x exactly
+    xb = to_device(d["x"], "f32")
+    z = W.wbmm_hier_forward(xb, torch.zeros_like(tg), torch.zeros_like(tl), 7)
+    torch.cuda.synchronize()
+    assert torch.equal(z, 2 * xb)
