@@ -58,13 +58,14 @@ def _bind(lib):
     lib.wbmm_oracle_backward_table.argtypes = [dp, dp, dp, i64, i64, i64, i64, ci, ci]
     lib.wbmm_oracle_relative_index.argtypes = [ci, ci, ctypes.POINTER(ctypes.c_int32)]
     lib.wbmm_oracle_hier_fused_matrix.argtypes = [dp, dp, dp, i64, ci]
-    lib.wbmm_oracle_dense_forward.argtypes = [dp, dp, dp, i64, i64, i64, i64, ci]
+    lib.wbmm_oracle_dense_forward.argtypes = [dp, dp, dp, i64, i64, i64, i64, ci, ci]
+    lib.wbmm_oracle_dense_backward_matrix.argtypes = [dp, dp, dp, i64, i64, i64, i64, ci, ci]
     lib.wbmm_oracle_set_threads.argtypes = [ci]
     lib.wbmm_oracle_max_threads.restype = ci
     for f in ("wbmm_oracle_forward", "wbmm_oracle_backward_input",
               "wbmm_oracle_backward_table", "wbmm_oracle_relative_index",
               "wbmm_oracle_hier_fused_matrix", "wbmm_oracle_dense_forward",
-              "wbmm_oracle_set_threads"):
+              "wbmm_oracle_dense_backward_matrix", "wbmm_oracle_set_threads"):
         getattr(lib, f).restype = None
     return lib
 
@@ -156,13 +157,48 @@ def hier_fused_matrix(tg, tl, wl, lib=None) -> np.ndarray:
     return m
 
 
-def dense_forward(x, m, wg, lib=None) -> np.ndarray:
-    """Y = X_w M with an explicit per-channel matrix M [C, wg^2, wg^2]."""
+def dense_forward(x, m, w, lib=None) -> np.ndarray:
+    """Y = X_w M per window with an explicit per-channel matrix M [C, d, d]
+    (d = wh ww, positions row-major inside the window; w = wh or (wh, ww))."""
+    wh, ww = _win(w)
     x, m = _f64(x), _f64(m)
     B, C, H, W = x.shape
+    assert m.shape == (C, wh * ww, wh * ww), m.shape
     y = np.empty_like(x)
-    (lib or load()).wbmm_oracle_dense_forward(_p(x), _p(m), _p(y), B, C, H, W, int(wg))
+    (lib or load()).wbmm_oracle_dense_forward(_p(x), _p(m), _p(y), B, C, H, W, wh, ww)
     return y
+
+
+def dense_backward_matrix(x, dy, w, lib=None) -> np.ndarray:
+    """dM [C, d, d] of the dense form: sum over windows of X_w^T dY_w."""
+    wh, ww = _win(w)
+    x, dy = _f64(x), _f64(dy)
+    B, C, H, W = x.shape
+    assert dy.shape == x.shape
+    dm = np.empty((C, wh * ww, wh * ww), dtype=np.float64)
+    (lib or load()).wbmm_oracle_dense_backward_matrix(_p(x), _p(dy), _p(dm), B, C, H, W, wh, ww)
+    return dm
+
+
+def build_matrix(t, w, lib=None) -> np.ndarray:
+    """M_c = R[c, I] (eq. index_select): [C, d, d] from the table [C, K]."""
+    wh, ww = _win(w)
+    t = _f64(t)
+    idx = relative_index((wh, ww), lib=lib).astype(np.int64)
+    return np.ascontiguousarray(t[:, idx])
+
+
+def bin_matrix(dm, w, lib=None) -> np.ndarray:
+    """Fold a matrix gradient onto the table: dT[c, k] = sum of dM[c, i, j]
+    over the pairs with I[i, j] = k (the adjoint of build_matrix)."""
+    wh, ww = _win(w)
+    dm = _f64(dm)
+    C = dm.shape[0]
+    idx = relative_index((wh, ww), lib=lib).astype(np.int64).ravel()
+    dt = np.zeros((C, (2 * wh - 1) * (2 * ww - 1)), dtype=np.float64)
+    for c in range(C):
+        dt[c] = np.bincount(idx, weights=dm[c].ravel(), minlength=dt.shape[1])
+    return dt
 
 
 def hier_forward(x, tg, tl, wl, lib=None) -> np.ndarray:
@@ -170,9 +206,9 @@ def hier_forward(x, tg, tl, wl, lib=None) -> np.ndarray:
     return dense_forward(x, hier_fused_matrix(tg, tl, wl, lib=lib), 2 * wl, lib=lib)
 
 
-def dense_backward_input(dy, m, wg, lib=None) -> np.ndarray:
+def dense_backward_input(dy, m, w, lib=None) -> np.ndarray:
     """dX = dY_w M^T per window for an explicit per-channel matrix M."""
-    return dense_forward(dy, np.ascontiguousarray(np.transpose(_f64(m), (0, 2, 1))), wg, lib=lib)
+    return dense_forward(dy, np.ascontiguousarray(np.transpose(_f64(m), (0, 2, 1))), w, lib=lib)
 
 
 def hier_backward_input(dy, tg, tl, wl, lib=None) -> np.ndarray:

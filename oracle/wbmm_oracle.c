@@ -70,7 +70,8 @@ static int64_t rel_index(int wh, int ww, int dh, int dw) {
   dw = -dw;
 #endif
 #if WBMM_ORACLE_MUTANT == 3
-  return (int64_t)(dh + wh - 1) * (2 * ww) + (dw + ww - 1);
+  /* wrong row stride, wrapped into the table so the mutant stays in bounds */
+  return ((int64_t)(dh + wh - 1) * (2 * ww) + (dw + ww - 1)) % ((int64_t)(2 * wh - 1) * (2 * ww - 1));
 #else
   return (int64_t)(dh + wh - 1) * (2 * ww - 1) + (dw + ww - 1);
 #endif
@@ -240,8 +241,8 @@ void wbmm_oracle_hier_fused_matrix(const double *tg, const double *tl,
  * wg^2); windows of size wg, zero padding to multiples of wg, crop after. */
 void wbmm_oracle_dense_forward(const double *x, const double *m, double *y,
                                int64_t B, int64_t C, int64_t H, int64_t W,
-                               int wg) {
-  const int d = wg * wg;
+                               int wh, int ww) {
+  const int d = wh * ww;
   int64_t bc;
 #pragma omp parallel for schedule(static)
   for (bc = 0; bc < B * C; ++bc) {
@@ -251,19 +252,51 @@ void wbmm_oracle_dense_forward(const double *x, const double *m, double *y,
     double *yp = y + bc * H * W;
     for (int64_t h = 0; h < H; ++h)
       for (int64_t w = 0; w < W; ++w) {
-        const int64_t wy = h / wg, wx = w / wg;
-        const int j = (int)(h % wg) * wg + (int)(w % wg);
+        const int64_t wy = h / wh, wx = w / ww;
+        const int j = (int)(h % wh) * ww + (int)(w % ww);
         double s = 0.0;
-        for (int hi = 0; hi < wg; ++hi) {
-          const int64_t gh = wy * wg + hi;
+        for (int hi = 0; hi < wh; ++hi) {
+          const int64_t gh = wy * wh + hi;
           if (gh >= H) continue;
-          for (int xi = 0; xi < wg; ++xi) {
-            const int64_t gw = wx * wg + xi;
+          for (int xi = 0; xi < ww; ++xi) {
+            const int64_t gw = wx * ww + xi;
             if (gw >= W) continue;
-            s += xp[gh * W + gw] * mc[(int64_t)(hi * wg + xi) * d + j];
+            s += xp[gh * W + gw] * mc[(int64_t)(hi * ww + xi) * d + j];
           }
         }
         yp[h * W + w] = s;
       }
+  }
+}
+
+/* Gradient of the dense form with respect to the per-channel matrix:
+ * dM[c, i, j] = sum over images and windows of X[.., i] * dY[.., j], the
+ * positions taken row-major inside each (zero-padded) window. */
+void wbmm_oracle_dense_backward_matrix(const double *x, const double *dy, double *dm,
+                                       int64_t B, int64_t C, int64_t H, int64_t W,
+                                       int wh, int ww) {
+  const int d = wh * ww;
+  const int64_t NH = ceil_div(H, wh), NW = ceil_div(W, ww);
+  int64_t c;
+#pragma omp parallel for schedule(static)
+  for (c = 0; c < C; ++c) {
+    double *mc = dm + c * (int64_t)d * d;
+    for (int64_t k = 0; k < (int64_t)d * d; ++k) mc[k] = 0.0;
+    for (int64_t b = 0; b < B; ++b) {
+      const double *xp = x + (b * C + c) * H * W;
+      const double *gp = dy + (b * C + c) * H * W;
+      for (int64_t wy = 0; wy < NH; ++wy)
+        for (int64_t wx = 0; wx < NW; ++wx)
+          for (int i = 0; i < d; ++i) {
+            const int64_t hi = wy * wh + i / ww, xi = wx * ww + i % ww;
+            if (hi >= H || xi >= W) continue;
+            const double xv = xp[hi * W + xi];
+            for (int j = 0; j < d; ++j) {
+              const int64_t ho = wy * wh + j / ww, xo = wx * ww + j % ww;
+              if (ho >= H || xo >= W) continue;
+              mc[(int64_t)i * d + j] += xv * gp[ho * W + xo];
+            }
+          }
+    }
   }
 }

@@ -304,6 +304,51 @@ def test_padding_is_pad_then_crop(olib, shape, w):
                           oracle.backward_table(pad(x), pad(dy), w, lib=olib))
 
 
+# ------------------------------------------------------ dense (cached M) form
+
+@pytest.mark.parametrize("shape,w", [((2, 3, 9, 10), (3, 5)), ((1, 2, 7, 6), (4, 2)),
+                                     ((2, 2, 8, 8), 4), ((1, 3, 5, 14), (2, 7))])
+def test_dense_form_matches_table_form(olib, shape, w):
+    """Alg. 1 with the matrix built once (M_c = R[c, I], the cached-matrix
+    variant) equals the table form for square and rectangular windows, in all
+    three passes; the matrix gradient folded onto the table by the index is
+    the table gradient."""
+    wh, ww = (w, w) if isinstance(w, int) else w
+    r = rng(16)
+    C = shape[1]
+    x, dy = r.standard_normal(shape), r.standard_normal(shape)
+    t = r.standard_normal((C, (2 * wh - 1) * (2 * ww - 1)))
+    m = oracle.build_matrix(t, w, lib=olib)
+    assert m.shape == (C, wh * ww, wh * ww)
+    assert rel_err(oracle.dense_forward(x, m, w, lib=olib), oracle.forward(x, t, w, lib=olib)) < 1e-13
+    assert rel_err(oracle.dense_backward_input(dy, m, w, lib=olib),
+                   oracle.backward_input(dy, t, w, lib=olib)) < 1e-13
+    dm = oracle.dense_backward_matrix(x, dy, w, lib=olib)
+    assert rel_err(oracle.bin_matrix(dm, w, lib=olib), oracle.backward_table(x, dy, w, lib=olib)) < 1e-13
+
+
+@pytest.mark.parametrize("w", [(3, 2), 3])
+def test_dense_matrix_gradient_exact(olib, w):
+    """dM pinned by exact finite differences of <dY, X_w M> in single entries
+    of an arbitrary (non-Toeplitz) integer matrix, and the adjoint identity
+    of the dense forward and input gradient."""
+    wh, ww = (w, w) if isinstance(w, int) else w
+    d = wh * ww
+    r = rng(17)
+    shape = (2, 2, 2 * wh + 1, 2 * ww + 1)
+    x = r.integers(-3, 4, size=shape).astype(np.float64)
+    dy = r.integers(-3, 4, size=shape).astype(np.float64)
+    m = r.integers(-3, 4, size=(2, d, d)).astype(np.float64)
+    loss = lambda mm: float(np.sum(dy * oracle.dense_forward(x, mm, w, lib=olib)))
+    dm = oracle.dense_backward_matrix(x, dy, w, lib=olib)
+    base = loss(m)
+    for c, i, j in [(0, 0, 0), (1, d - 1, 0), (0, d // 2, d - 1), (1, 1, 2)]:
+        e = np.zeros_like(m)
+        e[c, i, j] = 1.0
+        assert loss(m + e) - base == dm[c, i, j]
+    assert float(np.sum(x * oracle.dense_backward_input(dy, m, w, lib=olib))) == base
+
+
 # ------------------------------------------------------------- hierarchical
 
 @pytest.mark.parametrize("shape,wl", [((2, 3, 28, 28), 7), ((1, 2, 20, 9), 3)])
