@@ -171,6 +171,42 @@ wbmm_status wbmm_hier_backward(const void *x, const void *dy,
                                int64_t B, int64_t C, int64_t H, int64_t W,
                                int wl, wbmm_dtype dtype, void *stream);
 
+/* ---- Cached-matrix (dense) form, for any window w_h x w_w with
+ * 1 <= w_h, w_w <= 16 (Alg. 1 with the matrix built once, eq. index_select;
+ * the paper's cached variant).  Positions inside a window are row-major,
+ * p = h * w_w + x, d = w_h * w_w.  M is [C, d, d] in dtype, M[c][i][j] with
+ * i the input and j the output position; any matrix may be given (it need
+ * not come from a table), so rectangular windows, fused matrices and cached
+ * matrices share these calls.  Same tensor conventions as above. */
+
+/* m[c][i][j] = table[c][I(i, j)], table [C,(2 w_h - 1)(2 w_w - 1)] with
+ * I = (h_i - h_j + w_h - 1)(2 w_w - 1) + (x_i - x_j + w_w - 1). */
+wbmm_status wbmm_build_matrix(const void *table, void *m, int64_t C, int wh,
+                              int ww, wbmm_dtype dtype, void *stream);
+
+/* y_window = x_window * m[c] per w_h x w_w window. */
+wbmm_status wbmm_dense_forward(const void *x, const void *m, void *y,
+                               int64_t B, int64_t C, int64_t H, int64_t W,
+                               int wh, int ww, wbmm_dtype dtype, void *stream);
+
+/* dx_window = dy_window * m[c]^T. */
+wbmm_status wbmm_dense_backward_input(const void *dy, const void *m, void *dx,
+                                      int64_t B, int64_t C, int64_t H,
+                                      int64_t W, int wh, int ww,
+                                      wbmm_dtype dtype, void *stream);
+
+/* dm[c] = sum over images and windows of x_window^T dy_window: float32
+ * [C, d, d], overwritten. */
+wbmm_status wbmm_dense_backward_matrix(const void *x, const void *dy, float *dm,
+                                       int64_t B, int64_t C, int64_t H,
+                                       int64_t W, int wh, int ww,
+                                       wbmm_dtype dtype, void *stream);
+
+/* dtable[c][k] = sum of dm[c][i][j] over the pairs with I(i, j) = k (the
+ * adjoint of wbmm_build_matrix), in a fixed order; float32, overwritten. */
+wbmm_status wbmm_bin_matrix(const float *dm, float *dtable, int64_t C, int wh,
+                            int ww, void *stream);
+
 /* Static description of a status code (never NULL). */
 const char *wbmm_status_string(wbmm_status s);
 

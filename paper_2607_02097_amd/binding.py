@@ -9,8 +9,11 @@ Names follow the C entry points: ``wbmm_forward``, ``wbmm_backward_input``,
 ``wbmm_backward_table``, ``wbmm_backward_table_workspace_bytes``,
 ``wbmm_backward``, ``wbmm_backward_workspace_bytes``, the hierarchical form
 ``wbmm_hier_forward``, ``wbmm_hier_backward_input``, ``wbmm_hier_backward``,
-``wbmm_hier_backward_workspace_bytes``, and ``wbmm_relative_index``,
-``wbmm_status_string``.
+``wbmm_hier_backward_workspace_bytes``, the cached-matrix form
+``wbmm_build_matrix``, ``wbmm_dense_forward``, ``wbmm_dense_backward_input``,
+``wbmm_dense_backward_matrix``, ``wbmm_bin_matrix``, and
+``wbmm_relative_index``, ``wbmm_status_string``.  ``wbmm_rect_*`` compose the
+cached-matrix calls into WBMM for rectangular windows.
 """
 from __future__ import annotations
 
@@ -32,7 +35,9 @@ EXPORTED = ("wbmm_forward", "wbmm_backward_input", "wbmm_backward_table",
             "wbmm_backward_table_workspace_bytes", "wbmm_backward",
             "wbmm_backward_workspace_bytes", "wbmm_hier_forward",
             "wbmm_hier_backward_input", "wbmm_hier_backward",
-            "wbmm_hier_backward_workspace_bytes", "wbmm_status_string",
+            "wbmm_hier_backward_workspace_bytes", "wbmm_build_matrix",
+            "wbmm_dense_forward", "wbmm_dense_backward_input",
+            "wbmm_dense_backward_matrix", "wbmm_bin_matrix", "wbmm_status_string",
             "wbmm_relative_index", "wbmm_version")
 
 _lib = None
@@ -75,6 +80,17 @@ def load_library(path: str = LIB_PATH):
     lib.wbmm_hier_backward_workspace_bytes.restype = ctypes.c_size_t
     lib.wbmm_hier_backward.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t] + shape
     lib.wbmm_hier_backward.restype = st
+    dshape = [i64, i64, i64, i64, ci, ci, ci, vp]
+    lib.wbmm_build_matrix.argtypes = [vp, vp, i64, ci, ci, ci, vp]
+    lib.wbmm_build_matrix.restype = st
+    lib.wbmm_dense_forward.argtypes = [vp, vp, vp] + dshape
+    lib.wbmm_dense_forward.restype = st
+    lib.wbmm_dense_backward_input.argtypes = [vp, vp, vp] + dshape
+    lib.wbmm_dense_backward_input.restype = st
+    lib.wbmm_dense_backward_matrix.argtypes = [vp, vp, vp] + dshape
+    lib.wbmm_dense_backward_matrix.restype = st
+    lib.wbmm_bin_matrix.argtypes = [vp, vp, i64, ci, ci, vp]
+    lib.wbmm_bin_matrix.restype = st
     lib.wbmm_status_string.argtypes = [st]
     lib.wbmm_status_string.restype = ctypes.c_char_p
     lib.wbmm_relative_index.argtypes = [ci, ctypes.POINTER(ctypes.c_int32)]
@@ -317,6 +333,108 @@ def wbmm_hier_backward(x, dy, table_g, table_l, wl: int, workspace=None, stream=
     if st != WBMM_OK:
         raise WbmmError(st, "wbmm_hier_backward")
     return dx, dtg, dtl
+
+
+# ------------------------------------------------ cached-matrix (dense) form
+
+def _call(fn_name, dev, *args):
+    with torch.cuda.device(dev):
+        st = getattr(load_library(), fn_name)(*args)
+    if st != WBMM_OK:
+        raise WbmmError(st, fn_name)
+
+
+def wbmm_build_matrix(table, wh: int, ww: int, out=None, stream=None):
+    """M [C, d, d] (d = wh ww), M[c][i][j] = table[c][I(i, j)], in the
+    table's dtype."""
+    _check_tensor(table, "table")
+    C = table.shape[0]
+    d = int(wh) * int(ww)
+    if out is None:
+        out = torch.empty((C, d, d), dtype=table.dtype, device=table.device)
+    else:
+        _check_tensor(out, "out")
+        if out.numel() != C * d * d or out.dtype != table.dtype or out.device != table.device:
+            raise ValueError("out must be [C, d, d] in the table's dtype and device")
+    _call("wbmm_build_matrix", table.device, _ptr(table), _ptr(out), C, int(wh), int(ww), _code(table.dtype),
+          _stream(table, stream))
+    return out
+
+
+def _dense_like(fn_name, src, m, wh, ww, out, stream):
+    _check_tensor(src, "input")
+    _check_tensor(m, "m")
+    B, C, H, W = src.shape
+    d = int(wh) * int(ww)
+    if m.dtype != src.dtype or m.device != src.device or m.numel() != C * d * d:
+        raise ValueError("m must be [C, d, d] in the input's dtype and device")
+    if out is None:
+        out = torch.empty_like(src)
+    else:
+        _check_tensor(out, "out")
+        if out.shape != src.shape or out.dtype != src.dtype or out.device != src.device:
+            raise ValueError("out must match the input's shape, dtype and device")
+    _call(fn_name, src.device, _ptr(src), _ptr(m), _ptr(out), B, C, H, W, int(wh), int(ww), _code(src.dtype),
+          _stream(src, stream))
+    return out
+
+
+def wbmm_dense_forward(x, m, wh: int, ww: int, out=None, stream=None):
+    """y_window = x_window m[c] per wh x ww window."""
+    return _dense_like("wbmm_dense_forward", x, m, wh, ww, out, stream)
+
+
+def wbmm_dense_backward_input(dy, m, wh: int, ww: int, out=None, stream=None):
+    """dx_window = dy_window m[c]^T."""
+    return _dense_like("wbmm_dense_backward_input", dy, m, wh, ww, out, stream)
+
+
+def wbmm_dense_backward_matrix(x, dy, wh: int, ww: int, out=None, stream=None):
+    """dm [C, d, d] float32: sum over windows of x_window^T dy_window."""
+    _check_tensor(x, "x")
+    _check_tensor(dy, "dy")
+    if dy.shape != x.shape or dy.dtype != x.dtype or dy.device != x.device:
+        raise ValueError("dy must match x's shape, dtype and device")
+    B, C, H, W = x.shape
+    d = int(wh) * int(ww)
+    if out is None:
+        out = torch.empty((C, d, d), dtype=torch.float32, device=x.device)
+    _call("wbmm_dense_backward_matrix", x.device, _ptr(x), _ptr(dy), _ptr(out), B, C, H, W, int(wh), int(ww),
+          _code(x.dtype), _stream(x, stream))
+    return out
+
+
+def wbmm_bin_matrix(dm, wh: int, ww: int, out=None, stream=None):
+    """dtable [C, (2wh-1)(2ww-1)] float32 from a float32 matrix gradient."""
+    _check_tensor(dm, "dm")
+    if dm.dtype != torch.float32:
+        raise TypeError("dm must be float32")
+    C = dm.shape[0]
+    k = (2 * int(wh) - 1) * (2 * int(ww) - 1)
+    if out is None:
+        out = torch.empty((C, k), dtype=torch.float32, device=dm.device)
+    _call("wbmm_bin_matrix", dm.device, _ptr(dm), _ptr(out), C, int(wh), int(ww), _stream(dm, stream))
+    return out
+
+
+def wbmm_rect_forward(x, table, wh: int, ww: int, m=None, stream=None):
+    """WBMM with wh x ww windows (table [C,(2wh-1)(2ww-1)]): the matrix is
+    built (or ``m`` reused) and applied per window."""
+    if m is None:
+        m = wbmm_build_matrix(table, wh, ww, stream=stream)
+    return wbmm_dense_forward(x, m, wh, ww, stream=stream)
+
+
+def wbmm_rect_backward_input(dy, table, wh: int, ww: int, m=None, stream=None):
+    if m is None:
+        m = wbmm_build_matrix(table, wh, ww, stream=stream)
+    return wbmm_dense_backward_input(dy, m, wh, ww, stream=stream)
+
+
+def wbmm_rect_backward_table(x, dy, wh: int, ww: int, stream=None):
+    """Table gradient with wh x ww windows (float32): the matrix gradient
+    folded onto the table."""
+    return wbmm_bin_matrix(wbmm_dense_backward_matrix(x, dy, wh, ww, stream=stream), wh, ww, stream=stream)
 
 
 def wbmm_relative_index(w: int) -> torch.Tensor:

@@ -28,7 +28,7 @@ HIP_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++20", "-fPIC",
 # (dtype, window range) so the translation units compile in parallel.
 UNITS = [("wbmm_inst.hip", ["-DWBMM_INST_TAG=%s" % tag, "-DWBMM_INST_LO=%d" % lo])
          for tag in ("TagBF16", "TagF32", "TagF16") for lo in (9, 1)]
-UNITS += [("wbmm_dispatch.cpp", []), ("wbmm_api.cpp", [])]
+UNITS += [("wbmm_dense.hip", []), ("wbmm_dispatch.cpp", []), ("wbmm_api.cpp", [])]
 
 
 def hipcc() -> str:

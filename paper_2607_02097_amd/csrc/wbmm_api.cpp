@@ -242,6 +242,97 @@ wbmm_status wbmm_hier_backward(const void *x, const void *dy, const void *table_
   return from_hip(e);
 }
 
+// ---- cached-matrix (dense) form: any w_h x w_w window, d = w_h w_w <= 256
+
+static wbmm_status dense_window(int wh, int ww) {
+  if (wh <= 0 || ww <= 0) return WBMM_ERR_INVALID_ARG;
+  if (wh > wbmm::kMaxWindow || ww > wbmm::kMaxWindow) return WBMM_ERR_UNSUPPORTED;
+  return WBMM_OK;
+}
+
+// Shape check of a [B,C,H,W] tensor with w_h x w_w windows (Geom.w unused).
+static wbmm_status dense_shape(int64_t B, int64_t C, int64_t H, int64_t W, int wh, int ww, wbmm_dtype dtype,
+                               Geom *g, int64_t *bytes) {
+  wbmm_status s = dense_window(wh, ww);
+  if (s != WBMM_OK) return s;
+  // the square check with the larger side validates sizes and products;
+  // the window counts are then recomputed for w_h x w_w
+  s = check_shape(B, C, H, W, wh > ww ? wh : ww, dtype, g, bytes);
+  if (s != WBMM_OK) return s;
+  g->NH = (H + wh - 1) / wh;
+  g->NW = (W + ww - 1) / ww;
+  int64_t n;
+  if (!mul_ok(B, g->NH * g->NW, &n)) return WBMM_ERR_INVALID_ARG;
+  g->N = n;
+  if (n >= (int64_t)1 << 31 || C * n > (int64_t)UINT32_MAX) return WBMM_ERR_UNSUPPORTED;
+  return WBMM_OK;
+}
+
+wbmm_status wbmm_build_matrix(const void *table, void *m, int64_t C, int wh, int ww, wbmm_dtype dtype,
+                              void *stream) {
+  if (!valid_dtype((int)dtype)) return WBMM_ERR_UNSUPPORTED;
+  wbmm_status s = dense_window(wh, ww);
+  if (s != WBMM_OK) return s;
+  if (!table || !m || C <= 0) return WBMM_ERR_INVALID_ARG;
+  const size_t es = elem_size(dtype);
+  const int64_t d = (int64_t)wh * ww, k2 = (int64_t)(2 * wh - 1) * (2 * ww - 1);
+  int64_t mbytes;
+  if (!mul_ok(C, d * d * (int64_t)es, &mbytes)) return WBMM_ERR_INVALID_ARG;
+  if (!aligned(table, es) || !aligned(m, es)) return WBMM_ERR_INVALID_ARG;
+  if (overlap(table, C * k2 * (int64_t)es, m, mbytes)) return WBMM_ERR_INVALID_ARG;
+  return from_hip(wbmm::launch_dense_build((Dt)dtype, table, m, C, wh, ww, (hipStream_t)stream));
+}
+
+static wbmm_status dense_forward_like(const void *in, const void *m, void *out, int64_t B, int64_t C, int64_t H,
+                                      int64_t W, int wh, int ww, wbmm_dtype dtype, void *stream, bool trans) {
+  Geom g;
+  int64_t bytes = 0;
+  wbmm_status s = dense_shape(B, C, H, W, wh, ww, dtype, &g, &bytes);
+  if (s != WBMM_OK) return s;
+  if (!in || !m || !out) return WBMM_ERR_INVALID_ARG;
+  const size_t es = elem_size(dtype);
+  if (!aligned(in, es) || !aligned(m, es) || !aligned(out, es)) return WBMM_ERR_INVALID_ARG;
+  const int64_t d = (int64_t)wh * ww;
+  if (overlap(in, bytes, out, bytes) || overlap(m, C * d * d * (int64_t)es, out, bytes)) return WBMM_ERR_INVALID_ARG;
+  return from_hip(wbmm::launch_dense_forward((Dt)dtype, in, m, out, g, wh, ww, trans, (hipStream_t)stream));
+}
+
+wbmm_status wbmm_dense_forward(const void *x, const void *m, void *y, int64_t B, int64_t C, int64_t H, int64_t W,
+                               int wh, int ww, wbmm_dtype dtype, void *stream) {
+  return dense_forward_like(x, m, y, B, C, H, W, wh, ww, dtype, stream, false);
+}
+
+wbmm_status wbmm_dense_backward_input(const void *dy, const void *m, void *dx, int64_t B, int64_t C, int64_t H,
+                                      int64_t W, int wh, int ww, wbmm_dtype dtype, void *stream) {
+  return dense_forward_like(dy, m, dx, B, C, H, W, wh, ww, dtype, stream, true);
+}
+
+wbmm_status wbmm_dense_backward_matrix(const void *x, const void *dy, float *dm, int64_t B, int64_t C, int64_t H,
+                                       int64_t W, int wh, int ww, wbmm_dtype dtype, void *stream) {
+  Geom g;
+  int64_t bytes = 0;
+  wbmm_status s = dense_shape(B, C, H, W, wh, ww, dtype, &g, &bytes);
+  if (s != WBMM_OK) return s;
+  if (!x || !dy || !dm) return WBMM_ERR_INVALID_ARG;
+  const size_t es = elem_size(dtype);
+  if (!aligned(x, es) || !aligned(dy, es) || !aligned(dm, 4)) return WBMM_ERR_INVALID_ARG;
+  const int64_t d = (int64_t)wh * ww;
+  if (overlap(dm, C * d * d * 4, x, bytes) || overlap(dm, C * d * d * 4, dy, bytes)) return WBMM_ERR_INVALID_ARG;
+  return from_hip(wbmm::launch_dense_backward_matrix((Dt)dtype, x, dy, dm, g, wh, ww, (hipStream_t)stream));
+}
+
+wbmm_status wbmm_bin_matrix(const float *dm, float *dtable, int64_t C, int wh, int ww, void *stream) {
+  wbmm_status s = dense_window(wh, ww);
+  if (s != WBMM_OK) return s;
+  if (!dm || !dtable || C <= 0) return WBMM_ERR_INVALID_ARG;
+  if (!aligned(dm, 4) || !aligned(dtable, 4)) return WBMM_ERR_INVALID_ARG;
+  const int64_t d = (int64_t)wh * ww, k2 = (int64_t)(2 * wh - 1) * (2 * ww - 1);
+  int64_t mb;
+  if (!mul_ok(C, d * d * 4, &mb) || C * k2 > (int64_t)UINT32_MAX * 256) return WBMM_ERR_INVALID_ARG;
+  if (overlap(dm, mb, dtable, C * k2 * 4)) return WBMM_ERR_INVALID_ARG;
+  return from_hip(wbmm::launch_dense_bin(dm, dtable, C, wh, ww, (hipStream_t)stream));
+}
+
 const char *wbmm_status_string(wbmm_status s) {
   switch (s) {
     case WBMM_OK: return "WBMM_OK";

@@ -47,6 +47,17 @@ hipError_t launch_hier_forward(Dt dt, const void *x, const void *table_g,
                                const void *table_l, void *y, const Geom &g,
                                bool reverse_tables, hipStream_t stream);
 
+// Cached-matrix (dense) form, any w_h x w_w window with d = w_h w_w <= 256
+// (wbmm_dense.hip).  g.w is unused by these.
+hipError_t launch_dense_build(Dt dt, const void *table, void *m, int64_t C, int wh, int ww,
+                              hipStream_t stream);
+hipError_t launch_dense_forward(Dt dt, const void *x, const void *m, void *y, const Geom &g,
+                                int wh, int ww, bool transpose, hipStream_t stream);
+hipError_t launch_dense_backward_matrix(Dt dt, const void *x, const void *dy, float *dm,
+                                        const Geom &g, int wh, int ww, hipStream_t stream);
+hipError_t launch_dense_bin(const float *dm, float *dtable, int64_t C, int wh, int ww,
+                            hipStream_t stream);
+
 // Per-(dtype, window) entry points, defined by the wbmm_inst.hip
 // translation units and collected into tables by wbmm_dispatch.cpp.
 typedef hipError_t (*FwdFn)(const void *, const void *, void *, const Geom &, bool, hipStream_t);

@@ -171,3 +171,30 @@ def test_hier_rejects_bad_arguments(lib):
                dx=FAKE * 192, dtg=FAKE * 256, dtl=FAKE * 260)
     assert bwd_call(**big) == E                                  # no workspace
     assert bwd_call(ws=FAKE * 320, wsb=need - 4, **big) == E     # too small
+
+
+def test_dense_rejects_bad_arguments(lib):
+    E, U = W.WBMM_ERR_INVALID_ARG, W.WBMM_ERR_UNSUPPORTED
+    vp = ctypes.c_void_p
+    assert lib.wbmm_build_matrix(vp(0), vp(FAKE), 2, 3, 5, 1, None) == E
+    assert lib.wbmm_build_matrix(vp(FAKE), vp(0), 2, 3, 5, 1, None) == E
+    assert lib.wbmm_build_matrix(vp(FAKE), vp(FAKE), 2, 3, 5, 1, None) == E   # m overlaps the table
+    assert lib.wbmm_build_matrix(vp(FAKE), vp(FAKE * 8), 2, 17, 5, 1, None) == U
+    assert lib.wbmm_build_matrix(vp(FAKE), vp(FAKE * 8), 2, 0, 5, 1, None) == E
+    assert lib.wbmm_build_matrix(vp(FAKE), vp(FAKE * 8), 2, 3, 5, 9, None) == U
+
+    def dcall(fn, a=FAKE, m=FAKE * 8, out=FAKE * 16, B=1, C=2, H=9, Wd=10, wh=3, ww=5, d=1):
+        return getattr(lib, fn)(vp(a), vp(m), vp(out), B, C, H, Wd, wh, ww, d, None)
+
+    for fn in ("wbmm_dense_forward", "wbmm_dense_backward_input", "wbmm_dense_backward_matrix"):
+        assert dcall(fn, a=0) == E, fn
+        assert dcall(fn, m=0) == E, fn
+        assert dcall(fn, out=0) == E, fn
+        assert dcall(fn, ww=17) == U, fn
+        assert dcall(fn, B=0) == E, fn
+    assert dcall("wbmm_dense_forward", out=FAKE) == E          # output aliases input
+    assert dcall("wbmm_dense_forward", out=FAKE * 8 + 64) == E # output overlaps the matrix
+    assert dcall("wbmm_dense_backward_matrix", out=FAKE + 8) == E  # dm overlaps x
+    assert lib.wbmm_bin_matrix(vp(FAKE), vp(FAKE + 64), 2, 3, 5, None) == E   # overlap
+    assert lib.wbmm_bin_matrix(vp(0), vp(FAKE * 8), 2, 3, 5, None) == E
+    assert lib.wbmm_bin_matrix(vp(FAKE), vp(FAKE * 8), 2, 3, 0, None) == E

@@ -448,3 +448,64 @@ def test_hier_autograd_and_zero_tables():
     z = W.wbmm_hier_forward(xb, torch.zeros_like(tg), torch.zeros_like(tl), 7)
     torch.cuda.synchronize()
     assert torch.equal(z, 2 * xb)
+
+
+# ------------------------------------------------ cached-matrix (dense) form
+
+DENSE = [
+    # (B, C, H, W, wh, ww): rectangular and square windows, ragged maps
+    (2, 3, 9, 10, 3, 5),
+    (1, 2, 14, 21, 7, 7),
+    (2, 2, 28, 28, 14, 14),
+    (1, 2, 20, 17, 16, 8),
+    (3, 2, 5, 9, 2, 3),
+    (2, 1, 16, 32, 16, 16),
+    (1, 3, 7, 7, 1, 7),
+]
+
+
+def dense_draw(B, C, H, Wd, wh, ww, dtype, seed):
+    r = np.random.default_rng(seed)
+    d = {}
+    for k, shp, sd in (("x", (B, C, H, Wd), 1.0), ("dy", (B, C, H, Wd), 1.0),
+                       ("t", (C, (2 * wh - 1) * (2 * ww - 1)), 0.02),
+                       ("m", (C, wh * ww, wh * ww), 0.05)):
+        d[k], d[k + "64"] = synth.round_to(sd * r.standard_normal(shp), dtype)
+    return d
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("shape", DENSE, ids=lambda s: "B%dC%dH%dW%dw%dx%d" % s)
+def test_dense_form_parity(shape, dtype):
+    """An arbitrary (non-Toeplitz) per-channel matrix: forward, input gradient
+    and matrix gradient against the oracle; the matrix built from a table is
+    the table gathered bit for bit, and the rectangular-window WBMM composed
+    from it matches the oracle's table form in all three passes."""
+    B, C, H, Wd, wh, ww = shape
+    d = dense_draw(B, C, H, Wd, wh, ww, dtype, seed=51)
+    x, dy, t, m = (to_device(d[k], dtype) for k in ("x", "dy", "t", "m"))
+    got = {"fwd": W.wbmm_dense_forward(x, m, wh, ww), "dx": W.wbmm_dense_backward_input(dy, m, wh, ww),
+           "dm": W.wbmm_dense_backward_matrix(x, dy, wh, ww)}
+    mb = W.wbmm_build_matrix(t, wh, ww)
+    rect = {"fwd": W.wbmm_rect_forward(x, t, wh, ww), "dx": W.wbmm_rect_backward_input(dy, t, wh, ww),
+            "dt": W.wbmm_rect_backward_table(x, dy, wh, ww)}
+    torch.cuda.synchronize()
+    want = {"fwd": oracle.dense_forward(d["x64"], d["m64"], (wh, ww)),
+            "dx": oracle.dense_backward_input(d["dy64"], d["m64"], (wh, ww)),
+            "dm": oracle.dense_backward_matrix(d["x64"], d["dy64"], (wh, ww))}
+    check({k: to_f64(v) for k, v in got.items()}, want, dtype, "dense %s %s" % (dtype, shape))
+    assert np.array_equal(to_f64(mb), oracle.build_matrix(d["t64"], (wh, ww)))
+    want_r = {"fwd": oracle.forward(d["x64"], d["t64"], (wh, ww)),
+              "dx": oracle.backward_input(d["dy64"], d["t64"], (wh, ww)),
+              "dt": oracle.backward_table(d["x64"], d["dy64"], (wh, ww))}
+    check({k: to_f64(v) for k, v in rect.items()}, want_r, dtype, "rect %s %s" % (dtype, shape))
+
+
+def test_dense_bin_matrix_exact():
+    """Folding an integer-valued matrix onto the table: exact sums."""
+    r = np.random.default_rng(52)
+    for wh, ww in ((3, 5), (7, 7), (16, 2)):
+        dm64 = r.integers(-4, 5, size=(3, wh * ww, wh * ww)).astype(np.float64)
+        got = W.wbmm_bin_matrix(torch.from_numpy(dm64.astype(np.float32)).cuda(), wh, ww)
+        torch.cuda.synchronize()
+        assert np.array_equal(to_f64(got), oracle.bin_matrix(dm64, (wh, ww)))
