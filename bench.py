@@ -56,11 +56,11 @@ def parse():
 # on (sha256 of the kernel header); otherwise reported as null.
 TRAFFIC = {
     # (workload, kernel): measured bytes per dispatch (profiles/wbmm_traffic_*.txt)
-    ("bf16_b64_c192_28_w14", "bwd"): {"source": "049fd9639fe78f01", "bytes": 68180689},
-    ("bf16_b64_c192_28_w14", "fwd"): {"source": "049fd9639fe78f01", "bytes": 41098384},
-    ("bf16_b64_c192_28_w14", "dx"): {"source": "049fd9639fe78f01", "bytes": 41108509},
-    ("bf16_b64_c192_28_w14", "dt"): {"source": "049fd9639fe78f01", "bytes": 47624850},
-    ("bf16_b64_c96_56_w7", "fwd"): {"source": "049fd9639fe78f01", "bytes": 77438873},
+    ("bf16_b64_c192_28_w14", "bwd"): {"source": "ce1220a554221643", "bytes": 68084142},
+    ("bf16_b64_c192_28_w14", "fwd"): {"source": "ce1220a554221643", "bytes": 41074912},
+    ("bf16_b64_c192_28_w14", "dx"): {"source": "ce1220a554221643", "bytes": 41099426},
+    ("bf16_b64_c192_28_w14", "dt"): {"source": "ce1220a554221643", "bytes": 47518944},
+    ("bf16_b64_c96_56_w7", "fwd"): {"source": "ce1220a554221643", "bytes": 77428010},
 }
 
 

@@ -537,6 +537,7 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
   typedef FwdCfg<Tag, WIN> G;
   constexpr int RP = G::RP, LDSW = G::LDSW, K1 = G::K1;
   static_assert(!HIER || WIN % 2 == 0, "the hierarchical form needs an even window");
+  static_assert(LDSW % 4 == 0, "8- and 16-byte result writes");
 
   extern __shared__ __align__(16) unsigned char smem[];
   S *Ts = reinterpret_cast<S *>(smem + kFwdWaves * 16 * LDSW * Tag::ES);
@@ -579,7 +580,11 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
 #pragma unroll
       for (int s = 0; s < S_; ++s)
         af[s] = *reinterpret_cast<const Frag *>(&rowp[ln * LDSW + s * 32 + 8 * g]);
-      S *outp = rowp + (4 * g) * LDSW + ln;
+      // The products are taken as (M^T X^T): the table fragment is the A
+      // operand and the window-major fragment the B operand (the same
+      // registers serve both roles), so a lane's four results are four
+      // consecutive positions of one window and go to LDS as one 8-byte write.
+      S *outq = rowp + ln * LDSW + 4 * g;
       // Output tiles t and t+1 use the even and the odd fragments: two
       // independent accumulation chains.  Walking t upwards, fragment q is
       // first needed at t = max(0, NT-1-q) (same parity) and last at
@@ -597,13 +602,13 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
         f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int s = 0; s < S_; ++s) {
-          acc0 = mma<Tag>(af[s], bf[2 * s - t0 + NT - 1], acc0);
-          if (t0 + 1 < NT) acc1 = mma<Tag>(af[s], bf[2 * s - t0 - 1 + NT - 1], acc1);
+          acc0 = mma<Tag>(bf[2 * s - t0 + NT - 1], af[s], acc0);
+          if (t0 + 1 < NT) acc1 = mma<Tag>(bf[2 * s - t0 - 1 + NT - 1], af[s], acc1);
           if constexpr (HIER) {
             // local sub-window blocks
-            if (fwd_rows_meet<Tag, WIN>(s, t0, true)) acc0 = mma<Tag>(af[s], fwd_lfrag<Tag, WIN>(TBL, s, t0, g, ln), acc0);
+            if (fwd_rows_meet<Tag, WIN>(s, t0, true)) acc0 = mma<Tag>(fwd_lfrag<Tag, WIN>(TBL, s, t0, g, ln), af[s], acc0);
             if (t0 + 1 < NT && fwd_rows_meet<Tag, WIN>(s, t0 + 1, true))
-              acc1 = mma<Tag>(af[s], fwd_lfrag<Tag, WIN>(TBL, s, t0 + 1, g, ln), acc1);
+              acc1 = mma<Tag>(fwd_lfrag<Tag, WIN>(TBL, s, t0 + 1, g, ln), af[s], acc1);
           }
         }
 #pragma unroll
@@ -611,18 +616,17 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
           const int t = t0 + h;
           if (t >= NT) continue;
           f32x4 acc = h ? acc1 : acc0;
+          uint2 *o2 = reinterpret_cast<uint2 *>(outq + 16 * t);
           if constexpr (HIER) {
             // the two identity shortcuts: + 2 x at the output's own position,
             // read before the result overwrites it (pads hold zero)
-#pragma unroll
-            for (int rr = 0; rr < 4; ++rr) acc[rr] += 2.f * to_f32<Tag>(outp[rr * LDSW + 16 * t]);
+            const uint2 xv = *o2;
+            acc[0] += 2.f * to_f32<Tag>((u16)(xv.x & 0xffffu));
+            acc[1] += 2.f * to_f32<Tag>((u16)(xv.x >> 16));
+            acc[2] += 2.f * to_f32<Tag>((u16)(xv.y & 0xffffu));
+            acc[3] += 2.f * to_f32<Tag>((u16)(xv.y >> 16));
           }
-          const uint32_t lo = pack2<Tag>(acc[0], acc[1]);
-          const uint32_t hi = pack2<Tag>(acc[2], acc[3]);
-          outp[0 * LDSW + 16 * t] = (u16)(lo & 0xffffu);
-          outp[1 * LDSW + 16 * t] = (u16)(lo >> 16);
-          outp[2 * LDSW + 16 * t] = (u16)(hi & 0xffffu);
-          outp[3 * LDSW + 16 * t] = (u16)(hi >> 16);
+          *o2 = uint2{pack2<Tag>(acc[0], acc[1]), pack2<Tag>(acc[2], acc[3])};
         }
         // small windows: the window rows of output tiles t0 and t0+1 are
         // final; storing them now overlaps the stores with the products of
@@ -660,7 +664,8 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
       float af[S_];
 #pragma unroll
       for (int s = 0; s < S_; ++s) af[s] = rowp[ln * LDSW + 4 * s + g];
-      S *outp = rowp + (4 * g) * LDSW + ln;
+      // (M^T X^T) as in the 16-bit path: four consecutive positions per lane
+      float4 *outq = reinterpret_cast<float4 *>(rowp + ln * LDSW + 4 * g);
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -681,10 +686,9 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
               bv += Tsl[(dh + WL - 1) * K1L + xi - xo + WL - 1];
             if (hi == ho && xi == xo && xi < WIN && hi < WIN) bv += 2.f;
           }
-          acc = mma<Tag>(af[s], bv, acc);
+          acc = mma<Tag>(bv, af[s], acc);
         }
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) outp[rr * LDSW + 16 * t] = acc[rr];
+        outq[4 * t] = float4{acc[0], acc[1], acc[2], acc[3]};
       }
       store_sub<Tag, WIN>(a, y, c, m0, mw, lane, buf);
     }
@@ -1140,35 +1144,72 @@ __device__ __attribute__((always_inline)) inline void dt_finish(const f32x4 (&ac
   constexpr int NPM = max_tiles_per_wave<NPT>();
   float *scr = reinterpret_cast<float *>(smem) + WAVE * NPM * 272;
   float *binsum = reinterpret_cast<float *>(smem) + kWaves * NPM * 272;
+  if constexpr (R == 1) {
+    // One window row per tile (RP = 16): a bin is one diagonal dw = xi - xo
+    // of the 16 x 16 tile.  The tile is written skewed, element (xi, xo) at
+    // column (xo - xi) mod 16 of row xi, so that column s holds diagonal -s
+    // in rows 0 .. 15-s and diagonal 16-s in the rows below; a lane sums one
+    // column of one tile, top to bottom (the order of the general path).
+    // Pad positions (xi or xo >= WIN) are written as zero.
 #pragma unroll
-  for (int j = 0; j < NP; ++j) {
+    for (int rr = 0; rr < 4; ++rr) {
+      const int xi = 4 * g + rr;
+      float *row = scr + xi * 16 + ((ln - xi) & 15);
+      const bool ok = xi < WIN && ln < WIN;
 #pragma unroll
-    for (int rr = 0; rr < 4; ++rr) scr[j * 272 + (4 * g + rr) * 17 + ln] = acc[j][rr];
-  }
-  wave_lds_sync();
+      for (int j = 0; j < NP; ++j) row[j * 272] = ok ? acc[j][rr] : 0.f;
+    }
+    wave_lds_sync();
+    const int s = lane & 15;
 #pragma unroll
-  for (int it = 0; it < cdiv(NP * NBT, 64); ++it) {
-    const int b2 = lane + 64 * it;
-    if (b2 < NP * NBT) {
-      const int j = b2 / NBT;
-      const int bin = b2 - j * NBT;
-      const int da = bin / K1 - (R - 1);  // input sub-row minus output sub-row
-      const int dw = bin - (bin / K1) * K1 - (WIN - 1);
-      const float *t = scr + j * 272;
-      float sum = 0.f;
+    for (int it = 0; it < cdiv(NP * 16, 64); ++it) {
+      const int j = (lane >> 4) + 4 * it;
+      if (j < NP) {
+        const float *col = scr + j * 272 + s;
+        float lo = 0.f, hi = 0.f;
 #pragma unroll
-      for (int ra = 0; ra < R; ++ra) {
-        const int rb = ra - da;
-        const bool rok = rb >= 0 && rb < R;
-#pragma unroll
-        for (int xo = 0; xo < WIN; ++xo) {
-          const int xi = xo + dw;
-          const bool ok = rok && xi >= 0 && xi < WIN;
-          const float v = t[ok ? (ra * RP + xi) * 17 + rb * RP + xo : 0];
-          sum += ok ? v : 0.f;
+        for (int xi = 0; xi < 16; ++xi) {
+          const float v = col[xi * 16];
+          const bool upper = xi + s <= 15;
+          lo += upper ? v : 0.f;
+          hi += upper ? 0.f : v;
         }
+        float *bp = binsum + (PLO + j + NPT - 1) * NBT + WIN - 1;
+        if (s <= WIN - 1) bp[-s] = lo;
+        if (s >= 1 && 16 - s <= WIN - 1) bp[16 - s] = hi;
       }
-      binsum[(PLO + j + NPT - 1) * NBT + bin] = sum;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < NP; ++j) {
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) scr[j * 272 + (4 * g + rr) * 17 + ln] = acc[j][rr];
+    }
+    wave_lds_sync();
+#pragma unroll
+    for (int it = 0; it < cdiv(NP * NBT, 64); ++it) {
+      const int b2 = lane + 64 * it;
+      if (b2 < NP * NBT) {
+        const int j = b2 / NBT;
+        const int bin = b2 - j * NBT;
+        const int da = bin / K1 - (R - 1);  // input sub-row minus output sub-row
+        const int dw = bin - (bin / K1) * K1 - (WIN - 1);
+        const float *t = scr + j * 272;
+        float sum = 0.f;
+#pragma unroll
+        for (int ra = 0; ra < R; ++ra) {
+          const int rb = ra - da;
+          const bool rok = rb >= 0 && rb < R;
+#pragma unroll
+          for (int xo = 0; xo < WIN; ++xo) {
+            const int xi = xo + dw;
+            const bool ok = rok && xi >= 0 && xi < WIN;
+            const float v = t[ok ? (ra * RP + xi) * 17 + rb * RP + xo : 0];
+            sum += ok ? v : 0.f;
+          }
+        }
+        binsum[(PLO + j + NPT - 1) * NBT + bin] = sum;
+      }
     }
   }
   __syncthreads();
