@@ -64,6 +64,24 @@ TRAFFIC = {
 }
 
 
+def image_layout(wl):
+    """Whether the library runs this workload's 16-bit forward (and input
+    gradient) with the image-layout kernel (freshly allocated tensors are
+    16-byte aligned): windows tile the map, NW is a power of two up to 16, a
+    16-window sub-tile is whole bands of one image or whole images."""
+    if wl.dtype not in ("bf16", "f16") or wl.H % wl.w or wl.W % wl.w:
+        return False
+    nh, nw = wl.H // wl.w, wl.W // wl.w
+    if nw > 16 or nw & (nw - 1):
+        return False
+    wpi = nh * nw
+    if wpi % 16 == 0:
+        return (wl.w * wl.W) % 8 == 0
+    if 16 % wpi == 0:
+        return (wl.H * wl.W) % 8 == 0 and 2 * (16 // wpi) * wl.C * wl.H * wl.W < 2 ** 31
+    return False
+
+
 def kernel_source_hash():
     import hashlib
     path = os.path.join(ROOT, "paper_2607_02097_amd", "csrc", "wbmm_kernels.h")
@@ -294,7 +312,8 @@ def main():
     dom_flops = pass_flops(wl, dom)
     ai = dom_flops / dom_bytes
     ridge = peak * 1e12 / (HBM_PEAK_GBS * 1e9)
-    kernel_name = {"fwd": "wbmm_fwd_kernel<%s,%d,false>", "dx": "wbmm_fwd_kernel<%s,%d,true>",
+    fk = "wbmm_fwd_img_kernel" if image_layout(wl) else "wbmm_fwd_kernel"
+    kernel_name = {"fwd": fk + "<%s,%d,false>", "dx": fk + "<%s,%d,true>",
                    "dt": "wbmm_dt_kernel<%s,%d>", "bwd": "wbmm_bwd_kernel<%s,%d>",
                    "hfwd": "wbmm_fwd_kernel<%s,%d,false,true>",
                    "hbwd": "wbmm_hier_backward (3 launches) <%s,%d>"}[dom] % ({"bf16": "TagBF16", "f16": "TagF16",

@@ -695,176 +695,241 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
   }
 }
 
-// ------------------------------------------------ forward, band layout
-// Small 16-bit windows (w <= 8) on maps whose windows tile the image, whose
-// windows per band (NW) divide 16 and whose image rows start 16-byte
-// aligned: a sub-tile of 16 consecutive windows is then 16 / NW whole bands,
-// each band w image rows that are contiguous in memory.  The band moves with
-// 16-byte loads and stores at consecutive addresses (a window row of w < 8
-// elements would otherwise take several narrow accesses) and keeps its image
-// layout in LDS; the matrix-core A operands are gathered from it element by
-// element, and the rounded results are written back into it.  The rows of
-// each finished output-tile pair are stored while the next pair is
-// multiplied.
+// ------------------------------------------------ forward, image layout
+// 16-bit windows on maps that the windows tile, with NW (windows per band
+// row) a power of two and a 16-window sub-tile that is either a run of whole
+// bands inside one image (NH * NW a multiple of 16) or a run of whole images
+// (NH * NW divides 16).  A band is w contiguous image rows and the bands of
+// one image are contiguous, so a sub-tile is at most a few contiguous pieces
+// of memory: it moves with 16-byte loads and stores at consecutive addresses,
+// keeps its image layout in LDS, and the per-lane addressing is fixed for the
+// whole launch.  The products are those of the row kernel (same fragments,
+// same order); A operands are read as dwords and realigned by 16 bits where a
+// window row starts at an odd element, and results are written back into the
+// image copy (pads never), whose finished rows are stored while the next
+// output tiles are multiplied.
+struct ImgArgs {
+  int64_t chw;    // elements between consecutive images of a channel (C*H*W)
+  int64_t hw;     // elements of one image (H*W)
+  int W;          // image width
+  int BE;         // elements of one band (w * W)
+  int lgnw;       // log2(NW)
+  int NH;         // bands per image
+  int WPI;        // windows per image (NH * NW)
+  int whole;      // 1: a sub-tile is 16 / WPI whole images
+  int SEGC;       // 16-byte chunks per contiguous piece (an image, or the sub-tile)
+  float inv_segc; // 1 / SEGC
+  int CPR;        // chunks per band in the rows of one output-tile pair
+  int pair_store; // 1: rows are stored per output-tile pair, else per sub-tile
+};
+
 template <int WIN>
-struct BandCfg {
-  static constexpr int ELEMS = 16 * WIN * WIN;  // elements of one sub-tile
-  static constexpr int CH = ELEMS / 8;          // its 16-byte chunks
-  static constexpr int KC = cdiv(CH, 64);       // chunks per lane
-  static constexpr int BUF_BYTES = rup(ELEMS * 2, 16);
+struct ImgCfg {
+  static constexpr int ELEMS = 16 * WIN * WIN;              // elements of one sub-tile
+  static constexpr int CH = ELEMS / 8;                      // its 16-byte chunks
+  static constexpr int KC = cdiv(CH, 64);                   // chunks per lane
+  static constexpr int DUMMY = ELEMS + 8;                   // element that takes masked writes
+  static constexpr int BUF_BYTES = rup((ELEMS + 16) * 2, 16);  // + read overrun and dummy slot
+  static constexpr int RPP = rp_of(WIN) == 8 ? 4 : 2;       // window rows per output-tile pair
 };
 
 template <class Tag, int WIN>
-__host__ __device__ constexpr size_t fwd_band_lds_bytes() {
+__host__ __device__ constexpr size_t fwd_img_lds_bytes() {
   typedef FwdCfg<Tag, WIN> G;
-  return (size_t)kFwdWaves * BandCfg<WIN>::BUF_BYTES + (size_t)(G::TS_LEN + G::TB_LEN) * Tag::ES;
+  return (size_t)kFwdWaves * ImgCfg<WIN>::BUF_BYTES + (size_t)(G::TS_LEN + G::TB_LEN) * Tag::ES;
 }
 
-// Element offset of the first element of the band holding window n.
-__device__ __attribute__((always_inline)) inline int64_t band_offset(const KArgs &a, int64_t c, int64_t n, int win) {
-  const int nhw = a.NH * a.NW;
-  const int b = fdiv((int)n, nhw, a.inv_nhw);
-  const int wy = fdiv((int)n - b * nhw, a.NW, a.inv_nw);
-  return (((int64_t)b * a.C + c) * a.H + (int64_t)wy * win) * a.W;
-}
-
-// The 16-byte chunks of the bands of one sub-tile (window m0 and on, nb
-// bands), lane + 64 k; chunk q of the sub-tile is element 8 q of its LDS copy.
-template <int WIN>
-__device__ __attribute__((always_inline)) inline void band_load(const KArgs &a, const void *x, int64_t c, int64_t m0,
-                                                                 int nb, int lane, uint4 (&v)[BandCfg<WIN>::KC]) {
-  const int cpb = WIN * (int)a.W / 8;  // chunks per band
-#pragma unroll
-  for (int k = 0; k < BandCfg<WIN>::KC; ++k) {
-    const int q = lane + 64 * k;
-    v[k] = make_uint4(0, 0, 0, 0);
-    if (q < nb * cpb) {
-      const int j = q / cpb;
-      const int64_t e = band_offset(a, c, m0 + (int64_t)j * a.NW, WIN) + 8 * (int64_t)(q - j * cpb);
-      v[k] = *reinterpret_cast<const uint4 *>(reinterpret_cast<const char *>(x) + 2 * e);
-    }
-  }
+// Byte offset of chunk q of a sub-tile from the sub-tile's first element
+// (pieces of a sub-tile lie within 2^31 bytes of each other; the host checks
+// it); 0x7fffffff past the sub-tile's last chunk.  Offsets of the chunks of
+// missing pieces (a partial last sub-tile) are at least nseg * chw * 2.
+__device__ __attribute__((always_inline)) inline uint32_t img_chunk(const ImgArgs &ia, int q, int nch) {
+  const int seg = ia.whole ? fdiv(q, ia.SEGC, ia.inv_segc) : 0;
+  const uint32_t off = (uint32_t)seg * (uint32_t)(2 * ia.chw) + 16u * (uint32_t)(q - seg * ia.SEGC);
+  return q < nch ? off : 0x7fffffffu;
 }
 
 template <class Tag, int WIN, bool REV>
-__global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_band_kernel(const typename Tag::S *__restrict__ x,
-                                                                       const typename Tag::S *__restrict__ tab,
-                                                                       typename Tag::S *__restrict__ y, KArgs a) {
+__global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_img_kernel(const typename Tag::S *__restrict__ x,
+                                                                      const typename Tag::S *__restrict__ tab,
+                                                                      typename Tag::S *__restrict__ y, KArgs a,
+                                                                      ImgArgs ia) {
   typedef typename Tag::S S;
   typedef typename Tag::Frag Frag;
   typedef FwdCfg<Tag, WIN> G;
-  typedef BandCfg<WIN> BC;
-  static_assert(Tag::W16 && G::RP == 8, "band layout: 16-bit windows up to 8");
-  constexpr int S_ = G::S, NT = G::NT, NB = G::NB, KC = BC::KC;
+  typedef ImgCfg<WIN> IC;
+  static_assert(Tag::W16, "image layout: 16-bit");
+  constexpr int RP = G::RP, S_ = G::S, NT = G::NT, NB = G::NB, KC = IC::KC, RPP = IC::RPP;
 
   extern __shared__ __align__(16) unsigned char smem[];
-  S *Ts = reinterpret_cast<S *>(smem + kFwdWaves * BC::BUF_BYTES);
+  S *Ts = reinterpret_cast<S *>(smem + kFwdWaves * IC::BUF_BYTES);
   S *TB = Ts + G::TS_LEN;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  u16 *raw = reinterpret_cast<u16 *>(smem + wave * BC::BUF_BYTES);  // this wave's bands
+  u16 *raw = reinterpret_cast<u16 *>(smem + wave * IC::BUF_BYTES);  // this wave's sub-tile, image layout
+  const uint32_t *raw32 = reinterpret_cast<const uint32_t *>(raw);
 
   const int64_t c = blockIdx.x / a.tiles_per_ch;
   const int64_t n0 = (int64_t)(blockIdx.x - c * a.tiles_per_ch) * a.tile;
   const int nwin = (int)((n0 + a.tile <= a.N) ? a.tile : a.N - n0);
-  const int spw = a.tile / (16 * kFwdWaves);  // sub-tiles per wave
+  const int spw = a.tile / (16 * kFwdWaves);
   const int first = wave * spw;
   int nsub = (nwin - first * 16 + 15) / 16;
   nsub = nsub < 0 ? 0 : (nsub > spw ? spw : nsub);
-  const int W = (int)a.W;
-  const int NWb = a.NW;            // windows per band
-  const int BE = WIN * W;          // elements per band
-  auto bands_of = [&](int j) -> int {  // bands of sub-tile j
-    const int mw = nwin - (first + j) * 16;
-    return (mw < 16 ? mw : 16) / NWb;
+
+  // per-lane addressing, fixed for the launch (the chunk offsets are
+  // recomputed where used rather than held in registers)
+  auto chunk_off = [&](int k) -> uint32_t {
+    int l = lane;
+    asm volatile("" : "+v"(l));
+    return img_chunk(ia, l + 64 * k, IC::CH);
+  };
+  const int g = lane >> 4;
+  const int ln = lane & 15;
+  const int nwm = (1 << ia.lgnw) - 1;
+  const int abase = (ln >> ia.lgnw) * ia.BE + (ln & nwm) * WIN;  // window ln of the sub-tile in LDS
+  // store task of this lane per output-tile pair: band jj, chunk i of its rows
+  const int sjj = lane / ia.CPR;
+  const int si = lane - sjj * ia.CPR;
+  const int sseg = ia.whole ? sjj / ia.NH : 0;
+  const uint32_t soff = (uint32_t)sseg * (uint32_t)(2 * ia.chw) + 2u * (uint32_t)((sjj - sseg * ia.NH) * ia.BE + 8 * si);
+  const int sloff = sjj * ia.BE + 8 * si;
+
+  // element offset of the first element of sub-tile m0, the byte bound of
+  // its chunk offsets and its band count
+  auto sub_base = [&](int64_t m0, uint32_t &lim, int &nb) -> int64_t {
+    const int mi = (int)m0;
+    const int img = mi / ia.WPI;
+    const int inw = mi - img * ia.WPI;
+    const int64_t left = a.N - m0;
+    const int nw = left < 16 ? (int)left : 16;
+    lim = ia.whole ? (uint32_t)(nw / ia.WPI) * (uint32_t)(2 * ia.chw) : 0x7fffffffu;
+    nb = nw >> ia.lgnw;
+    return (int64_t)img * ia.chw + c * ia.hw + (int64_t)(inw >> ia.lgnw) * ia.BE;
+  };
+  auto load = [&](int64_t m0, uint4 (&v)[KC]) {
+    uint32_t lim;
+    int nb;
+    const char *src = reinterpret_cast<const char *>(x + sub_base(m0, lim, nb));
+#pragma unroll
+    for (int k = 0; k < KC; ++k) {
+      const uint32_t off = chunk_off(k);
+      v[k] = make_uint4(0, 0, 0, 0);
+      if (off < lim) v[k] = *reinterpret_cast<const uint4 *>(src + off);
+    }
   };
 
   uint4 nxt[KC];
-  if (nsub > 0) band_load<WIN>(a, x, c, n0 + first * 16, bands_of(0), lane, nxt);
+  if (nsub > 0) load(n0 + first * 16, nxt);
   fwd_tables<Tag, WIN, REV>(tab, nullptr, c, Ts, TB, nullptr, nullptr, tid);
 
-  const int g = lane >> 4;
-  const int ln = lane & 15;
   for (int j = 0; j < nsub; ++j) {
     const int64_t m0 = n0 + (first + j) * 16;
-    const int nb = bands_of(j);
-    const int nw16 = nb * NWb;  // windows of this sub-tile
+    uint32_t lim;
+    int nb;
+    char *dst = reinterpret_cast<char *>(y + sub_base(m0, lim, nb));
     wave_lds_sync();
 #pragma unroll
     for (int k = 0; k < KC; ++k) {
       const int q = lane + 64 * k;
-      if (q < BC::CH) *reinterpret_cast<uint4 *>(raw + 8 * q) = nxt[k];
+      if (q < IC::CH) *reinterpret_cast<uint4 *>(raw + 8 * q) = nxt[k];
     }
-    if (j + 1 < nsub) band_load<WIN>(a, x, c, m0 + 16, bands_of(j + 1), lane, nxt);
+    if (j + 1 < nsub) load(m0 + 16, nxt);
     wave_lds_sync();
-    // A fragment of K step s: window ln, its row 4s + g, columns 0..7
-    const int jb = ln / NWb, wx = ln - jb * NWb;
-    const int abase = jb * BE + wx * WIN;
+    // LDS addresses derived from ab are recomputed per sub-tile rather than
+    // held in registers across the loop
+    int ab = abase;
+    asm volatile("" : "+v"(ab));
+    // B operand of K step s (the window-major fragment): window ln, 8
+    // consecutive positions of one window row, read as dwords from its image
+    // copy and shifted by one element when the row starts at an odd element
     Frag af[S_];
 #pragma unroll
     for (int s = 0; s < S_; ++s) {
-      const int r = 4 * s + g;
-      Frag f = Frag{0, 0, 0, 0, 0, 0, 0, 0};
-      if (r < WIN && ln < nw16) {
+      const int r = RP == 8 ? 4 * s + g : 2 * s + (g >> 1);  // window row
+      const int x0 = RP == 8 ? 0 : 8 * (g & 1);              // first column
+      const bool rok = r < WIN;
+      const int e0 = ab + (rok ? r : 0) * ia.W + x0;
+      const uint32_t *p = raw32 + (e0 >> 1);
+      const uint32_t sh = (uint32_t)(e0 & 1) * 16u;
+      uint32_t d[5];
 #pragma unroll
-        for (int e = 0; e < WIN; ++e) f[e] = raw[abase + r * W + e];
+      for (int i = 0; i < 5; ++i) d[i] = p[i];
+      uint32_t u[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        uint32_t v = __builtin_amdgcn_alignbit(d[i + 1], d[i], sh);
+        // columns x0 + 2i, x0 + 2i + 1 beyond the window are zero pads
+        const int xa = x0 + 2 * i;
+        v = xa >= WIN ? 0u : (xa + 1 >= WIN ? (v & 0xffffu) : v);
+        u[i] = rok ? v : 0u;
       }
-      af[s] = f;
+      af[s] = __builtin_bit_cast(Frag, make_uint4(u[0], u[1], u[2], u[3]));
     }
-    // the four windows 4g .. 4g+3 this lane's results belong to
-    int obase[4];
-#pragma unroll
-    for (int rr = 0; rr < 4; ++rr) {
-      const int m = 4 * g + rr;
-      const int jo = m / NWb;
-      obase[rr] = m < nw16 ? jo * BE + (m - jo * NWb) * WIN : -1;
-    }
+    // stores rows [r0, r1) of every band of the sub-tile
+    auto store_rows = [&](int r0, int r1) {
+      const int cpr = (r1 - r0) * ia.W / 8;
+      if (si < cpr && sjj < nb) {
+        const uint4 val = *reinterpret_cast<const uint4 *>(raw + sloff + r0 * ia.W);
+        *reinterpret_cast<uint4 *>(dst + soff + 2u * (uint32_t)(r0 * ia.W)) = val;
+      }
+    };
     Frag bf[NB];
 #pragma unroll
     for (int t0 = 0; t0 < NT; t0 += 2) {
 #pragma unroll
       for (int q = 0; q < NB; ++q) {
-        const int tf = NT - 1 - q;  // smallest t with this parity using q
+        const int tf = NT - 1 - q;
         const int first_t = tf >= 0 ? tf : (((-tf) & 1) ? 1 : 0);
         if (first_t == t0 || first_t == t0 + 1) bf[q] = fwd_bfrag<Tag, WIN>(TB, q, g, ln);
       }
       f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < S_; ++s) {
-        acc0 = mma<Tag>(af[s], bf[2 * s - t0 + NT - 1], acc0);
-        if (t0 + 1 < NT) acc1 = mma<Tag>(af[s], bf[2 * s - t0 - 1 + NT - 1], acc1);
+        acc0 = mma<Tag>(bf[2 * s - t0 + NT - 1], af[s], acc0);
+        if (t0 + 1 < NT) acc1 = mma<Tag>(bf[2 * s - t0 - 1 + NT - 1], af[s], acc1);
       }
-      // results: output position ln of tile t = row 2t + ln / 8, column ln % 8
+      // results (M^T X^T): window ln, positions 16 t + 4 g .. + 3, i.e. one
+      // window row ho, columns xo0 .. xo0 + 3; columns and rows beyond the
+      // window go to the dummy element
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const int t = t0 + h;
         if (t >= NT) continue;
         const f32x4 acc = h ? acc1 : acc0;
-        const int ho = 2 * t + (ln >> 3), xo = ln & 7;
-        if (ho < WIN && xo < WIN) {
-          const uint32_t lo = pack2<Tag>(acc[0], acc[1]);
-          const uint32_t hi = pack2<Tag>(acc[2], acc[3]);
+        const int ho = RP == 8 ? 2 * t + (g >> 1) : t;
+        const int xo0 = RP == 8 ? 4 * (g & 1) : 4 * g;
+        const int o = ab + (ho < WIN ? ho : 0) * ia.W + xo0;
+        const uint32_t lo = pack2<Tag>(acc[0], acc[1]);
+        const uint32_t hi = pack2<Tag>(acc[2], acc[3]);
+        if constexpr ((WIN & 1) == 0) {
+          // even windows: every window row starts at an even element
+          uint32_t *o32 = reinterpret_cast<uint32_t *>(raw);
+          const int da = (ho < WIN && xo0 < WIN) ? o : IC::DUMMY;
+          const int db = (ho < WIN && xo0 + 2 < WIN) ? o + 2 : IC::DUMMY;
+          o32[da >> 1] = lo;
+          o32[db >> 1] = hi;
+        } else {
           const u16 vals[4] = {(u16)(lo & 0xffffu), (u16)(lo >> 16), (u16)(hi & 0xffffu), (u16)(hi >> 16)};
 #pragma unroll
-          for (int rr = 0; rr < 4; ++rr)
-            if (obase[rr] >= 0) raw[obase[rr] + ho * W + xo] = vals[rr];
+          for (int rr = 0; rr < 4; ++rr) raw[(ho < WIN && xo0 + rr < WIN) ? o + rr : IC::DUMMY] = vals[rr];
         }
       }
-      // image rows [2 t0, 2 t0 + 4) of every band are final: store them
+      if (ia.pair_store) {
+        wave_lds_sync();
+        const int r0 = RPP * (t0 / 2);
+        const int r1 = r0 + RPP < WIN ? r0 + RPP : WIN;
+        if (r0 < WIN) store_rows(r0, r1);
+      }
+    }
+    if (!ia.pair_store) {
       wave_lds_sync();
-      {
-        const int r0 = 2 * t0;
-        const int r1 = r0 + 4 < WIN ? r0 + 4 : WIN;
-        const int cpr = (r1 - r0) * W / 8;  // chunks per band in these rows
-        if (lane < nb * cpr) {
-          const int jj = lane / cpr;
-          const int i = r0 * W / 8 + (lane - jj * cpr);
-          const uint4 val = *reinterpret_cast<const uint4 *>(raw + jj * BE + 8 * i);
-          const int64_t e = band_offset(a, c, m0 + (int64_t)jj * NWb, WIN) + 8 * (int64_t)i;
-          *reinterpret_cast<uint4 *>(reinterpret_cast<char *>(y) + 2 * e) = val;
-        }
+#pragma unroll
+      for (int k = 0; k < KC; ++k) {
+        const uint32_t off = chunk_off(k);
+        if (off < lim) *reinterpret_cast<uint4 *>(dst + off) = *reinterpret_cast<const uint4 *>(raw + 8 * (lane + 64 * k));
       }
     }
   }
@@ -1555,6 +1620,39 @@ static int pick_fwd_tile(const Geom &g) {
   return 16 * kFwdWaves * spw;
 }
 
+// Whether a 16-bit forward can take the image-layout kernel, and its
+// geometry: windows tile the map, NW is a power of two, a 16-window sub-tile
+// is whole bands of one image or whole images, every piece starts on a 16-byte
+// boundary (both tensors 16-byte aligned).
+template <int WIN>
+static bool img_layout(const Geom &g, const void *x, const void *y, ImgArgs &ia) {
+  if (g.H % WIN != 0 || g.W % WIN != 0 || g.NW > 16 || (g.NW & (g.NW - 1)) != 0) return false;
+  if ((reinterpret_cast<uintptr_t>(x) & 15) != 0 || (reinterpret_cast<uintptr_t>(y) & 15) != 0) return false;
+  const int64_t wpi = g.NH * g.NW, be = (int64_t)WIN * g.W, hw = g.H * g.W;
+  const bool inside = wpi % 16 == 0;        // sub-tile = bands of one image
+  const bool whole = !inside && 16 % wpi == 0;  // sub-tile = whole images
+  if (!inside && !whole) return false;
+  if (inside ? be % 8 != 0 : hw % 8 != 0) return false;
+  // chunk offsets inside a sub-tile are 32-bit byte offsets
+  if (whole && 2 * (16 / wpi) * g.C * hw >= ((int64_t)1 << 31)) return false;
+  constexpr int RPP = ImgCfg<WIN>::RPP;
+  ia.chw = g.C * hw;
+  ia.hw = hw;
+  ia.W = (int)g.W;
+  ia.BE = (int)be;
+  int lg = 0;
+  while ((1 << lg) < g.NW) ++lg;
+  ia.lgnw = lg;
+  ia.NH = (int)g.NH;
+  ia.WPI = (int)wpi;
+  ia.whole = whole ? 1 : 0;
+  ia.SEGC = whole ? (int)(hw / 8) : ImgCfg<WIN>::CH;
+  ia.inv_segc = 1.0f / (float)ia.SEGC;
+  ia.pair_store = (RPP * g.W) % 8 == 0 && ((WIN % RPP) * g.W) % 8 == 0 && be % 8 == 0;
+  ia.CPR = ia.pair_store ? (int)(RPP * g.W / 8) : 1;
+  return true;
+}
+
 template <class Tag, int WIN>
 static hipError_t run_forward(const void *x, const void *t, void *y, const Geom &g, bool rev,
                               hipStream_t st) {
@@ -1563,18 +1661,15 @@ static hipError_t run_forward(const void *x, const void *t, void *y, const Geom 
   a.tile = pick_fwd_tile<Tag, WIN>(g);
   a.tiles_per_ch = (int)cdiv64(g.N, a.tile);
   const dim3 grid((unsigned)(g.C * a.tiles_per_ch));
-  if constexpr (Tag::W16 && rp_of(WIN) == 8) {
-    // band layout: windows tile the map, NW divides 16, image rows and both
-    // tensors 16-byte aligned
-    const bool band = g.H % WIN == 0 && g.W % WIN == 0 && 16 % g.NW == 0 && g.W % 8 == 0 &&
-                      (reinterpret_cast<uintptr_t>(x) & 15) == 0 && (reinterpret_cast<uintptr_t>(y) & 15) == 0;
-    if (band) {
-      constexpr size_t blds = fwd_band_lds_bytes<Tag, WIN>();
-      static_assert(blds <= 65536, "workgroup LDS above 64 KB");
+  if constexpr (Tag::W16) {
+    ImgArgs ia;
+    if (img_layout<WIN>(g, x, y, ia)) {
+      constexpr size_t ilds = fwd_img_lds_bytes<Tag, WIN>();
+      static_assert(ilds <= 65536, "workgroup LDS above 64 KB");
       if (rev)
-        wbmm_fwd_band_kernel<Tag, WIN, true><<<grid, dim3(kFwdThreads), blds, st>>>((const S *)x, (const S *)t, (S *)y, a);
+        wbmm_fwd_img_kernel<Tag, WIN, true><<<grid, dim3(kFwdThreads), ilds, st>>>((const S *)x, (const S *)t, (S *)y, a, ia);
       else
-        wbmm_fwd_band_kernel<Tag, WIN, false><<<grid, dim3(kFwdThreads), blds, st>>>((const S *)x, (const S *)t, (S *)y, a);
+        wbmm_fwd_img_kernel<Tag, WIN, false><<<grid, dim3(kFwdThreads), ilds, st>>>((const S *)x, (const S *)t, (S *)y, a, ia);
       return hipGetLastError();
     }
   }

@@ -166,16 +166,24 @@ def test_integer_data_bit_exact(w, dtype):
         assert np.array_equal(got[k], want[k]), k
 
 
-# shapes for the band-layout forward (16-bit, w <= 8, windows tile the map,
-# windows per band divide 16, rows 16-byte aligned)
-BAND = [
+# shapes for the image-layout forward (16-bit, windows tile the map, NW a
+# power of two, a 16-window sub-tile is whole bands of one image or whole
+# images, pieces 16-byte aligned)
+IMG = [
     (5, 3, 56, 56, 7),
-    (3, 2, 14, 56, 7),     # 48 windows per channel: a ragged last tile
+    (3, 2, 14, 56, 7),     # 16 windows per image; ragged last tile
     (2, 3, 16, 16, 4),     # 4 windows per band
-    (1, 2, 24, 64, 8),     # 8 windows per band
+    (1, 2, 24, 64, 8),     # 24 windows per image: neither layout, row path
     (2, 2, 8, 32, 2),      # 16 windows per band
-    (3, 2, 5, 40, 5),      # one band per image
+    (3, 2, 5, 40, 5),      # one band per image, two images per sub-tile, partial last sub-tile
     (1, 4, 16, 16, 1),
+    (4, 3, 28, 28, 14),    # four images per sub-tile
+    (3, 2, 28, 28, 14),    # three images in the only sub-tile
+    (1, 2, 112, 112, 14),  # bands of one image
+    (2, 3, 24, 48, 12),
+    (5, 2, 16, 32, 16),    # eight images per sub-tile, partial
+    (2, 2, 18, 36, 9),     # odd window (2-byte result writes), rows stored per sub-tile
+    (1, 2, 30, 60, 15),
 ]
 
 
@@ -189,9 +197,9 @@ def misaligned_like(t):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
-@pytest.mark.parametrize("shape", BAND, ids=lambda s: "B%dC%dH%dW%dw%d" % s)
-def test_band_layout_forward(shape, dtype):
-    """The band-layout forward and input gradient match the oracle and equal
+@pytest.mark.parametrize("shape", IMG, ids=lambda s: "B%dC%dH%dW%dw%d" % s)
+def test_image_layout_forward(shape, dtype):
+    """The image-layout forward and input gradient match the oracle and equal
     the row-path results bit for bit (same products, same order)."""
     B, C, H, Wd, w = shape
     d = draw(B, C, H, Wd, w, dtype, seed=21)
@@ -203,13 +211,13 @@ def test_band_layout_forward(shape, dtype):
     W.wbmm_backward_input(dym, t, w, out=dxm)
     torch.cuda.synchronize()
     assert torch.equal(y, ym) and torch.equal(dx, dxm)
-    check({"fwd": to_f64(y), "dx": to_f64(dx)}, run_oracle(d, w, ("fwd", "dx")), dtype, "band %s" % (shape,))
+    check({"fwd": to_f64(y), "dx": to_f64(dx)}, run_oracle(d, w, ("fwd", "dx")), dtype, "image layout %s" % (shape,))
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
-def test_band_layout_one_hot_bit_exact(dtype):
-    w = 7
-    B, C, H, Wd = 2, 6, 14, 56
+@pytest.mark.parametrize("w", [7, 14])
+def test_image_layout_one_hot_bit_exact(dtype, w):
+    B, C, H, Wd = (2, 6, 14, 56) if w == 7 else (3, 6, 28, 28)
     d = draw(B, C, H, Wd, w, dtype, seed=6)
     K = 2 * w - 1
     t64 = np.zeros((C, K * K))
