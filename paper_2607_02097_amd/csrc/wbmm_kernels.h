@@ -51,6 +51,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <initializer_list>
+
 #include "wbmm_internal.h"
 
 namespace wbmm {
@@ -144,6 +146,17 @@ struct KArgs {
   int tile;            // windows per workgroup tile (forward) / per slab (dtable)
   int tiles_per_ch;    // workgroups per channel
   float inv_nw, inv_nhw;
+  // Fixed-offset rows (gradient kernels): when tiled is set, windows tile the
+  // map, every window row is whole and starts on a dword, and a 16-window
+  // sub-tile (16-aligned) is whole bands of one image or whole images, so a
+  // row's byte offset from its sub-tile's first element depends only on its
+  // place in the sub-tile.
+  int tiled;
+  int lgnw;            // log2(NW)
+  int lgw;             // log2(windows per piece of a sub-tile): 4 inside one image, else log2(NH * NW)
+  int BE;              // elements of one band (w * W)
+  int WPI;             // windows per image
+  int64_t chw;         // elements between images of one channel (C * H * W)
 };
 
 // A window row: element offset (from the tensor base) of its first element,
@@ -196,6 +209,22 @@ __device__ __attribute__((always_inline)) inline Row<WIN, ES> row_of(const KArgs
     }
   }
   return r;
+}
+
+// Fixed-offset rows: element offset of the first element of the 16-window
+// sub-tile that starts at window m (a multiple of 16), and the byte offset of
+// row hi of its window vv (0..15) from there.
+__device__ __attribute__((always_inline)) inline int64_t tiled_sub_base(const KArgs &a, int64_t c, int64_t m) {
+  const int mi = (int)m;
+  const int img = mi / a.WPI;
+  const int inw = mi - img * a.WPI;
+  return (int64_t)img * a.chw + c * a.H * a.W + (int64_t)(inw >> a.lgnw) * a.BE;
+}
+template <int WIN, int ES>
+__device__ __attribute__((always_inline)) inline uint32_t tiled_row_off(const KArgs &a, int vv, int hi) {
+  const int nwm = (1 << a.lgnw) - 1, mw = (1 << a.lgw) - 1;
+  return (uint32_t)(vv >> a.lgw) * (uint32_t)(a.chw * ES) +
+         (uint32_t)((((vv & mw) >> a.lgnw) * a.BE + (vv & nwm) * WIN + hi * (int)a.W) * ES);
 }
 
 // Dwords of one padded row (RP elements) in registers.
@@ -1064,15 +1093,50 @@ __host__ __device__ constexpr size_t bwd_lds_bytes() {
 
 // Row copies of one stage: task q covers tensor (q / (CW * KR)), window
 // (q / KR) % CW of the stage and padded row q % KR (rows >= w are zero).
-template <class Tag, int WIN, class G>
-struct Stage {
-  RowData<WIN, Tag::ES> rd[G::RPT];
-};
+// Fixed-offset rows take another mapping: copy k covers tensor k / SUBS and
+// sub-tile k % SUBS (SUBS = CW / 16), thread tid its window tid / KR and
+// padded row tid % KR, so that every copy instruction has one base address.
+template <class G>
+__host__ __device__ constexpr int tiled_rpt() { return 2 * (G::CW / 16); }
 
 template <class Tag, int WIN, class G>
+struct Stage {
+  static constexpr int N = G::RPT > tiled_rpt<G>() ? G::RPT : tiled_rpt<G>();
+  RowData<WIN, Tag::ES> rd[N];
+};
+
+template <class Tag, int WIN, class G, bool TILED>
 __device__ __attribute__((always_inline)) inline void stage_load(const KArgs &a, const void *x, const void *dy,
                                                                   int64_t c, int64_t m0, int64_t m1, int tid,
                                                                   Stage<Tag, WIN, G> &st) {
+  if constexpr (TILED) {
+    // fixed-offset rows: whole and dword-aligned; one base address per copy
+    constexpr int NDV = (WIN * Tag::ES) / 4, SUBS = G::CW / 16;
+    typedef typename Tag::S S;
+    const int vv = tid / G::KR;
+    const int hi = tid - vv * G::KR;
+    const uint32_t off = tiled_row_off<WIN, Tag::ES>(a, vv & 15, hi);
+#pragma unroll
+    for (int k = 0; k < tiled_rpt<G>(); ++k) {
+      const int tens = k / SUBS, sub = k % SUBS;
+#pragma unroll
+      for (int i = 0; i < RowData<WIN, Tag::ES>::ND; ++i) st.rd[k].d[i] = 0;
+      const int64_t ms = m0 + 16 * sub;
+      if (vv < 16 && hi < WIN && ms + vv < m1) {
+        const S *src = tens ? reinterpret_cast<const S *>(dy) : reinterpret_cast<const S *>(x);
+        const uint32_t *p4 = reinterpret_cast<const uint32_t *>(
+            reinterpret_cast<const char *>(src + tiled_sub_base(a, c, ms)) + off);
+#pragma unroll
+        for (int i = 0; i + 4 <= NDV; i += 4) {
+          const u32x4a u = *reinterpret_cast<const u32x4a *>(p4 + i);
+          st.rd[k].d[i] = u.x; st.rd[k].d[i + 1] = u.y; st.rd[k].d[i + 2] = u.z; st.rd[k].d[i + 3] = u.w;
+        }
+#pragma unroll
+        for (int i = NDV & ~3; i < NDV; ++i) st.rd[k].d[i] = p4[i];
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int k = 0; k < G::RPT; ++k) {
     const int q = tid + k * kThreads;
@@ -1089,10 +1153,27 @@ __device__ __attribute__((always_inline)) inline void stage_load(const KArgs &a,
 }
 
 // Write a loaded stage window-major (padded rows, as in the forward tile).
-template <class Tag, int WIN, class G>
+template <class Tag, int WIN, class G, bool TILED>
 __device__ __attribute__((always_inline)) inline void stage_write(unsigned char *smem, int tid,
                                                                    const Stage<Tag, WIN, G> &st) {
   typedef RowData<WIN, Tag::ES> RD;
+  if constexpr (TILED) {
+    constexpr int SUBS = G::CW / 16;
+    const int vv = tid / G::KR;
+    const int hi = tid - vv * G::KR;
+    if (vv < 16) {
+#pragma unroll
+      for (int k = 0; k < tiled_rpt<G>(); ++k) {
+        const int tens = k / SUBS, sub = k % SUBS;
+        uint32_t *l4 = reinterpret_cast<uint32_t *>(smem + tens * G::BUF +
+                                                    ((16 * sub + vv) * G::LDSW + hi * G::RP) * Tag::ES);
+#pragma unroll
+        for (int i = 0; i < RD::ND; i += 4)
+          *reinterpret_cast<uint4 *>(l4 + i) = make_uint4(st.rd[k].d[i], st.rd[k].d[i + 1], st.rd[k].d[i + 2], st.rd[k].d[i + 3]);
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int k = 0; k < G::RPT; ++k) {
     const int q = tid + k * kThreads;
@@ -1347,7 +1428,7 @@ __device__ __attribute__((always_inline)) inline void dt_finish(const f32x4 (&ac
   if (tid == 0) __hip_atomic_store(&cnt[c], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-template <class Tag, int WIN, int WAVE>
+template <class Tag, int WIN, int WAVE, bool TILED>
 __device__ __attribute__((always_inline)) void dt_wave(const typename Tag::S *__restrict__ x, const typename Tag::S *__restrict__ dy,
                         float *__restrict__ dt, float *__restrict__ part, unsigned *__restrict__ cnt,
                         const KArgs &a, unsigned char *smem) {
@@ -1365,28 +1446,28 @@ __device__ __attribute__((always_inline)) void dt_wave(const typename Tag::S *__
   for (int j = 0; j < SP::na; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   Stage<Tag, WIN, G> st;
-  stage_load<Tag, WIN, G>(a, x, dy, c, s0, s1, tid, st);
+  stage_load<Tag, WIN, G, TILED>(a, x, dy, c, s0, s1, tid, st);
   for (int64_t m0 = s0; m0 < s1; m0 += G::CW) {
     if (m0 != s0) __syncthreads();  // previous stage consumed
-    stage_write<Tag, WIN, G>(smem, tid, st);
+    stage_write<Tag, WIN, G, TILED>(smem, tid, st);
     __syncthreads();
-    if (m0 + G::CW < s1) stage_load<Tag, WIN, G>(a, x, dy, c, m0 + G::CW, s1, tid, st);
+    if (m0 + G::CW < s1) stage_load<Tag, WIN, G, TILED>(a, x, dy, c, m0 + G::CW, s1, tid, st);
     dt_products<Tag, G, WAVE>(smem, smem + G::BUF, acc, lane);
   }
   dt_finish<Tag, WIN, G, WAVE>(acc, smem, dt, part, cnt, a, c, slab);
 }
 
-template <class Tag, int WIN>
+template <class Tag, int WIN, bool TILED>
 __global__ __launch_bounds__(kThreads, 3) void wbmm_dt_kernel(const typename Tag::S *__restrict__ x,
                                                               const typename Tag::S *__restrict__ dy,
                                                               float *__restrict__ dt, float *__restrict__ part,
                                                               unsigned *__restrict__ cnt, KArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   switch (threadIdx.x >> 6) {
-    case 0: dt_wave<Tag, WIN, 0>(x, dy, dt, part, cnt, a, smem); break;
-    case 1: dt_wave<Tag, WIN, 1>(x, dy, dt, part, cnt, a, smem); break;
-    case 2: dt_wave<Tag, WIN, 2>(x, dy, dt, part, cnt, a, smem); break;
-    default: dt_wave<Tag, WIN, 3>(x, dy, dt, part, cnt, a, smem); break;
+    case 0: dt_wave<Tag, WIN, 0, TILED>(x, dy, dt, part, cnt, a, smem); break;
+    case 1: dt_wave<Tag, WIN, 1, TILED>(x, dy, dt, part, cnt, a, smem); break;
+    case 2: dt_wave<Tag, WIN, 2, TILED>(x, dy, dt, part, cnt, a, smem); break;
+    default: dt_wave<Tag, WIN, 3, TILED>(x, dy, dt, part, cnt, a, smem); break;
   }
 }
 
@@ -1481,11 +1562,34 @@ __device__ __attribute__((always_inline)) inline void dx_products(const unsigned
 }
 
 // Store the stage's input-gradient rows (window-major in Obuf).
-template <class Tag, int WIN>
+template <class Tag, int WIN, bool TILED>
 __device__ __attribute__((always_inline)) inline void dx_store(const KArgs &a, void *dx, int64_t c, int64_t m0,
                                                                 int64_t m1, int tid, const unsigned char *Obuf) {
   typedef BwdCfg<Tag, WIN> G;
   typedef RowData<WIN, Tag::ES> RD;
+  if constexpr (TILED) {
+    constexpr int NDV = (WIN * Tag::ES) / 4, SUBS = G::CW / 16;
+    typedef typename Tag::S S;
+    const int vv = tid / WIN;
+    const int hi = tid - vv * WIN;
+    const uint32_t off = tiled_row_off<WIN, Tag::ES>(a, vv & 15, hi);
+#pragma unroll
+    for (int sub = 0; sub < SUBS; ++sub) {
+      const int64_t ms = m0 + 16 * sub;
+      if (vv < 16 && ms + vv < m1) {
+        const uint32_t *l4 = reinterpret_cast<const uint32_t *>(Obuf + ((16 * sub + vv) * G::LDSW + hi * G::RP) * Tag::ES);
+        uint32_t *p4 = reinterpret_cast<uint32_t *>(reinterpret_cast<char *>(reinterpret_cast<S *>(dx) + tiled_sub_base(a, c, ms)) + off);
+#pragma unroll
+        for (int i = 0; i + 4 <= NDV; i += 4) {
+          const uint4 u = *reinterpret_cast<const uint4 *>(l4 + i);
+          *reinterpret_cast<u32x4a *>(p4 + i) = u32x4a{u.x, u.y, u.z, u.w};
+        }
+#pragma unroll
+        for (int i = NDV & ~3; i < NDV; ++i) p4[i] = l4[i];
+      }
+    }
+    return;
+  }
   for (int q = tid; q < G::CW * WIN; q += kThreads) {
     const int v = q / WIN;
     const int hi = q - v * WIN;
@@ -1508,7 +1612,7 @@ __device__ __attribute__((always_inline)) inline void dx_store(const KArgs &a, v
 // share of X^T dY; after a barrier the x tile is free and receives the
 // input-gradient results computed from the dy tile, which are then stored
 // as rows.  dY is read once for both gradients.
-template <class Tag, int WIN, int WAVE>
+template <class Tag, int WIN, int WAVE, bool TILED>
 __device__ __attribute__((always_inline)) void bwd_wave(const typename Tag::S *__restrict__ x,
                                                         const typename Tag::S *__restrict__ dy,
                                                         const typename Tag::S *__restrict__ tab,
@@ -1535,7 +1639,7 @@ __device__ __attribute__((always_inline)) void bwd_wave(const typename Tag::S *_
   // first stage in flight; the reversed table row and (16-bit) its Toeplitz
   // blocks -> LDS
   Stage<Tag, WIN, G> st;
-  stage_load<Tag, WIN, G>(a, x, dy, c, s0, s1, tid, st);
+  stage_load<Tag, WIN, G, TILED>(a, x, dy, c, s0, s1, tid, st);
   {
     S *Ts = reinterpret_cast<S *>(smem + G::TS_OFF);
     const S *tc = tab + c * K2;
@@ -1567,20 +1671,20 @@ __device__ __attribute__((always_inline)) void bwd_wave(const typename Tag::S *_
 
   for (int64_t m0 = s0; m0 < s1; m0 += G::CW) {
     if (m0 != s0) __syncthreads();  // previous stage's rows stored
-    stage_write<Tag, WIN, G>(smem, tid, st);
+    stage_write<Tag, WIN, G, TILED>(smem, tid, st);
     __syncthreads();
-    if (m0 + G::CW < s1) stage_load<Tag, WIN, G>(a, x, dy, c, m0 + G::CW, s1, tid, st);
+    if (m0 + G::CW < s1) stage_load<Tag, WIN, G, TILED>(a, x, dy, c, m0 + G::CW, s1, tid, st);
     dt_products<Tag, G, WAVE>(Xt, Dt, acc, lane);
     __syncthreads();  // the x tile is no longer read
     dx_products<Tag, WIN, WAVE>(Dt, Xt, smem, lane);
     __syncthreads();
-    dx_store<Tag, WIN>(a, dx, c, m0, s1, tid, Xt);
+    dx_store<Tag, WIN, TILED>(a, dx, c, m0, s1, tid, Xt);
   }
   dt_finish<Tag, WIN, G, WAVE>(acc, smem, dt, part, cnt, a, c, slab);
 }
 
-template <class Tag, int WIN>
-__global__ __launch_bounds__(kThreads, 2) void wbmm_bwd_kernel(const typename Tag::S *__restrict__ x,
+template <class Tag, int WIN, bool TILED>
+__global__ __launch_bounds__(kThreads, (TILED ? 3 : 2)) void wbmm_bwd_kernel(const typename Tag::S *__restrict__ x,
                                                                const typename Tag::S *__restrict__ dy,
                                                                const typename Tag::S *__restrict__ tab,
                                                                typename Tag::S *__restrict__ dx,
@@ -1588,10 +1692,10 @@ __global__ __launch_bounds__(kThreads, 2) void wbmm_bwd_kernel(const typename Ta
                                                                unsigned *__restrict__ cnt, KArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   switch (threadIdx.x >> 6) {
-    case 0: bwd_wave<Tag, WIN, 0>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
-    case 1: bwd_wave<Tag, WIN, 1>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
-    case 2: bwd_wave<Tag, WIN, 2>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
-    default: bwd_wave<Tag, WIN, 3>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
+    case 0: bwd_wave<Tag, WIN, 0, TILED>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
+    case 1: bwd_wave<Tag, WIN, 1, TILED>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
+    case 2: bwd_wave<Tag, WIN, 2, TILED>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
+    default: bwd_wave<Tag, WIN, 3, TILED>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
   }
 }
 
@@ -1607,7 +1711,38 @@ static KArgs make_args(const Geom &g) {
   a.tile = 0; a.tiles_per_ch = 0;
   a.inv_nw = 1.0f / (float)g.NW;
   a.inv_nhw = 1.0f / (float)(g.NH * g.NW);
+  a.tiled = 0;
+  a.lgnw = 0; a.lgw = 0; a.BE = 0; a.WPI = 1; a.chw = 0;
   return a;
+}
+
+// Fixed-offset rows for the gradient kernels (see KArgs): windows tile the
+// map, NW a power of two, a 16-window sub-tile is whole bands of one image or
+// whole images (within 2^31 bytes), rows dword-aligned (float32, or an even
+// window) in every tensor the kernel moves.
+template <int WIN, int ES>
+static void set_tiled(const Geom &g, KArgs &a, std::initializer_list<const void *> ptrs) {
+  a.tiled = 0;
+  if (g.H % WIN != 0 || g.W % WIN != 0 || g.NW > 16 || (g.NW & (g.NW - 1)) != 0) return;
+  if (ES == 2 && (WIN & 1)) return;
+  for (const void *p : ptrs)
+    if ((reinterpret_cast<uintptr_t>(p) & 3) != 0) return;
+  const int64_t wpi = g.NH * g.NW;
+  const bool inside = wpi % 16 == 0, whole = !inside && 16 % wpi == 0;
+  if (!inside && !whole) return;
+  const int64_t chw = g.C * g.H * g.W;
+  if (16 * chw * ES >= ((int64_t)1 << 31) && whole) return;
+  if ((int64_t)WIN * g.W * 16 * ES >= ((int64_t)1 << 31)) return;
+  int lg = 0;
+  while ((1 << lg) < g.NW) ++lg;
+  int lw = 0;
+  while ((1 << lw) < wpi) ++lw;
+  a.tiled = 1;
+  a.lgnw = lg;
+  a.lgw = inside ? 4 : lw;
+  a.BE = (int)(WIN * g.W);
+  a.WPI = (int)wpi;
+  a.chw = chw;
 }
 
 // Windows per forward workgroup: kFwdWaves waves x sub-tiles per wave x 16.
@@ -1734,12 +1869,19 @@ static hipError_t run_dtable(const void *x, const void *dy, float *dt, void *ws,
   const DtPlan p = plan_dt<Tag, WIN>(g);
   a.tile = (int)p.slab_windows;
   a.tiles_per_ch = (int)p.slabs;
+  set_tiled<WIN, Tag::ES>(g, a, {x, dy});
   unsigned *cnt = p.slabs > 1 ? (unsigned *)ws : nullptr;
   float *part = p.slabs > 1 ? (float *)((char *)ws + counter_bytes(g.C)) : nullptr;
   constexpr size_t lds = dt_lds_bytes<Tag, WIN>();
   static_assert(lds <= 65536, "workgroup LDS above 64 KB");
-  wbmm_dt_kernel<Tag, WIN><<<dim3((unsigned)(g.C * p.slabs)), dim3(kThreads), lds, st>>>(
-      (const S *)x, (const S *)dy, dt, part, cnt, a);
+  const dim3 grid((unsigned)(g.C * p.slabs));
+  if constexpr (Tag::ES == 4 || WIN % 2 == 0) {
+    if (a.tiled) {
+      wbmm_dt_kernel<Tag, WIN, true><<<grid, dim3(kThreads), lds, st>>>((const S *)x, (const S *)dy, dt, part, cnt, a);
+      return hipGetLastError();
+    }
+  }
+  wbmm_dt_kernel<Tag, WIN, false><<<grid, dim3(kThreads), lds, st>>>((const S *)x, (const S *)dy, dt, part, cnt, a);
   return hipGetLastError();
 }
 
@@ -1751,12 +1893,21 @@ static hipError_t run_backward(const void *x, const void *dy, const void *t, voi
   const DtPlan p = plan_dt<Tag, WIN>(g);
   a.tile = (int)p.slab_windows;
   a.tiles_per_ch = (int)p.slabs;
+  set_tiled<WIN, Tag::ES>(g, a, {x, dy, dx});
   unsigned *cnt = p.slabs > 1 ? (unsigned *)ws : nullptr;
   float *part = p.slabs > 1 ? (float *)((char *)ws + counter_bytes(g.C)) : nullptr;
   constexpr size_t lds = bwd_lds_bytes<Tag, WIN>();
   static_assert(lds <= 65536, "workgroup LDS above 64 KB");
-  wbmm_bwd_kernel<Tag, WIN><<<dim3((unsigned)(g.C * p.slabs)), dim3(kThreads), lds, st>>>(
-      (const S *)x, (const S *)dy, (const S *)t, (S *)dx, dt, part, cnt, a);
+  const dim3 grid((unsigned)(g.C * p.slabs));
+  if constexpr (Tag::ES == 4 || WIN % 2 == 0) {
+    if (a.tiled) {
+      wbmm_bwd_kernel<Tag, WIN, true><<<grid, dim3(kThreads), lds, st>>>((const S *)x, (const S *)dy, (const S *)t,
+                                                                         (S *)dx, dt, part, cnt, a);
+      return hipGetLastError();
+    }
+  }
+  wbmm_bwd_kernel<Tag, WIN, false><<<grid, dim3(kThreads), lds, st>>>((const S *)x, (const S *)dy, (const S *)t,
+                                                                      (S *)dx, dt, part, cnt, a);
   return hipGetLastError();
 }
 

@@ -109,6 +109,46 @@ def test_fused_backward_small(shape, dtype):
     check_fused(d, w, dtype, "%s %s" % (dtype, shape))
 
 
+# shapes whose gradient kernels take fixed-offset rows (windows tile the map,
+# NW a power of two, 16-window sub-tiles are whole bands of one image or whole
+# images; 16-bit needs an even window)
+TILED = [
+    (20, 3, 28, 28, 14),   # four images per sub-tile
+    (3, 2, 28, 28, 14),    # a partial sub-tile (three images)
+    (9, 2, 14, 14, 14),    # one window per image, partial sub-tile
+    (1, 2, 112, 112, 14),  # bands of one image
+    (2, 2, 32, 64, 16),
+    (4, 3, 24, 24, 12),
+    (2, 3, 40, 40, 10),
+    (3, 2, 18, 36, 9),     # odd window: float32 only
+    (5, 3, 56, 56, 7),     # odd window: float32 only
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", TILED, ids=lambda s: "B%dC%dH%dW%dw%d" % s)
+def test_fixed_offset_rows_backward(shape, dtype):
+    """Gradients on tensors whose rows the kernels address by fixed offsets
+    equal those on misaligned copies (generic row addressing) bit for bit, and
+    the oracle within tolerance."""
+    B, C, H, Wd, w = shape
+    d = draw(B, C, H, Wd, w, dtype, seed=31)
+    x, t, dy = (to_device(d[k], dtype) for k in ("x", "t", "dy"))
+    dx, dt = W.wbmm_backward(x, dy, t, w)
+    dt_s = W.wbmm_backward_table(x, dy, w)
+    if dtype != "f32":
+        xm, dym = misaligned_like(x), misaligned_like(dy)
+        dxm = misaligned_like(torch.zeros_like(dy))
+        dtm = torch.empty_like(dt)
+        W.wbmm_backward(xm, dym, t, w, dx=dxm, dtable=dtm)
+        dtm2 = W.wbmm_backward_table(xm, dym, w)
+        torch.cuda.synchronize()
+        assert torch.equal(dx, dxm) and torch.equal(dt, dtm) and torch.equal(dt_s, dtm2)
+    torch.cuda.synchronize()
+    assert torch.equal(dt, dt_s)
+    check({"dx": to_f64(dx), "dt": to_f64(dt)}, run_oracle(d, w, ("dx", "dt")), dtype, "tiled %s %s" % (dtype, shape))
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("w", list(range(1, 17)))
 def test_fused_backward_every_window_size(w, dtype):
