@@ -1363,14 +1363,23 @@ __device__ __attribute__((always_inline)) inline void dt_finish(const f32x4 (&ac
   // offset (dh, dw) in a fixed order
   const bool single = a.tiles_per_ch == 1;
   for (int k = tid; k < K2; k += kThreads) {
-    const int dhi = k / K1;
-    const int dwi = k - dhi * K1;
-    const int dh = dhi - (WIN - 1);
     float s = 0.f;
-    for (int P = -(NPT - 1); P <= NPT - 1; ++P) {
-      const int da = dh - P * R;
-      if (da < -(R - 1) || da > R - 1) continue;
-      s += binsum[(P + NPT - 1) * NBT + (da + R - 1) * K1 + dwi];
+    if constexpr (R == 1) {
+      // one window row per tile: offset dh has the single bin of P = dh,
+      // stored at index k
+      s = binsum[k];
+    } else {
+      const int dhi = k / K1;
+      const int dwi = k - dhi * K1;
+      const int dh = dhi - (WIN - 1);
+      // the tiles P with |dh - P R| <= R - 1 (at most two), in increasing P
+      // floor(dh / R) .. floor((dh + R - 1) / R), numerators made positive
+      const int plo = (dh + R * WIN) / R - WIN;
+      const int phi = (dh + R - 1 + R * WIN) / R - WIN;
+      for (int P = plo; P <= phi; ++P) {
+        if (P < -(NPT - 1) || P > NPT - 1) continue;
+        s += binsum[(P + NPT - 1) * NBT + (dh - P * R + R - 1) * K1 + dwi];
+      }
     }
     if (single) {
       dt[c * K2 + k] = s;
