@@ -56,11 +56,11 @@ def parse():
 # on (sha256 of the kernel header); otherwise reported as null.
 TRAFFIC = {
     # (workload, kernel): measured bytes per dispatch (profiles/wbmm_traffic_*.txt)
-    ("bf16_b64_c192_28_w14", "bwd"): {"source": "ce1220a554221643", "bytes": 68084142},
-    ("bf16_b64_c192_28_w14", "fwd"): {"source": "ce1220a554221643", "bytes": 41074912},
-    ("bf16_b64_c192_28_w14", "dx"): {"source": "ce1220a554221643", "bytes": 41099426},
-    ("bf16_b64_c192_28_w14", "dt"): {"source": "ce1220a554221643", "bytes": 47518944},
-    ("bf16_b64_c96_56_w7", "fwd"): {"source": "ce1220a554221643", "bytes": 77428010},
+    ("bf16_b64_c192_28_w14", "bwd"): {"source": "6c40bfb75629c315", "bytes": 68624506},
+    ("bf16_b64_c192_28_w14", "fwd"): {"source": "6c40bfb75629c315", "bytes": 41349953},
+    ("bf16_b64_c192_28_w14", "dx"): {"source": "6c40bfb75629c315", "bytes": 41279024},
+    ("bf16_b64_c192_28_w14", "dt"): {"source": "6c40bfb75629c315", "bytes": 46896089},
+    ("bf16_b64_c96_56_w7", "fwd"): {"source": "6c40bfb75629c315", "bytes": 77504687},
 }
 
 
@@ -80,6 +80,25 @@ def image_layout(wl):
     if 16 % wpi == 0:
         return (wl.H * wl.W) % 8 == 0 and 2 * (16 // wpi) * wl.C * wl.H * wl.W < 2 ** 31
     return False
+
+
+def fixed_offset_rows(wl):
+    """Whether the gradient kernels address this workload's rows by fixed
+    offsets (see the kernel header): windows tile the map, NW a power of two
+    up to 16, 16-window sub-tiles are whole bands of one image or whole
+    images, and rows start on a dword (float32, or an even window)."""
+    if wl.H % wl.w or wl.W % wl.w or (wl.dtype != "f32" and wl.w % 2):
+        return False
+    nh, nw = wl.H // wl.w, wl.W // wl.w
+    if nw > 16 or nw & (nw - 1):
+        return False
+    es = 4 if wl.dtype == "f32" else 2
+    wpi = nh * nw
+    if wpi % 16 != 0 and 16 % wpi != 0:
+        return False
+    if 16 % wpi == 0 and wpi % 16 != 0 and 16 * wl.C * wl.H * wl.W * es >= 2 ** 31:
+        return False
+    return wl.w * wl.W * 16 * es < 2 ** 31
 
 
 def kernel_source_hash():
@@ -313,8 +332,9 @@ def main():
     ai = dom_flops / dom_bytes
     ridge = peak * 1e12 / (HBM_PEAK_GBS * 1e9)
     fk = "wbmm_fwd_img_kernel" if image_layout(wl) else "wbmm_fwd_kernel"
+    tl = "true" if fixed_offset_rows(wl) else "false"
     kernel_name = {"fwd": fk + "<%s,%d,false>", "dx": fk + "<%s,%d,true>",
-                   "dt": "wbmm_dt_kernel<%s,%d>", "bwd": "wbmm_bwd_kernel<%s,%d>",
+                   "dt": "wbmm_dt_kernel<%s,%d," + tl + ">", "bwd": "wbmm_bwd_kernel<%s,%d," + tl + ">",
                    "hfwd": "wbmm_fwd_kernel<%s,%d,false,true>",
                    "hbwd": "wbmm_hier_backward (3 launches) <%s,%d>"}[dom] % ({"bf16": "TagBF16", "f16": "TagF16",
                                                           "f32": "TagF32"}[wl.dtype], wl.w)

@@ -339,7 +339,7 @@ struct FwdCfg {
   static constexpr int LDSW = Tag::W16 ? KP + 8 : KP + ((4 - KP) % 64 + 64) % 64;
   static constexpr int K1 = 2 * WIN - 1;
   static constexpr int K2 = K1 * K1;
-  static constexpr int TS_LEN = rup(K2, 8);
+  static constexpr int TS_LEN = rup(K2 + 9, 8);       // + the overrun of tb_chunk's dword reads
   static constexpr int TB_LEN = Tag::W16 ? K1 * RP * RP : 0;
   // hierarchical form (WIN = 2 wl): the local table of the wl x wl
   // sub-windows and its Toeplitz blocks
@@ -453,6 +453,28 @@ __device__ __attribute__((always_inline)) inline void store_sub(const KArgs &a, 
   }
 }
 
+// One 8-element chunk of a row of the Toeplitz blocks: table entries
+// k0 + xi for xi = xi0 .. xi0 + 7, zero where xi >= WIN.  Read as five dwords
+// of the table copy in LDS (4-byte aligned, padded past its end) and shifted
+// by one element when k0 + xi0 is odd.
+template <int WIN>
+__device__ __attribute__((always_inline)) inline u16x8 tb_chunk(const u16 *Ts, int k0, int xi0) {
+  const int kb = k0 + xi0;
+  const uint32_t *p = reinterpret_cast<const uint32_t *>(Ts) + (kb >> 1);
+  const uint32_t sh = (uint32_t)(kb & 1) * 16u;
+  uint32_t d[5];
+#pragma unroll
+  for (int i = 0; i < 5; ++i) d[i] = p[i];
+  uint32_t u[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t v = __builtin_amdgcn_alignbit(d[i + 1], d[i], sh);
+    const int xa = xi0 + 2 * i;
+    u[i] = xa >= WIN ? 0u : (xa + 1 >= WIN ? (v & 0xffffu) : v);
+  }
+  return __builtin_bit_cast(u16x8, make_uint4(u[0], u[1], u[2], u[3]));
+}
+
 // The table row of channel c (read back to front for the input gradient)
 // -> Ts with coalesced loads; for 16-bit, the Toeplitz blocks
 // TB[dh][x_out][x_in] of M_c gathered from it.  The hierarchical form also
@@ -484,15 +506,7 @@ __device__ __attribute__((always_inline)) inline void fwd_tables(const typename 
       const int dhi = row / RP;
       const int xo = row - dhi * RP;
       u16x8 v = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
-      if (xo < WIN) {
-        const int k0 = dhi * K1 - xo + WIN - 1;  // table index of x_in = 0
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int xi = xi0 + e < WIN ? xi0 + e : WIN - 1;
-          const u16 t = Ts[k0 + xi];
-          v[e] = xi0 + e < WIN ? t : (u16)0;
-        }
-      }
+      if (xo < WIN) v = tb_chunk<WIN>(Ts, dhi * K1 - xo + WIN - 1, xi0);  // table index of x_in = 0
       *reinterpret_cast<u16x8 *>(&TB[row * RP + xi0]) = v;
     }
     if constexpr (HIER) {
@@ -1664,15 +1678,7 @@ __device__ __attribute__((always_inline)) void bwd_wave(const typename Tag::S *_
         const int dhi = row / RP;
         const int xo = row - dhi * RP;
         u16x8 v = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
-        if (xo < WIN) {
-          const int k0 = dhi * K1 - xo + WIN - 1;  // table index of x_in = 0
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const int xi = xi0 + e < WIN ? xi0 + e : WIN - 1;
-            const u16 t = Ts[k0 + xi];
-            v[e] = xi0 + e < WIN ? t : (u16)0;
-          }
-        }
+        if (xo < WIN) v = tb_chunk<WIN>(Ts, dhi * K1 - xo + WIN - 1, xi0);  // table index of x_in = 0
         *reinterpret_cast<u16x8 *>(&TB[row * RP + xi0]) = v;
       }
     }
