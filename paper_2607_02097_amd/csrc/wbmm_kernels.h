@@ -227,6 +227,20 @@ __device__ __attribute__((always_inline)) inline uint32_t tiled_row_off(const KA
          (uint32_t)((((vv & mw) >> a.lgnw) * a.BE + (vv & nwm) * WIN + hi * (int)a.W) * ES);
 }
 
+// Fixed-offset row hi of window m0 + vv (m0 a multiple of 16, vv < 16) as a
+// whole dword-aligned row.
+template <int WIN, int ES>
+__device__ __attribute__((always_inline)) inline Row<WIN, ES> tiled_row(const KArgs &a, int64_t c, int64_t m0, int vv, int hi) {
+  Row<WIN, ES> r;
+  const int nwm = (1 << a.lgnw) - 1, mw = (1 << a.lgw) - 1;
+  r.eoff = tiled_sub_base(a, c, m0) + (int64_t)(vv >> a.lgw) * a.chw +
+           (int64_t)(((vv & mw) >> a.lgnw) * a.BE + (vv & nwm) * WIN + hi * (int)a.W);
+  r.cols = WIN;
+  r.mode = kDword;
+  r.odd = 0;
+  return r;
+}
+
 // Dwords of one padded row (RP elements) in registers.
 template <int WIN, int ES>
 struct RowData {
@@ -398,7 +412,7 @@ struct SubRows {
   RowData<WIN, Tag::ES> rd[PER_LANE];
 };
 
-template <class Tag, int WIN>
+template <class Tag, int WIN, bool TILED>
 __device__ __attribute__((always_inline)) inline void load_sub(const KArgs &a, const void *x, int64_t c, int64_t m0, int nwin, int lane,
                                 SubRows<Tag, WIN> &o) {
   constexpr int KR = FwdCfg<Tag, WIN>::KR;
@@ -409,7 +423,11 @@ __device__ __attribute__((always_inline)) inline void load_sub(const KArgs &a, c
     const int hi = q - v * KR;
     Row<WIN, Tag::ES> r;
     r.cols = 0; r.eoff = 0; r.mode = kNone; r.odd = 0;
-    if (q < SubRows<Tag, WIN>::N && v < nwin) r = row_of<WIN, Tag::ES>(a, x, c, m0 + v, hi);
+    if constexpr (TILED) {
+      if (q < SubRows<Tag, WIN>::N && v < nwin && hi < WIN) r = tiled_row<WIN, Tag::ES>(a, c, m0, v, hi);
+    } else if (q < SubRows<Tag, WIN>::N && v < nwin) {
+      r = row_of<WIN, Tag::ES>(a, x, c, m0 + v, hi);
+    }
     load_row<WIN, Tag::ES>(x, r, o.rd[k]);
   }
 }
@@ -431,7 +449,7 @@ __device__ __attribute__((always_inline)) inline void write_sub(unsigned char *b
   }
 }
 
-template <class Tag, int WIN>
+template <class Tag, int WIN, bool TILED>
 __device__ __attribute__((always_inline)) inline void store_sub(const KArgs &a, void *y, int64_t c, int64_t m0, int nwin, int lane,
                                  const unsigned char *buf) {
   typedef FwdCfg<Tag, WIN> G;
@@ -440,7 +458,7 @@ __device__ __attribute__((always_inline)) inline void store_sub(const KArgs &a, 
     const int v = q / WIN;
     const int hi = q - v * WIN;
     if (v >= nwin) break;
-    const Row<WIN, Tag::ES> r = row_of<WIN, Tag::ES>(a, y, c, m0 + v, hi);
+    const Row<WIN, Tag::ES> r = TILED ? tiled_row<WIN, Tag::ES>(a, c, m0, v, hi) : row_of<WIN, Tag::ES>(a, y, c, m0 + v, hi);
     if (r.mode == kNone) continue;
     const uint32_t *l4 = reinterpret_cast<const uint32_t *>(buf + (v * G::LDSW + hi * G::RP) * Tag::ES);
     uint32_t d[RD::ND];
@@ -570,7 +588,7 @@ __device__ __attribute__((always_inline)) inline typename Tag::Frag fwd_lfrag(co
   return same ? f : typename Tag::Frag{0, 0, 0, 0, 0, 0, 0, 0};
 }
 
-template <class Tag, int WIN, bool REV, bool HIER = false>
+template <class Tag, int WIN, bool REV, bool HIER = false, bool TILED = false>
 __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename Tag::S *__restrict__ x,
                                                                   const typename Tag::S *__restrict__ tab,
                                                                   const typename Tag::S *__restrict__ tabl,
@@ -605,7 +623,7 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
   // ---- 1. first sub-tile's rows in flight; the table (Toeplitz blocks of
   //         M_c for 16-bit, the table itself for float32) -> LDS
   SubRows<Tag, WIN> nxt;
-  if (nsub > 0) load_sub<Tag, WIN>(a, x, c, n0 + first * 16, nwin - first * 16, lane, nxt);
+  if (nsub > 0) load_sub<Tag, WIN, TILED>(a, x, c, n0 + first * 16, nwin - first * 16, lane, nxt);
   fwd_tables<Tag, WIN, REV, HIER>(tab, tabl, c, Ts, TB, Tsl, TBL, tid);
 
   const int g = lane >> 4;   // lane group
@@ -618,7 +636,7 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
       const int64_t m0 = n0 + (first + j) * 16;
       const int mw = nwin - (first + j) * 16;  // windows left from m0
       write_sub<Tag, WIN>(buf, lane, nxt);
-      if (j + 1 < nsub) load_sub<Tag, WIN>(a, x, c, m0 + 16, mw - 16, lane, nxt);
+      if (j + 1 < nsub) load_sub<Tag, WIN, TILED>(a, x, c, m0 + 16, mw - 16, lane, nxt);
       Frag af[S_];
 #pragma unroll
       for (int s = 0; s < S_; ++s)
@@ -681,7 +699,8 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
           const int v = lane & 15;
           const int hr = t0 * RPT + (lane >> 4);
           if ((lane >> 4) < 2 * RPT && hr < WIN && v < mw) {
-            const Row<WIN, Tag::ES> r = row_of<WIN, Tag::ES>(a, y, c, m0 + v, hr);
+            const Row<WIN, Tag::ES> r =
+                TILED ? tiled_row<WIN, Tag::ES>(a, c, m0, v, hr) : row_of<WIN, Tag::ES>(a, y, c, m0 + v, hr);
             if (r.mode != kNone) {
               const uint32_t *l4 = reinterpret_cast<const uint32_t *>(buf + (v * LDSW + hr * RP) * Tag::ES);
               uint32_t dd[RowData<WIN, Tag::ES>::ND];
@@ -695,7 +714,7 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
           }
         }
       }
-      if constexpr (RP != 8) store_sub<Tag, WIN>(a, y, c, m0, mw, lane, buf);
+      if constexpr (RP != 8) store_sub<Tag, WIN, TILED>(a, y, c, m0, mw, lane, buf);
     }
   } else {
     constexpr int S_ = G::S, NT = G::NT;
@@ -703,7 +722,7 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
       const int64_t m0 = n0 + (first + j) * 16;
       const int mw = nwin - (first + j) * 16;
       write_sub<Tag, WIN>(buf, lane, nxt);
-      if (j + 1 < nsub) load_sub<Tag, WIN>(a, x, c, m0 + 16, mw - 16, lane, nxt);
+      if (j + 1 < nsub) load_sub<Tag, WIN, TILED>(a, x, c, m0 + 16, mw - 16, lane, nxt);
       float af[S_];
 #pragma unroll
       for (int s = 0; s < S_; ++s) af[s] = rowp[ln * LDSW + 4 * s + g];
@@ -733,7 +752,7 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
         }
         outq[4 * t] = float4{acc[0], acc[1], acc[2], acc[3]};
       }
-      store_sub<Tag, WIN>(a, y, c, m0, mw, lane, buf);
+      store_sub<Tag, WIN, TILED>(a, y, c, m0, mw, lane, buf);
     }
   }
 }
@@ -1827,6 +1846,18 @@ static hipError_t run_forward(const void *x, const void *t, void *y, const Geom 
   // float32 windows of 13 and more take up to 70 KB (LDS is reached with ds
   // instructions only)
   static_assert(lds <= 160 * 1024, "workgroup LDS above the 160 KB of a compute unit");
+  if constexpr (Tag::ES == 4 || WIN % 2 == 0) {
+    set_tiled<WIN, Tag::ES>(g, a, {x, y});
+    if (a.tiled) {
+      if (rev)
+        wbmm_fwd_kernel<Tag, WIN, true, false, true><<<grid, dim3(kFwdThreads), lds, st>>>((const S *)x, (const S *)t, nullptr,
+                                                                                          (S *)y, a);
+      else
+        wbmm_fwd_kernel<Tag, WIN, false, false, true><<<grid, dim3(kFwdThreads), lds, st>>>((const S *)x, (const S *)t, nullptr,
+                                                                                           (S *)y, a);
+      return hipGetLastError();
+    }
+  }
   if (rev)
     wbmm_fwd_kernel<Tag, WIN, true><<<grid, dim3(kFwdThreads), lds, st>>>((const S *)x, (const S *)t, nullptr, (S *)y, a);
   else

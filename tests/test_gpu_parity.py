@@ -128,25 +128,30 @@ TILED = [
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("shape", TILED, ids=lambda s: "B%dC%dH%dW%dw%d" % s)
 def test_fixed_offset_rows_backward(shape, dtype):
-    """Gradients on tensors whose rows the kernels address by fixed offsets
-    equal those on misaligned copies (generic row addressing) bit for bit, and
-    the oracle within tolerance."""
+    """Forward and gradients on tensors whose rows the kernels address by
+    fixed offsets equal those on misaligned copies (generic row addressing)
+    bit for bit, and the oracle within tolerance."""
     B, C, H, Wd, w = shape
     d = draw(B, C, H, Wd, w, dtype, seed=31)
     x, t, dy = (to_device(d[k], dtype) for k in ("x", "t", "dy"))
     dx, dt = W.wbmm_backward(x, dy, t, w)
     dt_s = W.wbmm_backward_table(x, dy, w)
+    y = W.wbmm_forward(x, t, w)
     if dtype != "f32":
         xm, dym = misaligned_like(x), misaligned_like(dy)
         dxm = misaligned_like(torch.zeros_like(dy))
+        ym = misaligned_like(torch.zeros_like(x))
         dtm = torch.empty_like(dt)
         W.wbmm_backward(xm, dym, t, w, dx=dxm, dtable=dtm)
         dtm2 = W.wbmm_backward_table(xm, dym, w)
+        W.wbmm_forward(xm, t, w, out=ym)
         torch.cuda.synchronize()
         assert torch.equal(dx, dxm) and torch.equal(dt, dtm) and torch.equal(dt_s, dtm2)
+        assert torch.equal(y, ym)
     torch.cuda.synchronize()
     assert torch.equal(dt, dt_s)
-    check({"dx": to_f64(dx), "dt": to_f64(dt)}, run_oracle(d, w, ("dx", "dt")), dtype, "tiled %s %s" % (dtype, shape))
+    check({"fwd": to_f64(y), "dx": to_f64(dx), "dt": to_f64(dt)}, run_oracle(d, w, ("fwd", "dx", "dt")), dtype,
+          "tiled %s %s" % (dtype, shape))
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
