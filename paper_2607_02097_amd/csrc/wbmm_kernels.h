@@ -1105,7 +1105,7 @@ struct PSpan {
 
 template <class G>
 __host__ __device__ constexpr size_t bins_lds_bytes() {
-  return (size_t)(kWaves * max_tiles_per_wave<G::NPT>() * 16 * 17 + G::NACC * G::NBT) * 4;
+  return (size_t)(kWaves * max_tiles_per_wave<G::NPT>() * 272 + G::NACC * G::NBT) * 4;
 }
 
 template <class Tag, int WIN>
@@ -1321,22 +1321,26 @@ __device__ __attribute__((always_inline)) inline void dt_finish(const f32x4 (&ac
   // issues the reads of all its bins at once (out-of-range terms read a valid
   // slot and are masked to zero).
   constexpr int NPM = max_tiles_per_wave<NPT>();
-  float *scr = reinterpret_cast<float *>(smem) + WAVE * NPM * 272;
-  float *binsum = reinterpret_cast<float *>(smem) + kWaves * NPM * 272;
+  constexpr int TSTR = 272;  // floats per tile (16 rows of 17, or of 16 for one-row tiles)
+  float *scr = reinterpret_cast<float *>(smem) + WAVE * NPM * TSTR;
+  float *binsum = reinterpret_cast<float *>(smem) + kWaves * NPM * TSTR;
   if constexpr (R == 1) {
     // One window row per tile (RP = 16): a bin is one diagonal dw = xi - xo
     // of the 16 x 16 tile.  The tile is written skewed, element (xi, xo) at
     // column (xo - xi) mod 16 of row xi, so that column s holds diagonal -s
     // in rows 0 .. 15-s and diagonal 16-s in the rows below; a lane sums one
     // column of one tile, top to bottom (the order of the general path).
-    // Pad positions (xi or xo >= WIN) are written as zero.
+    // Pad positions (xi or xo >= WIN) are written as zero.  Row xi is
+    // stored at row 4 (xi / 4) + (xi + xi / 4) % 4 (pitch 16), so that the
+    // four 16-lane groups of a write (xi = 4 g + rr) fall on four different
+    // 16-bank groups.
 #pragma unroll
     for (int rr = 0; rr < 4; ++rr) {
       const int xi = 4 * g + rr;
-      float *row = scr + xi * 16 + ((ln - xi) & 15);
+      float *row = scr + (4 * g + ((rr + g) & 3)) * 16 + ((ln - xi) & 15);
       const bool ok = xi < WIN && ln < WIN;
 #pragma unroll
-      for (int j = 0; j < NP; ++j) row[j * 272] = ok ? acc[j][rr] : 0.f;
+      for (int j = 0; j < NP; ++j) row[j * TSTR] = ok ? acc[j][rr] : 0.f;
     }
     wave_lds_sync();
     const int s = lane & 15;
@@ -1344,11 +1348,11 @@ __device__ __attribute__((always_inline)) inline void dt_finish(const f32x4 (&ac
     for (int it = 0; it < cdiv(NP * 16, 64); ++it) {
       const int j = (lane >> 4) + 4 * it;
       if (j < NP) {
-        const float *col = scr + j * 272 + s;
+        const float *col = scr + j * TSTR + s;
         float lo = 0.f, hi = 0.f;
 #pragma unroll
         for (int xi = 0; xi < 16; ++xi) {
-          const float v = col[xi * 16];
+          const float v = col[((xi & ~3) + ((xi + (xi >> 2)) & 3)) * 16];
           const bool upper = xi + s <= 15;
           lo += upper ? v : 0.f;
           hi += upper ? 0.f : v;
@@ -1362,7 +1366,7 @@ __device__ __attribute__((always_inline)) inline void dt_finish(const f32x4 (&ac
 #pragma unroll
     for (int j = 0; j < NP; ++j) {
 #pragma unroll
-      for (int rr = 0; rr < 4; ++rr) scr[j * 272 + (4 * g + rr) * 17 + ln] = acc[j][rr];
+      for (int rr = 0; rr < 4; ++rr) scr[j * TSTR + (4 * g + rr) * 17 + ln] = acc[j][rr];
     }
     wave_lds_sync();
 #pragma unroll
@@ -1373,7 +1377,7 @@ __device__ __attribute__((always_inline)) inline void dt_finish(const f32x4 (&ac
         const int bin = b2 - j * NBT;
         const int da = bin / K1 - (R - 1);  // input sub-row minus output sub-row
         const int dw = bin - (bin / K1) * K1 - (WIN - 1);
-        const float *t = scr + j * 272;
+        const float *t = scr + j * TSTR;
         float sum = 0.f;
 #pragma unroll
         for (int ra = 0; ra < R; ++ra) {
