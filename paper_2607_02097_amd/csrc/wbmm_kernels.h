@@ -51,6 +51,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
 #include <initializer_list>
 
 #include "wbmm_internal.h"
@@ -1300,20 +1301,18 @@ __device__ __attribute__((always_inline)) inline void dt_products(const unsigned
 // bins, then the slab's dT; with several slabs per channel the channel's
 // last workgroup sums the partials.  Starts with a workgroup barrier (the
 // bins reuse the LDS of the stages).
+// Diagonal binning of one wave's accumulator tiles into the bins at the
+// end of the scratch (LDS of the stages); no workgroup barrier inside.
 template <class Tag, int WIN, class G, int WAVE>
-__device__ __attribute__((always_inline)) inline void dt_finish(const f32x4 (&acc)[PSpan<G::NPT, WAVE>::na],
-                                                                 unsigned char *smem, float *__restrict__ dt,
-                                                                 float *__restrict__ part, unsigned *__restrict__ cnt,
-                                                                 const KArgs &a, int64_t c, int64_t slab) {
+__device__ __attribute__((always_inline)) inline void dt_bin(const f32x4 (&acc)[PSpan<G::NPT, WAVE>::na],
+                                                              unsigned char *smem) {
   typedef PSpan<G::NPT, WAVE> SP;
   constexpr int NPT = G::NPT, RP = G::RP, R = G::R;
-  constexpr int K1 = G::K1, K2 = G::K2, NBT = G::NBT;
+  constexpr int K1 = G::K1, NBT = G::NBT;
   constexpr int PLO = SP::lo, NP = SP::np;
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
+  const int lane = threadIdx.x & 63;
   const int g = lane >> 4;
   const int ln = lane & 15;
-  __syncthreads();
 
   // ---- diagonal binning, fixed order.  Every tile of the wave goes to LDS
   // at once; bin (da, dw) of tile P sums the elements
@@ -1395,11 +1394,25 @@ __device__ __attribute__((always_inline)) inline void dt_finish(const f32x4 (&ac
       }
     }
   }
-  __syncthreads();
+}
+
+// This slab's table gradient from the bins (a fixed-order combine); with
+// several slabs per channel the channel's last workgroup sums the partials.
+// NTH threads take part; starts after a workgroup barrier that follows the
+// binning.
+template <class Tag, int WIN, class G, int NTH>
+__device__ __attribute__((always_inline)) inline void dt_reduce(unsigned char *smem, float *__restrict__ dt,
+                                                                 float *__restrict__ part, unsigned *__restrict__ cnt,
+                                                                 const KArgs &a, int64_t c, int64_t slab) {
+  constexpr int NPT = G::NPT, R = G::R;
+  constexpr int K1 = G::K1, K2 = G::K2, NBT = G::NBT;
+  constexpr int NPM = max_tiles_per_wave<NPT>();
+  const int tid = threadIdx.x;
+  float *binsum = reinterpret_cast<float *>(smem) + kWaves * NPM * 272;
   // this slab's table gradient: combine the (P, sub-row offset) bins of each
   // offset (dh, dw) in a fixed order
   const bool single = a.tiles_per_ch == 1;
-  for (int k = tid; k < K2; k += kThreads) {
+  for (int k = tid; k < K2; k += NTH) {
     float s = 0.f;
     if constexpr (R == 1) {
       // one window row per tile: offset dh has the single bin of P = dh,
@@ -1443,7 +1456,7 @@ __device__ __attribute__((always_inline)) inline void dt_finish(const f32x4 (&ac
   if (*flag == 0) return;
   // all loads of a group of slabs are issued before the sums, which keep
   // the slab order
-  constexpr int KPT = cdiv(K2, kThreads);
+  constexpr int KPT = cdiv(K2, NTH);
   constexpr int SG = 8;
   float s[KPT];
 #pragma unroll
@@ -1452,7 +1465,7 @@ __device__ __attribute__((always_inline)) inline void dt_finish(const f32x4 (&ac
     float v[KPT][SG];
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
-      const int k = tid + i * kThreads;
+      const int k = tid + i * NTH;
 #pragma unroll
       for (int j = 0; j < SG; ++j)
         v[i][j] = (k < K2 && j0 + j < a.tiles_per_ch)
@@ -1468,10 +1481,21 @@ __device__ __attribute__((always_inline)) inline void dt_finish(const f32x4 (&ac
   }
 #pragma unroll
   for (int i = 0; i < KPT; ++i) {
-    const int k = tid + i * kThreads;
+    const int k = tid + i * NTH;
     if (k < K2) dt[c * K2 + k] = s[i];
   }
   if (tid == 0) __hip_atomic_store(&cnt[c], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <class Tag, int WIN, class G, int WAVE>
+__device__ __attribute__((always_inline)) inline void dt_finish(const f32x4 (&acc)[PSpan<G::NPT, WAVE>::na],
+                                                                 unsigned char *smem, float *__restrict__ dt,
+                                                                 float *__restrict__ part, unsigned *__restrict__ cnt,
+                                                                 const KArgs &a, int64_t c, int64_t slab) {
+  __syncthreads();
+  dt_bin<Tag, WIN, G, WAVE>(acc, smem);
+  __syncthreads();
+  dt_reduce<Tag, WIN, G, kThreads>(smem, dt, part, cnt, a, c, slab);
 }
 
 template <class Tag, int WIN, int WAVE, bool TILED>
@@ -1525,16 +1549,18 @@ __global__ __launch_bounds__(kThreads, 3) void wbmm_dt_kernel(const typename Tag
 // outermost (all its output tiles accumulate at once), each tile's sum over
 // K in the forward's order.  The rounded results go to Obuf (window-major,
 // the x stage, no longer read).
-template <class Tag, int WIN, int WAVE>
+template <class Tag, int WIN, int WAVE, int NDX = kWaves>
 __device__ __attribute__((always_inline)) inline void dx_products(const unsigned char *Dbuf, unsigned char *Obuf,
-                                                                   const unsigned char *smem, int lane) {
+                                                                   const typename Tag::S *Ts, const typename Tag::S *TB,
+                                                                   int lane) {
   typedef typename Tag::S S;
   typedef typename Tag::Frag Frag;
   typedef BwdCfg<Tag, WIN> G;
   typedef FwdCfg<Tag, WIN> F;
   constexpr int RP = G::RP, LDSW = G::LDSW, NT = F::NT, S_ = F::S, K1 = G::K1;
+  constexpr int WPS = NDX / G::SUBS;  // waves per sub-tile
   constexpr int SUB = WAVE % G::SUBS, PART = WAVE / G::SUBS;
-  constexpr int T0 = PART * NT / G::WPS, T1 = (PART + 1) * NT / G::WPS, NTW = T1 - T0;
+  constexpr int T0 = PART * NT / WPS, T1 = (PART + 1) * NT / WPS, NTW = T1 - T0;
   const int g = lane >> 4;
   const int ln = lane & 15;
   const S *rowp = reinterpret_cast<const S *>(Dbuf) + SUB * 16 * LDSW;
@@ -1545,7 +1571,6 @@ __device__ __attribute__((always_inline)) inline void dx_products(const unsigned
     for (int j = 0; j < NTW; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
     if constexpr (Tag::W16) {
       constexpr int NB = F::NB;
-      const S *TB = reinterpret_cast<const S *>(smem + G::TB_OFF);
       auto load_bf = [&](int q) -> Frag {
         const int d0 = q - (NT - 1);
         int dh, xi0;
@@ -1582,7 +1607,6 @@ __device__ __attribute__((always_inline)) inline void dx_products(const unsigned
         outp[3 * LDSW + 16 * t] = (u16)(hi >> 16);
       }
     } else {
-      const S *Ts = reinterpret_cast<const S *>(smem + G::TS_OFF);
 #pragma unroll
       for (int s = 0; s < S_; ++s) {
         const float af = rowp[ln * LDSW + 4 * s + g];
@@ -1714,7 +1738,8 @@ __device__ __attribute__((always_inline)) void bwd_wave(const typename Tag::S *_
     if (m0 + G::CW < s1) stage_load<Tag, WIN, G, TILED>(a, x, dy, c, m0 + G::CW, s1, tid, st);
     dt_products<Tag, G, WAVE>(Xt, Dt, acc, lane);
     __syncthreads();  // the x tile is no longer read
-    dx_products<Tag, WIN, WAVE>(Dt, Xt, smem, lane);
+    dx_products<Tag, WIN, WAVE>(Dt, Xt, reinterpret_cast<const S *>(smem + G::TS_OFF),
+                                reinterpret_cast<const S *>(smem + G::TB_OFF), lane);
     __syncthreads();
     dx_store<Tag, WIN, TILED>(a, dx, c, m0, s1, tid, Xt);
   }
@@ -1737,9 +1762,257 @@ __global__ __launch_bounds__(kThreads, (TILED ? 3 : 2)) void wbmm_bwd_kernel(con
   }
 }
 
+// ------------------------------------------ fused backward, channel stream
+// Fixed-offset rows, few channels per compute unit: one 12-wave workgroup
+// per (channel, slab) and at most one workgroup per compute unit, streaming
+// the slab's stages through double-buffered LDS (x and dy tiles, and the
+// input-gradient results) with one workgroup barrier per stage.  Waves 0-3
+// take the table-gradient products (the P ranges of the 4-wave kernel),
+// waves 4-11 the input-gradient products (four waves per 16-window
+// sub-tile); at any time every wave copies the next stage into LDS, the
+// stage after it into registers and the previous stage's dX rows to HBM.
+// Products, bins and sums are those of wbmm_bwd_kernel, so the results are
+// bitwise the same.
+constexpr int kStreamWaves = 12;
+constexpr int kStreamThreads = 64 * kStreamWaves;
+constexpr int kStreamDt = 4;  // table-gradient waves
+
+template <class Tag, int WIN>
+struct StreamCfg {
+  typedef BwdCfg<Tag, WIN> G;
+  typedef FwdCfg<Tag, WIN> F;
+  static constexpr int SUBS = G::SUBS;                     // 16-window sub-tiles per stage
+  static constexpr int NCP = 2 * SUBS;                     // row copies: (tensor, sub-tile)
+  static constexpr int WPC = kStreamWaves / NCP;           // waves per copy
+  static constexpr int RC = 16 * G::KR;                    // rows per copy
+  static constexpr int IT = cdiv(RC, WPC * 64);            // rows per thread and copy
+  static constexpr int STAGE = 2 * G::BUF;                 // x tile + dy tile
+  static constexpr int O_OFF = 2 * STAGE;                  // two dX result buffers of G::BUF
+  static constexpr int TS_OFF = O_OFF + 2 * G::BUF;
+  static constexpr int TB_OFF = TS_OFF + rup(F::TS_LEN * Tag::ES, 16);
+  static constexpr int END = TB_OFF + F::TB_LEN * Tag::ES;
+  static_assert(kStreamWaves % NCP == 0, "whole waves per copy");
+  static_assert(bins_lds_bytes<G>() <= O_OFF, "bins must not reach the dX buffers");
+};
+
+template <class Tag, int WIN>
+__host__ __device__ constexpr size_t stream_lds_bytes() {
+  return (size_t)StreamCfg<Tag, WIN>::END;
+}
+
+template <class Tag, int WIN>
+struct StreamRows {
+  RowData<WIN, Tag::ES> rd[StreamCfg<Tag, WIN>::IT];
+};
+
+// Rows of this wave's copy (tensor, sub-tile) of the stage at m0 -> registers.
+template <class Tag, int WIN>
+__device__ __attribute__((always_inline)) inline void stream_load(const KArgs &a, const typename Tag::S *x,
+                                                                   const typename Tag::S *dy, int64_t c, int64_t m0,
+                                                                   int64_t m1, int wave, int lane,
+                                                                   StreamRows<Tag, WIN> &st) {
+  typedef StreamCfg<Tag, WIN> SC;
+  typedef BwdCfg<Tag, WIN> G;
+  constexpr int NDV = (WIN * Tag::ES) / 4;
+  const int cp = wave / SC::WPC;
+  const int tens = cp / SC::SUBS, sub = cp % SC::SUBS;
+  const int64_t ms = m0 + 16 * sub;
+  const char *base = reinterpret_cast<const char *>((tens ? dy : x) + tiled_sub_base(a, c, ms));
+#pragma unroll
+  for (int k = 0; k < SC::IT; ++k) {
+    const int t = (wave % SC::WPC) * 64 + lane + k * SC::WPC * 64;
+    const int vv = t / G::KR;
+    const int hi = t - vv * G::KR;
+#pragma unroll
+    for (int i = 0; i < RowData<WIN, Tag::ES>::ND; ++i) st.rd[k].d[i] = 0;
+    if (t < SC::RC && hi < WIN && ms + vv < m1) {
+      const uint32_t *p4 = reinterpret_cast<const uint32_t *>(base + tiled_row_off<WIN, Tag::ES>(a, vv, hi));
+#pragma unroll
+      for (int i = 0; i + 4 <= NDV; i += 4) {
+        const u32x4a u = *reinterpret_cast<const u32x4a *>(p4 + i);
+        st.rd[k].d[i] = u.x; st.rd[k].d[i + 1] = u.y; st.rd[k].d[i + 2] = u.z; st.rd[k].d[i + 3] = u.w;
+      }
+#pragma unroll
+      for (int i = NDV & ~3; i < NDV; ++i) st.rd[k].d[i] = p4[i];
+    }
+  }
+}
+
+// The loaded rows -> window-major padded rows of one stage buffer.
+template <class Tag, int WIN>
+__device__ __attribute__((always_inline)) inline void stream_write(unsigned char *stage, int wave, int lane,
+                                                                    const StreamRows<Tag, WIN> &st) {
+  typedef StreamCfg<Tag, WIN> SC;
+  typedef BwdCfg<Tag, WIN> G;
+  typedef RowData<WIN, Tag::ES> RD;
+  const int cp = wave / SC::WPC;
+  const int tens = cp / SC::SUBS, sub = cp % SC::SUBS;
+#pragma unroll
+  for (int k = 0; k < SC::IT; ++k) {
+    const int t = (wave % SC::WPC) * 64 + lane + k * SC::WPC * 64;
+    const int vv = t / G::KR;
+    const int hi = t - vv * G::KR;
+    if (t < SC::RC) {
+      uint32_t *l4 = reinterpret_cast<uint32_t *>(stage + tens * G::BUF + ((16 * sub + vv) * G::LDSW + hi * G::RP) * Tag::ES);
+#pragma unroll
+      for (int i = 0; i < RD::ND; i += 4)
+        *reinterpret_cast<uint4 *>(l4 + i) = make_uint4(st.rd[k].d[i], st.rd[k].d[i + 1], st.rd[k].d[i + 2], st.rd[k].d[i + 3]);
+    }
+  }
+}
+
+// The dX rows of the stage at m0 (window-major in Obuf) -> dx.
+template <class Tag, int WIN>
+__device__ __attribute__((always_inline)) inline void stream_store(const KArgs &a, typename Tag::S *dx, int64_t c,
+                                                                    int64_t m0, int64_t m1, int tid,
+                                                                    const unsigned char *Obuf) {
+  typedef BwdCfg<Tag, WIN> G;
+  constexpr int NDV = (WIN * Tag::ES) / 4, RS = 16 * WIN;  // rows per sub-tile
+#pragma unroll
+  for (int k = 0; k < cdiv(G::SUBS * RS, kStreamThreads); ++k) {
+    const int q = tid + k * kStreamThreads;
+    const int sub = q / RS;
+    const int r = q - sub * RS;
+    const int vv = r / WIN;
+    const int hi = r - vv * WIN;
+    const int64_t ms = m0 + 16 * sub;
+    if (q < G::SUBS * RS && ms + vv < m1) {
+      const uint32_t *l4 = reinterpret_cast<const uint32_t *>(Obuf + ((16 * sub + vv) * G::LDSW + hi * G::RP) * Tag::ES);
+      uint32_t *p4 = reinterpret_cast<uint32_t *>(reinterpret_cast<char *>(dx + tiled_sub_base(a, c, ms)) +
+                                                  tiled_row_off<WIN, Tag::ES>(a, vv, hi));
+#pragma unroll
+      for (int i = 0; i + 4 <= NDV; i += 4) {
+        const uint4 u = *reinterpret_cast<const uint4 *>(l4 + i);
+        *reinterpret_cast<u32x4a *>(p4 + i) = u32x4a{u.x, u.y, u.z, u.w};
+      }
+#pragma unroll
+      for (int i = NDV & ~3; i < NDV; ++i) p4[i] = l4[i];
+    }
+  }
+}
+
+// One wave of the stream kernel: DTW >= 0 is a table-gradient wave (its P
+// range), else DXW >= 0 an input-gradient wave (idle but for the copies
+// when DX is false: the table gradient alone, with the same stages, bins and
+// sums as the fused pass).
+template <class Tag, int WIN, int DTW, int DXW, bool DX>
+__device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S *__restrict__ x,
+                                                           const typename Tag::S *__restrict__ dy,
+                                                           const typename Tag::S *__restrict__ tab,
+                                                           typename Tag::S *__restrict__ dx, float *__restrict__ dt,
+                                                           float *__restrict__ part, unsigned *__restrict__ cnt,
+                                                           const KArgs &a, unsigned char *smem) {
+  typedef typename Tag::S S;
+  typedef StreamCfg<Tag, WIN> SC;
+  typedef BwdCfg<Tag, WIN> G;
+  typedef PSpan<G::NPT, (DTW >= 0 ? DTW : 0)> SP;
+  constexpr int RP = G::RP, K1 = G::K1, K2 = G::K2, CW = G::CW;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int64_t c = blockIdx.x / a.tiles_per_ch;
+  const int64_t slab = blockIdx.x - c * a.tiles_per_ch;
+  const int64_t s0 = slab * a.tile;
+  const int64_t s1 = (s0 + a.tile < a.N) ? s0 + a.tile : a.N;
+  const int nst = (int)((s1 - s0 + CW - 1) / CW);
+  S *Ts = reinterpret_cast<S *>(smem + SC::TS_OFF);
+  S *TB = reinterpret_cast<S *>(smem + SC::TB_OFF);
+
+  f32x4 acc[SP::na];
+#pragma unroll
+  for (int j = 0; j < SP::na; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // stage 0 in flight; the reversed table row and (16-bit) its Toeplitz
+  // blocks -> LDS; stage 0 -> LDS buffer 0, stage 1 in flight
+  StreamRows<Tag, WIN> st;
+  stream_load<Tag, WIN>(a, x, dy, c, s0, s1, wave, lane, st);
+  if constexpr (DX) {
+    const S *tc = tab + c * K2;
+    for (int k = tid; k < K2; k += kStreamThreads) Ts[k] = tc[K2 - 1 - k];
+    __syncthreads();
+    if constexpr (Tag::W16) {
+      constexpr int CPR = RP / 8;
+      constexpr int NCH = K1 * RP * CPR;
+      for (int ch = tid; ch < NCH; ch += kStreamThreads) {
+        const int row = ch / CPR;  // = dhi * RP + x_out
+        const int xi0 = (ch - row * CPR) * 8;
+        const int dhi = row / RP;
+        const int xo = row - dhi * RP;
+        u16x8 v = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+        if (xo < WIN) v = tb_chunk<WIN>(Ts, dhi * K1 - xo + WIN - 1, xi0);  // table index of x_in = 0
+        *reinterpret_cast<u16x8 *>(&TB[row * RP + xi0]) = v;
+      }
+    }
+  }
+  stream_write<Tag, WIN>(smem, wave, lane, st);
+  if (nst > 1) stream_load<Tag, WIN>(a, x, dy, c, s0 + CW, s1, wave, lane, st);
+  __syncthreads();
+
+  for (int s = 0; s < nst; ++s) {
+    const int64_t m0 = s0 + (int64_t)s * CW;
+    unsigned char *cur = smem + (s & 1) * SC::STAGE;
+    unsigned char *obuf = smem + SC::O_OFF + (s & 1) * G::BUF;
+    // this stage's products
+    if constexpr (DTW >= 0) {
+      dt_products<Tag, G, DTW>(cur, cur + G::BUF, acc, lane);
+    } else if constexpr (DX) {
+      dx_products<Tag, WIN, DXW, kStreamWaves - kStreamDt>(cur + G::BUF, obuf, Ts, TB, lane);
+    }
+    // the next stage into the other buffer (free since the last barrier),
+    // the one after it in flight, the previous stage's dX rows out
+    if (s + 1 < nst) stream_write<Tag, WIN>(smem + ((s + 1) & 1) * SC::STAGE, wave, lane, st);
+    if (s + 2 < nst) stream_load<Tag, WIN>(a, x, dy, c, m0 + 2 * CW, s1, wave, lane, st);
+    if (DX && s > 0) stream_store<Tag, WIN>(a, dx, c, m0 - CW, s1, tid, smem + SC::O_OFF + ((s - 1) & 1) * G::BUF);
+    __syncthreads();
+  }
+  // the last stage's dX rows out while the table-gradient waves bin their
+  // tiles (the bins lie below the dX buffers)
+  if constexpr (DX)
+    stream_store<Tag, WIN>(a, dx, c, s0 + (int64_t)(nst - 1) * CW, s1, tid,
+                           smem + SC::O_OFF + ((nst - 1) & 1) * G::BUF);
+  if constexpr (DTW >= 0) dt_bin<Tag, WIN, G, DTW>(acc, smem);
+  __syncthreads();
+  dt_reduce<Tag, WIN, G, kStreamThreads>(smem, dt, part, cnt, a, c, slab);
+}
+
+template <class Tag, int WIN, bool DX>
+__global__ __launch_bounds__(kStreamThreads, 3) void wbmm_bwd_stream_kernel(
+    const typename Tag::S *__restrict__ x, const typename Tag::S *__restrict__ dy,
+    const typename Tag::S *__restrict__ tab, typename Tag::S *__restrict__ dx, float *__restrict__ dt,
+    float *__restrict__ part, unsigned *__restrict__ cnt, KArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  switch (threadIdx.x >> 6) {
+    case 0: stream_wave<Tag, WIN, 0, -1, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
+    case 1: stream_wave<Tag, WIN, 1, -1, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
+    case 2: stream_wave<Tag, WIN, 2, -1, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
+    case 3: stream_wave<Tag, WIN, 3, -1, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
+    case 4: stream_wave<Tag, WIN, -1, 0, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
+    case 5: stream_wave<Tag, WIN, -1, 1, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
+    case 6: stream_wave<Tag, WIN, -1, 2, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
+    case 7: stream_wave<Tag, WIN, -1, 3, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
+    case 8: stream_wave<Tag, WIN, -1, 4, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
+    case 9: stream_wave<Tag, WIN, -1, 5, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
+    case 10: stream_wave<Tag, WIN, -1, 6, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
+    default: stream_wave<Tag, WIN, -1, 7, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
+  }
+}
+
 // ============================================================ host side
 
 static int64_t cdiv64(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Compute units of the current device (cached per device; 0 if unknown).
+static int compute_units() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  int n = cache[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    cache[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
 
 static KArgs make_args(const Geom &g) {
   KArgs a;
@@ -1911,6 +2184,24 @@ static DtPlan plan_dt(const Geom &g) {
 // followed by the per-slab partial sums.
 static size_t counter_bytes(int64_t C) { return (size_t)((C * 4 + 255) / 256 * 256); }
 
+// Launch plan of the channel-stream kernel (fixed-offset rows, no more
+// channels than compute units): one workgroup per (channel, slab), at most
+// one per compute unit.  Its slabs never outnumber those of plan_dt, which
+// sizes the workspace.
+template <class Tag, int WIN>
+static bool stream_plan(const Geom &g, KArgs &b) {
+  typedef BwdCfg<Tag, WIN> G;
+  const int ncu = compute_units();
+  if (!b.tiled || ncu <= 0 || g.C > ncu) return false;
+  const int64_t stages = cdiv64(g.N, G::CW);
+  int64_t slabs = ncu / g.C;
+  if (slabs > stages) slabs = stages;
+  if (slabs < 1) slabs = 1;
+  b.tile = (int)(cdiv64(cdiv64(g.N, slabs), G::CW) * G::CW);
+  b.tiles_per_ch = (int)cdiv64(g.N, b.tile);
+  return true;
+}
+
 template <class Tag, int WIN>
 static hipError_t run_dtable(const void *x, const void *dy, float *dt, void *ws, const Geom &g,
                              hipStream_t st) {
@@ -1920,6 +2211,18 @@ static hipError_t run_dtable(const void *x, const void *dy, float *dt, void *ws,
   a.tile = (int)p.slab_windows;
   a.tiles_per_ch = (int)p.slabs;
   set_tiled<WIN, Tag::ES>(g, a, {x, dy});
+  if constexpr (Tag::ES == 4 || WIN % 2 == 0) {
+    KArgs b = a;
+    if (stream_plan<Tag, WIN>(g, b)) {
+      // the same stages, bins and sums as the fused pass
+      unsigned *scnt = b.tiles_per_ch > 1 ? (unsigned *)ws : nullptr;
+      float *spart = b.tiles_per_ch > 1 ? (float *)((char *)ws + counter_bytes(g.C)) : nullptr;
+      constexpr size_t slds = stream_lds_bytes<Tag, WIN>();
+      wbmm_bwd_stream_kernel<Tag, WIN, false><<<dim3((unsigned)(g.C * b.tiles_per_ch)), dim3(kStreamThreads), slds, st>>>(
+          (const S *)x, (const S *)dy, nullptr, nullptr, dt, spart, scnt, b);
+      return hipGetLastError();
+    }
+  }
   unsigned *cnt = p.slabs > 1 ? (unsigned *)ws : nullptr;
   float *part = p.slabs > 1 ? (float *)((char *)ws + counter_bytes(g.C)) : nullptr;
   constexpr size_t lds = dt_lds_bytes<Tag, WIN>();
@@ -1944,6 +2247,18 @@ static hipError_t run_backward(const void *x, const void *dy, const void *t, voi
   a.tile = (int)p.slab_windows;
   a.tiles_per_ch = (int)p.slabs;
   set_tiled<WIN, Tag::ES>(g, a, {x, dy, dx});
+  if constexpr (Tag::ES == 4 || WIN % 2 == 0) {
+    KArgs b = a;
+    if (stream_plan<Tag, WIN>(g, b)) {
+      unsigned *scnt = b.tiles_per_ch > 1 ? (unsigned *)ws : nullptr;
+      float *spart = b.tiles_per_ch > 1 ? (float *)((char *)ws + counter_bytes(g.C)) : nullptr;
+      constexpr size_t slds = stream_lds_bytes<Tag, WIN>();
+      static_assert(slds <= 160 * 1024, "workgroup LDS above the 160 KB of a compute unit");
+      wbmm_bwd_stream_kernel<Tag, WIN, true><<<dim3((unsigned)(g.C * b.tiles_per_ch)), dim3(kStreamThreads), slds, st>>>(
+          (const S *)x, (const S *)dy, (const S *)t, (S *)dx, dt, spart, scnt, b);
+      return hipGetLastError();
+    }
+  }
   unsigned *cnt = p.slabs > 1 ? (unsigned *)ws : nullptr;
   float *part = p.slabs > 1 ? (float *)((char *)ws + counter_bytes(g.C)) : nullptr;
   constexpr size_t lds = bwd_lds_bytes<Tag, WIN>();

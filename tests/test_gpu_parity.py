@@ -146,8 +146,13 @@ def test_fixed_offset_rows_backward(shape, dtype):
         dtm2 = W.wbmm_backward_table(xm, dym, w)
         W.wbmm_forward(xm, t, w, out=ym)
         torch.cuda.synchronize()
-        assert torch.equal(dx, dxm) and torch.equal(dt, dtm) and torch.equal(dt_s, dtm2)
-        assert torch.equal(y, ym)
+        assert torch.equal(dx, dxm) and torch.equal(y, ym)
+        # few channels per compute unit: the fixed-offset gradients stream
+        # each channel through one workgroup, the generic kernels split it into
+        # slabs; the same products summed in another order
+        assert torch.equal(dtm, dtm2)
+        scale = float(dt.abs().max()) + 1e-30
+        assert float((dt - dtm).abs().max()) <= 1e-5 * scale
     torch.cuda.synchronize()
     assert torch.equal(dt, dt_s)
     check({"fwd": to_f64(y), "dx": to_f64(dx), "dt": to_f64(dt)}, run_oracle(d, w, ("fwd", "dx", "dt")), dtype,
@@ -400,7 +405,8 @@ def test_hip_graph_replay_matches_eager():
 
 def test_workspace_counters_reset_between_calls():
     """The table gradient leaves its per-channel counters at zero: one zeroed
-    workspace serves repeated calls and smaller shapes, bit for bit."""
+    workspace serves repeated calls and smaller shapes (bit for bit against a
+    fresh workspace)."""
     big = synth.WORKLOADS["bf16_b16_c64_112_w14"]
     d = synth.draw_workload(big, seed=5)
     x, dy = (to_device(d[k], "bf16") for k in ("x", "dy"))
@@ -416,8 +422,12 @@ def test_workspace_counters_reset_between_calls():
     assert int(counters.abs().sum()) == 0
     xs, dys = x[:, :48].contiguous(), dy[:, :48].contiguous()
     small = W.wbmm_backward_table(xs, dys, 14, workspace=ws)
+    fresh = W.wbmm_backward_table(xs, dys, 14, workspace=W.new_workspace(need))
     torch.cuda.synchronize()
-    assert torch.equal(small, ref[:48])
+    assert torch.equal(small, fresh)
+    # the slab split depends on the channel count: the same products, summed
+    # in another order
+    assert float((small - ref[:48]).abs().max()) <= 1e-5 * float(ref[:48].abs().max())
 
 
 # ------------------------------------------------------------- hierarchical
