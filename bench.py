@@ -56,11 +56,11 @@ def parse():
 # on (sha256 of the kernel header); otherwise reported as null.
 TRAFFIC = {
     # (workload, kernel): measured bytes per dispatch (profiles/wbmm_traffic_*.txt)
-    ("bf16_b64_c192_28_w14", "bwd"): {"source": "6c40bfb75629c315", "bytes": 68624506},
-    ("bf16_b64_c192_28_w14", "fwd"): {"source": "6c40bfb75629c315", "bytes": 41349953},
-    ("bf16_b64_c192_28_w14", "dx"): {"source": "6c40bfb75629c315", "bytes": 41279024},
-    ("bf16_b64_c192_28_w14", "dt"): {"source": "6c40bfb75629c315", "bytes": 46896089},
-    ("bf16_b64_c96_56_w7", "fwd"): {"source": "6c40bfb75629c315", "bytes": 77504687},
+    ("bf16_b64_c192_28_w14", "bwd"): {"source": "68edc0dce3f21244", "bytes": 62499909},
+    ("bf16_b64_c192_28_w14", "fwd"): {"source": "68edc0dce3f21244", "bytes": 41287283},
+    ("bf16_b64_c192_28_w14", "dx"): {"source": "68edc0dce3f21244", "bytes": 41295490},
+    ("bf16_b64_c192_28_w14", "dt"): {"source": "68edc0dce3f21244", "bytes": 42187714},
+    ("bf16_b64_c96_56_w7", "fwd"): {"source": "68edc0dce3f21244", "bytes": 77533511},
 }
 
 
@@ -333,8 +333,14 @@ def main():
     ridge = peak * 1e12 / (HBM_PEAK_GBS * 1e9)
     fk = "wbmm_fwd_img_kernel" if image_layout(wl) else "wbmm_fwd_kernel"
     tl = "true" if fixed_offset_rows(wl) else "false"
+    # channel-stream gradients: fixed-offset rows and no more channels than
+    # compute units (256 on MI355X)
+    stream = fixed_offset_rows(wl) and wl.C <= torch.cuda.get_device_properties(0).multi_processor_count
+    dtk = "wbmm_bwd_stream_kernel" if stream else "wbmm_dt_kernel"
+    bwk = "wbmm_bwd_stream_kernel" if stream else "wbmm_bwd_kernel"
     kernel_name = {"fwd": fk + "<%s,%d,false>", "dx": fk + "<%s,%d,true>",
-                   "dt": "wbmm_dt_kernel<%s,%d," + tl + ">", "bwd": "wbmm_bwd_kernel<%s,%d," + tl + ">",
+                   "dt": dtk + "<%s,%d," + ("false" if stream else tl) + ">",
+                   "bwd": bwk + "<%s,%d," + ("true" if stream else tl) + ">",
                    "hfwd": "wbmm_fwd_kernel<%s,%d,false,true>",
                    "hbwd": "wbmm_hier_backward (3 launches) <%s,%d>"}[dom] % ({"bf16": "TagBF16", "f16": "TagF16",
                                                           "f32": "TagF32"}[wl.dtype], wl.w)
