@@ -494,6 +494,42 @@ __device__ __attribute__((always_inline)) inline u16x8 tb_chunk(const u16 *Ts, i
   return __builtin_bit_cast(u16x8, make_uint4(u[0], u[1], u[2], u[3]));
 }
 
+// The table row of channel c (and the local table of the hierarchical form)
+// held in registers between the loads and their copy to LDS, so that the
+// loads can be issued before the bulk loads of the input rows instead of
+// queueing behind them.
+template <class Tag, int WIN, bool HIER, int NTH>
+struct TabRegs {
+  typedef FwdCfg<Tag, WIN> G;
+  static constexpr int N = cdiv(G::K2, NTH);
+  static constexpr int NL = HIER ? cdiv(G::K2L, NTH) : 1;
+  typename Tag::S v[N];
+  typename Tag::S vl[NL];
+};
+
+template <class Tag, int WIN, bool REV, bool HIER, int NTH>
+__device__ __attribute__((always_inline)) inline void tab_load(const typename Tag::S *__restrict__ tab,
+                                                                const typename Tag::S *__restrict__ tabl, int64_t c,
+                                                                int tid, TabRegs<Tag, WIN, HIER, NTH> &tr) {
+  typedef FwdCfg<Tag, WIN> G;
+  constexpr int K2 = G::K2;
+  const typename Tag::S *tc = tab + c * K2;
+#pragma unroll
+  for (int i = 0; i < tr.N; ++i) {
+    const int k = tid + i * NTH;
+    if (k < K2) tr.v[i] = tc[REV ? K2 - 1 - k : k];
+  }
+  if constexpr (HIER) {
+    constexpr int K2L = G::K2L;
+    const typename Tag::S *tl = tabl + c * K2L;
+#pragma unroll
+    for (int i = 0; i < tr.NL; ++i) {
+      const int k = tid + i * NTH;
+      if (k < K2L) tr.vl[i] = tl[REV ? K2L - 1 - k : k];
+    }
+  }
+}
+
 // The table row of channel c (read back to front for the input gradient)
 // -> Ts with coalesced loads; for 16-bit, the Toeplitz blocks
 // TB[dh][x_out][x_in] of M_c gathered from it.  The hierarchical form also
@@ -501,19 +537,24 @@ __device__ __attribute__((always_inline)) inline u16x8 tb_chunk(const u16 *Ts, i
 // TBL[dh][x_out][x_in], zero unless x_in and x_out lie in the same half of the
 // window (the same local sub-window column).  Ends with a workgroup barrier.
 template <class Tag, int WIN, bool REV, bool HIER = false>
-__device__ __attribute__((always_inline)) inline void fwd_tables(const typename Tag::S *__restrict__ tab,
-                                                                  const typename Tag::S *__restrict__ tabl, int64_t c,
+__device__ __attribute__((always_inline)) inline void fwd_tables(const TabRegs<Tag, WIN, HIER, kFwdThreads> &tr,
                                                                   typename Tag::S *Ts, typename Tag::S *TB,
                                                                   typename Tag::S *Tsl, typename Tag::S *TBL, int tid) {
   typedef typename Tag::S S;
   typedef FwdCfg<Tag, WIN> G;
   constexpr int RP = G::RP, K1 = G::K1, K2 = G::K2;
-  const S *tc = tab + c * K2;
-  for (int k = tid; k < K2; k += kFwdThreads) Ts[k] = tc[REV ? K2 - 1 - k : k];
+#pragma unroll
+  for (int i = 0; i < tr.N; ++i) {
+    const int k = tid + i * kFwdThreads;
+    if (k < K2) Ts[k] = tr.v[i];
+  }
   if constexpr (HIER) {
     constexpr int K2L = G::K2L;
-    const S *tl = tabl + c * K2L;
-    for (int k = tid; k < K2L; k += kFwdThreads) Tsl[k] = tl[REV ? K2L - 1 - k : k];
+#pragma unroll
+    for (int i = 0; i < tr.NL; ++i) {
+      const int k = tid + i * kFwdThreads;
+      if (k < K2L) Tsl[k] = tr.vl[i];
+    }
   }
   if constexpr (Tag::W16) {
     __syncthreads();
@@ -623,9 +664,11 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
 
   // ---- 1. first sub-tile's rows in flight; the table (Toeplitz blocks of
   //         M_c for 16-bit, the table itself for float32) -> LDS
+  TabRegs<Tag, WIN, HIER, kFwdThreads> tr;
+  tab_load<Tag, WIN, REV, HIER, kFwdThreads>(tab, tabl, c, tid, tr);
   SubRows<Tag, WIN> nxt;
   if (nsub > 0) load_sub<Tag, WIN, TILED>(a, x, c, n0 + first * 16, nwin - first * 16, lane, nxt);
-  fwd_tables<Tag, WIN, REV, HIER>(tab, tabl, c, Ts, TB, Tsl, TBL, tid);
+  fwd_tables<Tag, WIN, REV, HIER>(tr, Ts, TB, Tsl, TBL, tid);
 
   const int g = lane >> 4;   // lane group
   const int ln = lane & 15;  // row (A) / column (B, C) inside a 16x16 tile
@@ -884,9 +927,11 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_img_kernel(const type
     }
   };
 
+  TabRegs<Tag, WIN, false, kFwdThreads> tr;
+  tab_load<Tag, WIN, REV, false, kFwdThreads>(tab, nullptr, c, tid, tr);
   uint4 nxt[KC];
   if (nsub > 0) load(n0 + first * 16, nxt);
-  fwd_tables<Tag, WIN, REV>(tab, nullptr, c, Ts, TB, nullptr, nullptr, tid);
+  fwd_tables<Tag, WIN, REV>(tr, Ts, TB, nullptr, nullptr, tid);
 
   for (int j = 0; j < nsub; ++j) {
     const int64_t m0 = n0 + (first + j) * 16;
@@ -1706,14 +1751,18 @@ __device__ __attribute__((always_inline)) void bwd_wave(const typename Tag::S *_
 #pragma unroll
   for (int j = 0; j < SP::na; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // first stage in flight; the reversed table row and (16-bit) its Toeplitz
+  // the reversed table row and the first stage in flight (the table first,
+  // ahead of the bulk loads); the table row and (16-bit) its Toeplitz
   // blocks -> LDS
+  TabRegs<Tag, WIN, false, kThreads> tr;
+  tab_load<Tag, WIN, true, false, kThreads>(tab, nullptr, c, tid, tr);
   Stage<Tag, WIN, G> st;
   stage_load<Tag, WIN, G, TILED>(a, x, dy, c, s0, s1, tid, st);
   {
     S *Ts = reinterpret_cast<S *>(smem + G::TS_OFF);
-    const S *tc = tab + c * K2;
-    for (int k = tid; k < K2; k += kThreads) Ts[k] = tc[K2 - 1 - k];
+#pragma unroll
+    for (int i = 0; i < tr.N; ++i)
+      if (tid + i * kThreads < K2) Ts[tid + i * kThreads] = tr.v[i];
     if constexpr (Tag::W16) {
       __syncthreads();
       S *TB = reinterpret_cast<S *>(smem + G::TB_OFF);
@@ -1922,13 +1971,17 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
 #pragma unroll
   for (int j = 0; j < SP::na; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // stage 0 in flight; the reversed table row and (16-bit) its Toeplitz
-  // blocks -> LDS; stage 0 -> LDS buffer 0, stage 1 in flight
+  // the reversed table row and stage 0 in flight (the table first, ahead
+  // of the bulk loads); the table row and (16-bit) its Toeplitz blocks ->
+  // LDS; stage 0 -> LDS buffer 0, stage 1 in flight
+  TabRegs<Tag, WIN, false, kStreamThreads> tr;
+  if constexpr (DX) tab_load<Tag, WIN, true, false, kStreamThreads>(tab, nullptr, c, tid, tr);
   StreamRows<Tag, WIN> st;
   stream_load<Tag, WIN>(a, x, dy, c, s0, s1, wave, lane, st);
   if constexpr (DX) {
-    const S *tc = tab + c * K2;
-    for (int k = tid; k < K2; k += kStreamThreads) Ts[k] = tc[K2 - 1 - k];
+#pragma unroll
+    for (int i = 0; i < tr.N; ++i)
+      if (tid + i * kStreamThreads < K2) Ts[tid + i * kStreamThreads] = tr.v[i];
     __syncthreads();
     if constexpr (Tag::W16) {
       constexpr int CPR = RP / 8;
