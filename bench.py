@@ -56,11 +56,11 @@ def parse():
 # on (sha256 of the kernel header); otherwise reported as null.
 TRAFFIC = {
     # (workload, kernel): measured bytes per dispatch (profiles/wbmm_traffic_*.txt)
-    ("bf16_b64_c192_28_w14", "bwd"): {"source": "68edc0dce3f21244", "bytes": 62499909},
-    ("bf16_b64_c192_28_w14", "fwd"): {"source": "68edc0dce3f21244", "bytes": 41287283},
-    ("bf16_b64_c192_28_w14", "dx"): {"source": "68edc0dce3f21244", "bytes": 41295490},
-    ("bf16_b64_c192_28_w14", "dt"): {"source": "68edc0dce3f21244", "bytes": 42187714},
-    ("bf16_b64_c96_56_w7", "fwd"): {"source": "68edc0dce3f21244", "bytes": 77533511},
+    ("bf16_b64_c192_28_w14", "bwd"): {"source": "0a0742ceb616921d", "bytes": 62512694},
+    ("bf16_b64_c192_28_w14", "fwd"): {"source": "0a0742ceb616921d", "bytes": 41181440},
+    ("bf16_b64_c192_28_w14", "dx"): {"source": "0a0742ceb616921d", "bytes": 41231232},
+    ("bf16_b64_c192_28_w14", "dt"): {"source": "0a0742ceb616921d", "bytes": 42177231},
+    ("bf16_b64_c96_56_w7", "fwd"): {"source": "0a0742ceb616921d", "bytes": 77531271},
 }
 
 
