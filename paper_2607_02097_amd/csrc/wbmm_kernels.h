@@ -1342,32 +1342,22 @@ __device__ __attribute__((always_inline)) inline void dt_products(const unsigned
   }
 }
 
-// Table gradient of the workgroup's slab from the accumulators: diagonal
-// bins, then the slab's dT; with several slabs per channel the channel's
-// last workgroup sums the partials.  Starts with a workgroup barrier (the
-// bins reuse the LDS of the stages).
-// Diagonal binning of one wave's accumulator tiles into the bins at the
-// end of the scratch (LDS of the stages); no workgroup barrier inside.
+// Diagonal binning of one wave's accumulator tiles, in two halves: the
+// tiles go to this wave's scratch (scr) and the bins are summed from it into
+// binsum.  No workgroup barrier inside; the halves are separated by a wave
+// barrier (dt_bin) or by anything that orders the wave's LDS accesses.
+template <class G>
+__host__ __device__ constexpr int bin_tiles_per_wave() { return max_tiles_per_wave<G::NPT>(); }
+constexpr int kBinTile = 272;  // floats per tile (16 rows of 17, or of 16 for one-row tiles)
+
 template <class Tag, int WIN, class G, int WAVE>
-__device__ __attribute__((always_inline)) inline void dt_bin(const f32x4 (&acc)[PSpan<G::NPT, WAVE>::na],
-                                                              unsigned char *smem) {
+__device__ __attribute__((always_inline)) inline void dt_bin_write(const f32x4 (&acc)[PSpan<G::NPT, WAVE>::na],
+                                                                    float *scr) {
   typedef PSpan<G::NPT, WAVE> SP;
-  constexpr int NPT = G::NPT, RP = G::RP, R = G::R;
-  constexpr int K1 = G::K1, NBT = G::NBT;
-  constexpr int PLO = SP::lo, NP = SP::np;
+  constexpr int R = G::R, NP = SP::np, TSTR = kBinTile;
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4;
   const int ln = lane & 15;
-
-  // ---- diagonal binning, fixed order.  Every tile of the wave goes to LDS
-  // at once; bin (da, dw) of tile P sums the elements
-  // (ra*RP + xo + dw, rb*RP + xo) with ra - rb = da over xo, and every lane
-  // issues the reads of all its bins at once (out-of-range terms read a valid
-  // slot and are masked to zero).
-  constexpr int NPM = max_tiles_per_wave<NPT>();
-  constexpr int TSTR = 272;  // floats per tile (16 rows of 17, or of 16 for one-row tiles)
-  float *scr = reinterpret_cast<float *>(smem) + WAVE * NPM * TSTR;
-  float *binsum = reinterpret_cast<float *>(smem) + kWaves * NPM * TSTR;
   if constexpr (R == 1) {
     // One window row per tile (RP = 16): a bin is one diagonal dw = xi - xo
     // of the 16 x 16 tile.  The tile is written skewed, element (xi, xo) at
@@ -1386,7 +1376,23 @@ __device__ __attribute__((always_inline)) inline void dt_bin(const f32x4 (&acc)[
 #pragma unroll
       for (int j = 0; j < NP; ++j) row[j * TSTR] = ok ? acc[j][rr] : 0.f;
     }
-    wave_lds_sync();
+  } else {
+#pragma unroll
+    for (int j = 0; j < NP; ++j) {
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) scr[j * TSTR + (4 * g + rr) * 17 + ln] = acc[j][rr];
+    }
+  }
+}
+
+template <class Tag, int WIN, class G, int WAVE>
+__device__ __attribute__((always_inline)) inline void dt_bin_sum(const float *scr, float *binsum) {
+  typedef PSpan<G::NPT, WAVE> SP;
+  constexpr int NPT = G::NPT, RP = G::RP, R = G::R;
+  constexpr int K1 = G::K1, NBT = G::NBT;
+  constexpr int PLO = SP::lo, NP = SP::np, TSTR = kBinTile;
+  const int lane = threadIdx.x & 63;
+  if constexpr (R == 1) {
     const int s = lane & 15;
 #pragma unroll
     for (int it = 0; it < cdiv(NP * 16, 64); ++it) {
@@ -1407,12 +1413,6 @@ __device__ __attribute__((always_inline)) inline void dt_bin(const f32x4 (&acc)[
       }
     }
   } else {
-#pragma unroll
-    for (int j = 0; j < NP; ++j) {
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr) scr[j * TSTR + (4 * g + rr) * 17 + ln] = acc[j][rr];
-    }
-    wave_lds_sync();
 #pragma unroll
     for (int it = 0; it < cdiv(NP * NBT, 64); ++it) {
       const int b2 = lane + 64 * it;
@@ -1437,6 +1437,78 @@ __device__ __attribute__((always_inline)) inline void dt_bin(const f32x4 (&acc)[
         }
         binsum[(PLO + j + NPT - 1) * NBT + bin] = sum;
       }
+    }
+  }
+}
+
+// Diagonal binning of one wave's accumulator tiles into the bins at the
+// end of the scratch (LDS of the stages); no workgroup barrier inside.
+// Every tile of the wave goes to LDS at once; bin (da, dw) of tile P sums
+// the elements (ra*RP + xo + dw, rb*RP + xo) with ra - rb = da over xo, in a
+// fixed order.
+template <class Tag, int WIN, class G, int WAVE>
+__device__ __attribute__((always_inline)) inline void dt_bin(const f32x4 (&acc)[PSpan<G::NPT, WAVE>::na],
+                                                              unsigned char *smem) {
+  constexpr int NPM = bin_tiles_per_wave<G>();
+  float *scr = reinterpret_cast<float *>(smem) + WAVE * NPM * kBinTile;
+  float *binsum = reinterpret_cast<float *>(smem) + kWaves * NPM * kBinTile;
+  dt_bin_write<Tag, WIN, G, WAVE>(acc, scr);
+  wave_lds_sync();
+  dt_bin_sum<Tag, WIN, G, WAVE>(scr, binsum);
+}
+
+// The bins of the four table-gradient waves' tiles (already written to the
+// scratch by dt_bin_write) summed by all NTH threads of the workgroup: task
+// (wave, tile, column) for one-row tiles, (wave, tile, bin) otherwise, each
+// summed as dt_bin_sum sums it.
+template <class Tag, int WIN, class G, int NTH>
+__device__ __attribute__((always_inline)) inline void dt_bin_sum_all(const float *scr0, float *binsum, int tid) {
+  constexpr int NPT = G::NPT, RP = G::RP, R = G::R, K1 = G::K1, NBT = G::NBT;
+  constexpr int NPM = bin_tiles_per_wave<G>(), TSTR = kBinTile;
+  constexpr int TPT = R == 1 ? 16 : NBT;  // tasks per tile
+  constexpr int NP0 = PSpan<NPT, 0>::np, NP1 = PSpan<NPT, 1>::np, NP2 = PSpan<NPT, 2>::np, NP3 = PSpan<NPT, 3>::np;
+  constexpr int E0 = NP0 * TPT, E1 = E0 + NP1 * TPT, E2 = E1 + NP2 * TPT, E3 = E2 + NP3 * TPT;
+  for (int t = tid; t < E3; t += NTH) {
+    int W, r, plo;
+    if (t < E0) { W = 0; r = t; plo = PSpan<NPT, 0>::lo; }
+    else if (t < E1) { W = 1; r = t - E0; plo = PSpan<NPT, 1>::lo; }
+    else if (t < E2) { W = 2; r = t - E1; plo = PSpan<NPT, 2>::lo; }
+    else { W = 3; r = t - E2; plo = PSpan<NPT, 3>::lo; }
+    const int j = r / TPT;
+    const int q = r - j * TPT;
+    const float *tile = scr0 + (W * NPM + j) * TSTR;
+    if constexpr (R == 1) {
+      const int s = q;
+      const float *col = tile + s;
+      float lo = 0.f, hi = 0.f;
+#pragma unroll
+      for (int xi = 0; xi < 16; ++xi) {
+        const float v = col[((xi & ~3) + ((xi + (xi >> 2)) & 3)) * 16];
+        const bool upper = xi + s <= 15;
+        lo += upper ? v : 0.f;
+        hi += upper ? 0.f : v;
+      }
+      float *bp = binsum + (plo + j + NPT - 1) * NBT + WIN - 1;
+      if (s <= WIN - 1) bp[-s] = lo;
+      if (s >= 1 && 16 - s <= WIN - 1) bp[16 - s] = hi;
+    } else {
+      const int bin = q;
+      const int da = bin / K1 - (R - 1);
+      const int dw = bin - (bin / K1) * K1 - (WIN - 1);
+      float sum = 0.f;
+#pragma unroll
+      for (int ra = 0; ra < R; ++ra) {
+        const int rb = ra - da;
+        const bool rok = rb >= 0 && rb < R;
+#pragma unroll
+        for (int xo = 0; xo < WIN; ++xo) {
+          const int xi = xo + dw;
+          const bool ok = rok && xi >= 0 && xi < WIN;
+          const float v = tile[ok ? (ra * RP + xi) * 17 + rb * RP + xo : 0];
+          sum += ok ? v : 0.f;
+        }
+      }
+      binsum[(plo + j + NPT - 1) * NBT + bin] = sum;
     }
   }
 }
@@ -1532,6 +1604,10 @@ __device__ __attribute__((always_inline)) inline void dt_reduce(unsigned char *s
   if (tid == 0) __hip_atomic_store(&cnt[c], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Table gradient of the workgroup's slab from the accumulators: diagonal
+// bins, then the slab's dT; with several slabs per channel the channel's
+// last workgroup sums the partials.  Starts with a workgroup barrier (the
+// bins reuse the LDS of the stages).
 template <class Tag, int WIN, class G, int WAVE>
 __device__ __attribute__((always_inline)) inline void dt_finish(const f32x4 (&acc)[PSpan<G::NPT, WAVE>::na],
                                                                  unsigned char *smem, float *__restrict__ dt,
@@ -2023,7 +2099,13 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
   if constexpr (DX)
     stream_store<Tag, WIN>(a, dx, c, s0 + (int64_t)(nst - 1) * CW, s1, tid,
                            smem + SC::O_OFF + ((nst - 1) & 1) * G::BUF);
-  if constexpr (DTW >= 0) dt_bin<Tag, WIN, G, DTW>(acc, smem);
+  // the table-gradient waves' tiles to the scratch, then the bins summed by
+  // all twelve waves
+  constexpr int NPM = bin_tiles_per_wave<G>();
+  if constexpr (DTW >= 0) dt_bin_write<Tag, WIN, G, DTW>(acc, reinterpret_cast<float *>(smem) + DTW * NPM * kBinTile);
+  __syncthreads();
+  dt_bin_sum_all<Tag, WIN, G, kStreamThreads>(reinterpret_cast<const float *>(smem),
+                                              reinterpret_cast<float *>(smem) + kWaves * NPM * kBinTile, tid);
   __syncthreads();
   dt_reduce<Tag, WIN, G, kStreamThreads>(smem, dt, part, cnt, a, c, slab);
 }
