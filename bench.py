@@ -56,11 +56,11 @@ def parse():
 # on (sha256 of the kernel header); otherwise reported as null.
 TRAFFIC = {
     # (workload, kernel): measured bytes per dispatch (profiles/wbmm_traffic_*.txt)
-    ("bf16_b64_c192_28_w14", "bwd"): {"source": "0a0742ceb616921d", "bytes": 62512694},
-    ("bf16_b64_c192_28_w14", "fwd"): {"source": "0a0742ceb616921d", "bytes": 41181440},
-    ("bf16_b64_c192_28_w14", "dx"): {"source": "0a0742ceb616921d", "bytes": 41231232},
-    ("bf16_b64_c192_28_w14", "dt"): {"source": "0a0742ceb616921d", "bytes": 42177231},
-    ("bf16_b64_c96_56_w7", "fwd"): {"source": "0a0742ceb616921d", "bytes": 77531271},
+    ("bf16_b64_c192_28_w14", "bwd"): {"source": "20674b9b95627877", "bytes": 62608065},
+    ("bf16_b64_c192_28_w14", "fwd"): {"source": "20674b9b95627877", "bytes": 41254879},
+    ("bf16_b64_c192_28_w14", "dx"): {"source": "20674b9b95627877", "bytes": 41199352},
+    ("bf16_b64_c192_28_w14", "dt"): {"source": "20674b9b95627877", "bytes": 42201010},
+    ("bf16_b64_c96_56_w7", "fwd"): {"source": "20674b9b95627877", "bytes": 77530540},
 }
 
 
@@ -137,6 +137,32 @@ def pass_bytes(wl, p, es):
 
 def pass_flops(wl, p):
     return wl.flops(("dx", "dt") if p == "bwd" else (p,))
+
+
+def run_marks(n, nrun=5):
+    """Events that split a timed loop of n iterations into up to nrun runs
+    (recorded on the stream inside the timed region: they add no
+    synchronisation)."""
+    import torch
+    nrun = max(1, min(nrun, n))
+    bounds = [round(n * (k + 1) / nrun) for k in range(nrun)]
+    return [torch.cuda.Event(enable_timing=True) for _ in bounds], bounds
+
+
+def run_times(start, marks, bounds, per_iter):
+    """ms per step of each run between consecutive marks."""
+    out, prev, lo = [], start, 0
+    for mk, hi in zip(marks, bounds):
+        out.append(prev.elapsed_time(mk) / ((hi - lo) * per_iter))
+        prev, lo = mk, hi
+    return out
+
+
+def quartiles(v):
+    """Median and the first and third quartiles (linear interpolation)."""
+    import numpy as np
+    q1, q2, q3 = np.percentile(np.asarray(v, dtype=np.float64), [25, 50, 75])
+    return float(q2), float(q1), float(q3)
 
 
 def main():
@@ -260,14 +286,20 @@ def main():
         # plain stream launches (hardware-counter runs serialise dispatches)
         t_start = torch.cuda.Event(enable_timing=True)
         t_end = torch.cuda.Event(enable_timing=True)
+        marks, bounds = run_marks(steps)
         torch.cuda.synchronize()
         t_start.record(stream)
-        for i in range(steps):
-            for p in step_kernels:
-                launch(p, i)
+        i = 0
+        for mk, bd in zip(marks, bounds):
+            while i < bd:
+                for p in step_kernels:
+                    launch(p, i)
+                i += 1
+            mk.record(stream)
         t_end.record(stream)
         torch.cuda.synchronize()
         ms_step = t_start.elapsed_time(t_end) / steps
+        run_ms = run_times(t_start, marks, bounds, 1)
         per_pass = {}
         for p in timed:
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -302,13 +334,19 @@ def main():
         # same stream to get the average duration of each kernel launch
         t_start = torch.cuda.Event(enable_timing=True)
         t_end = torch.cuda.Event(enable_timing=True)
+        marks, bounds = run_marks(reps)
         torch.cuda.synchronize()
         t_start.record(stream)
-        for _ in range(reps):
-            g_step.replay()
+        i = 0
+        for mk, bd in zip(marks, bounds):
+            while i < bd:
+                g_step.replay()
+                i += 1
+            mk.record(stream)
         t_end.record(stream)
         torch.cuda.synchronize()
         ms_step = t_start.elapsed_time(t_end) / steps
+        run_ms = run_times(t_start, marks, bounds, R)
         per_pass = {}
         for p in timed:
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -335,12 +373,12 @@ def main():
     tl = "true" if fixed_offset_rows(wl) else "false"
     # channel-stream gradients: fixed-offset rows and no more channels than
     # compute units (256 on MI355X)
-    stream = fixed_offset_rows(wl) and wl.C <= torch.cuda.get_device_properties(0).multi_processor_count
-    dtk = "wbmm_bwd_stream_kernel" if stream else "wbmm_dt_kernel"
-    bwk = "wbmm_bwd_stream_kernel" if stream else "wbmm_bwd_kernel"
+    chan_stream = fixed_offset_rows(wl) and wl.C <= torch.cuda.get_device_properties(0).multi_processor_count
+    dtk = "wbmm_bwd_stream_kernel" if chan_stream else "wbmm_dt_kernel"
+    bwk = "wbmm_bwd_stream_kernel" if chan_stream else "wbmm_bwd_kernel"
     kernel_name = {"fwd": fk + "<%s,%d,false>", "dx": fk + "<%s,%d,true>",
-                   "dt": dtk + "<%s,%d," + ("false" if stream else tl) + ">",
-                   "bwd": bwk + "<%s,%d," + ("true" if stream else tl) + ">",
+                   "dt": dtk + "<%s,%d," + ("false" if chan_stream else tl) + ">",
+                   "bwd": bwk + "<%s,%d," + ("true" if chan_stream else tl) + ">",
                    "hfwd": "wbmm_fwd_kernel<%s,%d,false,true>",
                    "hbwd": "wbmm_hier_backward (3 launches) <%s,%d>"}[dom] % ({"bf16": "TagBF16", "f16": "TagF16",
                                                           "f32": "TagF32"}[wl.dtype], wl.w)
@@ -359,6 +397,53 @@ def main():
     roof.update({"traffic": traffic, "kernel": kernel_name, "pass": dom,
                  "avg_ms": round(dom_ms, 5), "algorithmic_bytes": dom_bytes,
                  "algorithmic_flops": dom_flops})
+
+    # the bandwidth a plain device copy of one activation tensor reaches on
+    # this GPU, in the same cache mode (the same input sets rotated), as a
+    # measured ceiling beside the nominal HBM peak
+    act_bytes = wl.B * wl.C * wl.H * wl.W * es
+    scratch = torch.empty_like(sets[0][0])
+    ncopy = 10
+    if args.eager:
+        def copies():
+            for i in range(ncopy):
+                scratch.copy_(sets[i % nsets][0])
+    else:
+        g_copy = torch.cuda.CUDAGraph()
+        cs = torch.cuda.Stream(dev)
+        cs.wait_stream(stream)
+        with torch.cuda.graph(g_copy, stream=cs):
+            for i in range(ncopy):
+                scratch.copy_(sets[i % nsets][0])
+        stream.wait_stream(cs)
+        torch.cuda.synchronize()
+        copies = g_copy.replay
+    copies()
+    torch.cuda.synchronize()
+    ca, cb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ncr = max(1, min(reps, 100))
+    ca.record(stream)
+    for _ in range(ncr):
+        copies()
+    cb.record(stream)
+    torch.cuda.synchronize()
+    copy_ms = ca.elapsed_time(cb) / (ncr * ncopy)
+    copy_gbps = 2 * act_bytes / (copy_ms * 1e-3) / 1e9
+    roof["copy_gbps"] = round(copy_gbps, 1)
+    if roof["bound"] == "hbm":
+        roof["frac_of_copy"] = round(roof["achieved"] / copy_gbps, 4)
+
+    # the step against its own roofline: algorithmic flops over algorithmic
+    # bytes of the step's kernels, attainable = min(MFMA peak, AI x HBM peak)
+    step_bytes = sum(pass_bytes(wl, p, es) for p in step_kernels)
+    step_ai = flops / step_bytes
+    attain = min(peak, step_ai * HBM_PEAK_GBS / 1e3)
+    step_roof = {"flops": flops, "bytes": step_bytes, "ai_flop_per_byte": round(step_ai, 2),
+                 "attainable_tflops": round(attain, 1), "frac": round(tflops / attain, 4),
+                 "attainable_at_copy_bw_tflops": round(min(peak, step_ai * copy_gbps / 1e3), 1)}
+    med, q1, q3 = quartiles(run_ms)
+    runs = {"n": len(run_ms), "ms_per_step": [round(v, 5) for v in run_ms],
+            "median_ms": round(med, 5), "iqr_ms": [round(q1, 5), round(q3, 5)]}
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -405,6 +490,8 @@ def main():
         "launch": "eager stream launches" if args.eager else "HIP graph replay, %d steps per graph" % R,
         "eager_ms_per_step": round(eager_ms, 5),
         "roofline": roof,
+        "step_roofline": step_roof,
+        "runs": runs,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out))
