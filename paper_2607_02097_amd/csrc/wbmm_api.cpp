@@ -202,7 +202,16 @@ size_t wbmm_hier_backward_workspace_bytes(int64_t B, int64_t C, int64_t H, int64
   int64_t bytes = 0;
   if (hier_shapes(B, C, H, W, wl, dtype, &gg, &gl, &bytes) != WBMM_OK) return 0;
   const size_t a = wbmm::dtable_workspace_bytes((Dt)dtype, gg), b = wbmm::dtable_workspace_bytes((Dt)dtype, gl);
-  return a > b ? a : b;
+  size_t need = a > b ? a : b;
+  // one pass over both tables: counters and both tables' partials, for at
+  // most the slabs of the global table's plan
+  const wbmm::DtPlan p = wbmm::plan_dtable((Dt)dtype, gg);
+  if (p.slabs > 1) {
+    const int64_t kg = (int64_t)(4 * wl - 1) * (4 * wl - 1), kl = (int64_t)(2 * wl - 1) * (2 * wl - 1);
+    const size_t both = (size_t)((C * 4 + 255) / 256 * 256) + (size_t)p.slabs * (size_t)C * (size_t)(kg + kl) * 4;
+    if (both > need) need = both;
+  }
+  return need;
 }
 
 wbmm_status wbmm_hier_backward(const void *x, const void *dy, const void *table_g, const void *table_l, void *dx,
@@ -237,8 +246,12 @@ wbmm_status wbmm_hier_backward(const void *x, const void *dy, const void *table_
   }
   hipStream_t st = (hipStream_t)stream;
   hipError_t e = wbmm::launch_hier_forward((Dt)dtype, dy, table_g, table_l, dx, gg, true, st);
-  if (e == hipSuccess) e = wbmm::launch_dtable((Dt)dtype, x, dy, dtable_g, workspace, gg, st);
-  if (e == hipSuccess) e = wbmm::launch_dtable((Dt)dtype, x, dy, dtable_l, workspace, gl, st);
+  bool both = false;
+  if (e == hipSuccess) e = wbmm::launch_hier_dtable((Dt)dtype, x, dy, dtable_g, dtable_l, workspace, need, gg, st, &both);
+  if (e == hipSuccess && !both) {
+    e = wbmm::launch_dtable((Dt)dtype, x, dy, dtable_g, workspace, gg, st);
+    if (e == hipSuccess) e = wbmm::launch_dtable((Dt)dtype, x, dy, dtable_l, workspace, gl, st);
+  }
   return from_hip(e);
 }
 

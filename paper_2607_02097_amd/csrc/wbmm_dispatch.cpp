@@ -54,6 +54,15 @@ hipError_t launch_hier_forward(Dt dt, const void *x, const void *table_g, const 
   return e->hier_fwd(x, table_g, table_l, y, g, reverse_tables, stream);
 }
 
+hipError_t launch_hier_dtable(Dt dt, const void *x, const void *dy, float *dtable_g, float *dtable_l,
+                              void *workspace, size_t workspace_bytes, const Geom &g, hipStream_t stream,
+                              bool *done) {
+  *done = false;
+  const Entry *e = find(dt, g.w);
+  if (!e) return hipErrorInvalidValue;
+  return e->hier_dt(x, dy, dtable_g, dtable_l, workspace, workspace_bytes, g, stream, done);
+}
+
 DtPlan plan_dtable(Dt dt, const Geom &g) {
   const Entry *e = find(dt, g.w);
   if (!e) return DtPlan{0, 0};

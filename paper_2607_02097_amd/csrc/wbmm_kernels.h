@@ -1290,10 +1290,18 @@ __device__ __attribute__((always_inline)) inline u16x8 dt_frag16(const unsigned 
   return __builtin_bit_cast(u16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
-// This wave's share of X^T dY for one stage (K = the stage's windows).
-template <class Tag, class G, int WAVE>
-__device__ __attribute__((always_inline)) inline void dt_products(const unsigned char *Xt, const unsigned char *Dt,
-                                                                   f32x4 (&acc)[PSpan<G::NPT, WAVE>::na], int lane) {
+// This wave's share of X^T dY for one stage (K = the stage's windows).  With
+// HL > 0 (hierarchical form, local window HL, one window row per tile) the
+// products of tile pairs whose rows lie in the same half of the window go to
+// accl instead of acc: acc + accl is the global table's tile, accl alone
+// holds every pair of the local table (the same products, none added).
+template <class Tag, class G, int WAVE, int HL>
+__device__ __attribute__((always_inline)) inline void dt_products_split(const unsigned char *Xt,
+                                                                         const unsigned char *Dt,
+                                                                         f32x4 (&acc)[PSpan<G::NPT, WAVE>::na],
+                                                                         f32x4 (&accl)[PSpan<G::NPT, WAVE>::na],
+                                                                         int lane) {
+  static_assert(HL == 0 || G::R == 1, "local halves need one window row per tile");
   typedef typename Tag::Frag Frag;
   typedef PSpan<G::NPT, WAVE> SP;
   constexpr int NPT = G::NPT, CW = G::CW;
@@ -1315,7 +1323,10 @@ __device__ __attribute__((always_inline)) inline void dt_products(const unsigned
 #pragma unroll
         for (int j = 0; j < NP; ++j) {
           const int po = pi - (PLO + j);
-          if (po >= 0 && po < NPT) acc[j] = mma<Tag>(af, bf[po], acc[j]);
+          if (po >= 0 && po < NPT) {
+            if (HL > 0 && (pi < HL) == (po < HL)) accl[j] = mma<Tag>(af, bf[po], accl[j]);
+            else acc[j] = mma<Tag>(af, bf[po], acc[j]);
+          }
         }
       }
     } else {
@@ -1334,12 +1345,21 @@ __device__ __attribute__((always_inline)) inline void dt_products(const unsigned
 #pragma unroll
           for (int j = 0; j < NP; ++j) {
             const int po = pi - (PLO + j);
-            if (po >= 0 && po < NPT) acc[j] = mma<Tag>(af, bf[po], acc[j]);
+            if (po >= 0 && po < NPT) {
+              if (HL > 0 && (pi < HL) == (po < HL)) accl[j] = mma<Tag>(af, bf[po], accl[j]);
+              else acc[j] = mma<Tag>(af, bf[po], acc[j]);
+            }
           }
         }
       }
     }
   }
+}
+
+template <class Tag, class G, int WAVE>
+__device__ __attribute__((always_inline)) inline void dt_products(const unsigned char *Xt, const unsigned char *Dt,
+                                                                   f32x4 (&acc)[PSpan<G::NPT, WAVE>::na], int lane) {
+  dt_products_split<Tag, G, WAVE, 0>(Xt, Dt, acc, acc, lane);
 }
 
 // Diagonal binning of one wave's accumulator tiles, in two halves: the
@@ -1511,6 +1531,106 @@ __device__ __attribute__((always_inline)) inline void dt_bin_sum_all(const float
       binsum[(plo + j + NPT - 1) * NBT + bin] = sum;
     }
   }
+}
+
+// Hierarchical form: the local table's bins from the same-half accumulator
+// tiles of the four table-gradient waves (written to the scratch by
+// dt_bin_write; one window row per tile).  Bin (P, dwl), P = hi - ho and
+// dwl = xi - xo, sums the elements (xi, xo) of tile P with both columns in
+// the same half of the window, xo ascending; one task per bin.
+template <class G, int HL, int NTH>
+__device__ __attribute__((always_inline)) inline void dt_bin_sum_local(const float *scr0, float *binl, int tid) {
+  static_assert(G::R == 1, "one window row per tile");
+  constexpr int WIN = G::NPT, K1L = 2 * HL - 1, NPM = bin_tiles_per_wave<G>();
+  constexpr PRange PR = make_prange<G::NPT>();
+  for (int t = tid; t < K1L * K1L; t += NTH) {
+    const int P = t / K1L - (HL - 1);
+    const int dw = t - (t / K1L) * K1L - (HL - 1);
+    int W = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w)
+      if (P >= PR.lo[w] && P <= PR.hi[w]) W = w;
+    int lo = PR.lo[0];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w)
+      if (W == w) lo = PR.lo[w];
+    const float *tile = scr0 + (W * NPM + (P - lo)) * kBinTile;
+    float sum = 0.f;
+#pragma unroll
+    for (int xo = 0; xo < WIN; ++xo) {
+      const int xi = xo + dw;
+      const bool ok = xi >= 0 && xi < WIN && (xi < HL) == (xo < HL);
+      const int xs = ok ? xi : 0;
+      // element (xi, xo) of the skewed tile: row 4 (xi / 4) + (xi + xi / 4) % 4,
+      // column (xo - xi) mod 16
+      const float v = tile[((xs & ~3) + ((xs + (xs >> 2)) & 3)) * 16 + ((xo - xs) & 15)];
+      sum += ok ? v : 0.f;
+    }
+    binl[t] = sum;
+  }
+}
+
+// Hierarchical form: both table gradients of the slab from their bins (one
+// window row per tile: bin k of either table is its entry k); with several
+// slabs per channel one ticket per workgroup, and the channel's last
+// workgroup sums the partials of both tables in slab order and resets the
+// counter.
+template <class G, int HL, int NTH>
+__device__ __attribute__((always_inline)) inline void dt_reduce_hier(unsigned char *smem, const float *bing,
+                                                                      const float *binl, float *__restrict__ dtg,
+                                                                      float *__restrict__ dtl, float *__restrict__ partg,
+                                                                      float *__restrict__ partl,
+                                                                      unsigned *__restrict__ cnt, const KArgs &a,
+                                                                      int64_t c, int64_t slab) {
+  static_assert(G::R == 1, "one window row per tile");
+  constexpr int K2 = G::K2, K2L = (2 * HL - 1) * (2 * HL - 1), KT = K2 + K2L;
+  const int tid = threadIdx.x;
+  const bool single = a.tiles_per_ch == 1;
+  for (int k = tid; k < KT; k += NTH) {
+    const bool loc = k >= K2;
+    const int kk = loc ? k - K2 : k;
+    const float s = loc ? binl[kk] : bing[kk];
+    if (single) {
+      if (loc) dtl[c * K2L + kk] = s;
+      else dtg[c * K2 + kk] = s;
+    } else {
+      float *dst = loc ? &partl[(slab * a.C + c) * K2L + kk] : &partg[(slab * a.C + c) * K2 + kk];
+      __hip_atomic_store(dst, s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+  if (single) return;
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  int *flag = reinterpret_cast<int *>(smem);
+  if (tid == 0) {
+    const unsigned ticket = __hip_atomic_fetch_add(&cnt[c], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    *flag = ticket == (unsigned)(a.tiles_per_ch - 1);
+  }
+  __syncthreads();
+  if (*flag == 0) return;
+  constexpr int SG = 8;
+  for (int k = tid; k < KT; k += NTH) {
+    const bool loc = k >= K2;
+    const int kk = loc ? k - K2 : k;
+    float s = 0.f;
+    for (int j0 = 0; j0 < a.tiles_per_ch; j0 += SG) {
+      float v[SG];
+#pragma unroll
+      for (int j = 0; j < SG; ++j) {
+        const int64_t sl = j0 + j;
+        v[j] = sl < a.tiles_per_ch
+                   ? __hip_atomic_load(loc ? &partl[(sl * a.C + c) * K2L + kk] : &partg[(sl * a.C + c) * K2 + kk],
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                   : 0.f;
+      }
+#pragma unroll
+      for (int j = 0; j < SG; ++j)
+        if (j0 + j < a.tiles_per_ch) s += v[j];
+    }
+    if (loc) dtl[c * K2L + kk] = s;
+    else dtg[c * K2 + kk] = s;
+  }
+  if (tid == 0) __hip_atomic_store(&cnt[c], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // This slab's table gradient from the bins (a fixed-order combine); with
@@ -2020,13 +2140,14 @@ __device__ __attribute__((always_inline)) inline void stream_store(const KArgs &
 // range), else DXW >= 0 an input-gradient wave (idle but for the copies
 // when DX is false: the table gradient alone, with the same stages, bins and
 // sums as the fused pass).
-template <class Tag, int WIN, int DTW, int DXW, bool DX>
+template <class Tag, int WIN, int DTW, int DXW, bool DX, int HL>
 __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S *__restrict__ x,
                                                            const typename Tag::S *__restrict__ dy,
                                                            const typename Tag::S *__restrict__ tab,
                                                            typename Tag::S *__restrict__ dx, float *__restrict__ dt,
                                                            float *__restrict__ part, unsigned *__restrict__ cnt,
-                                                           const KArgs &a, unsigned char *smem) {
+                                                           const KArgs &a, unsigned char *smem,
+                                                           float *__restrict__ dtl, float *__restrict__ partl) {
   typedef typename Tag::S S;
   typedef StreamCfg<Tag, WIN> SC;
   typedef BwdCfg<Tag, WIN> G;
@@ -2043,9 +2164,9 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
   S *Ts = reinterpret_cast<S *>(smem + SC::TS_OFF);
   S *TB = reinterpret_cast<S *>(smem + SC::TB_OFF);
 
-  f32x4 acc[SP::na];
+  f32x4 acc[SP::na], accl[SP::na];
 #pragma unroll
-  for (int j = 0; j < SP::na; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int j = 0; j < SP::na; ++j) acc[j] = accl[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   // the reversed table row and stage 0 in flight (the table first, ahead
   // of the bulk loads); the table row and (16-bit) its Toeplitz blocks ->
@@ -2083,7 +2204,7 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
     unsigned char *obuf = smem + SC::O_OFF + (s & 1) * G::BUF;
     // this stage's products
     if constexpr (DTW >= 0) {
-      dt_products<Tag, G, DTW>(cur, cur + G::BUF, acc, lane);
+      dt_products_split<Tag, G, DTW, HL>(cur, cur + G::BUF, acc, accl, lane);
     } else if constexpr (DX) {
       dx_products<Tag, WIN, DXW, kStreamWaves - kStreamDt>(cur + G::BUF, obuf, Ts, TB, lane);
     }
@@ -2102,34 +2223,72 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
   // the table-gradient waves' tiles to the scratch, then the bins summed by
   // all twelve waves
   constexpr int NPM = bin_tiles_per_wave<G>();
-  if constexpr (DTW >= 0) dt_bin_write<Tag, WIN, G, DTW>(acc, reinterpret_cast<float *>(smem) + DTW * NPM * kBinTile);
-  __syncthreads();
-  dt_bin_sum_all<Tag, WIN, G, kStreamThreads>(reinterpret_cast<const float *>(smem),
-                                              reinterpret_cast<float *>(smem) + kWaves * NPM * kBinTile, tid);
-  __syncthreads();
-  dt_reduce<Tag, WIN, G, kStreamThreads>(smem, dt, part, cnt, a, c, slab);
+  float *scr = reinterpret_cast<float *>(smem);
+  float *bing = scr + kWaves * NPM * kBinTile;
+  if constexpr (HL > 0) {
+    // hierarchical form: the global table's tiles are acc + accl, the local
+    // table's the same-half tiles accl alone, binned after them in the same
+    // scratch
+    float *binl = bing + G::NACC * G::NBT;
+    if constexpr (DTW >= 0) {
+      f32x4 tot[SP::na];
+#pragma unroll
+      for (int j = 0; j < SP::na; ++j) {
+        const int P = SP::lo + j;
+        tot[j] = acc[j];
+        if (P > -HL && P < HL) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) tot[j][e] += accl[j][e];
+        }
+      }
+      dt_bin_write<Tag, WIN, G, DTW>(tot, scr + DTW * NPM * kBinTile);
+    }
+    __syncthreads();
+    dt_bin_sum_all<Tag, WIN, G, kStreamThreads>(scr, bing, tid);
+    __syncthreads();
+    if constexpr (DTW >= 0) dt_bin_write<Tag, WIN, G, DTW>(accl, scr + DTW * NPM * kBinTile);
+    __syncthreads();
+    dt_bin_sum_local<G, HL, kStreamThreads>(scr, binl, tid);
+    __syncthreads();
+    dt_reduce_hier<G, HL, kStreamThreads>(smem, bing, binl, dt, dtl, part, partl, cnt, a, c, slab);
+  } else {
+    if constexpr (DTW >= 0) dt_bin_write<Tag, WIN, G, DTW>(acc, scr + DTW * NPM * kBinTile);
+    __syncthreads();
+    dt_bin_sum_all<Tag, WIN, G, kStreamThreads>(scr, bing, tid);
+    __syncthreads();
+    dt_reduce<Tag, WIN, G, kStreamThreads>(smem, dt, part, cnt, a, c, slab);
+  }
 }
 
-template <class Tag, int WIN, bool DX>
+// HL > 0: the hierarchical form's two table gradients (global window WIN,
+// local window HL = WIN / 2) from one pass, DX false.
+template <class Tag, int WIN, bool DX, int HL = 0>
 __global__ __launch_bounds__(kStreamThreads, 3) void wbmm_bwd_stream_kernel(
     const typename Tag::S *__restrict__ x, const typename Tag::S *__restrict__ dy,
     const typename Tag::S *__restrict__ tab, typename Tag::S *__restrict__ dx, float *__restrict__ dt,
-    float *__restrict__ part, unsigned *__restrict__ cnt, KArgs a) {
+    float *__restrict__ part, unsigned *__restrict__ cnt, KArgs a, float *__restrict__ dtl,
+    float *__restrict__ partl) {
+  static_assert(HL == 0 || (!DX && 2 * HL == WIN), "local table gradient: table gradients only, WIN = 2 HL");
+  static_assert(HL == 0 || bins_lds_bytes<BwdCfg<Tag, WIN>>() + (size_t)(2 * HL - 1) * (2 * HL - 1) * 4 <=
+                               (size_t)StreamCfg<Tag, WIN>::O_OFF,
+                "both tables' bins within the stage buffers");
   extern __shared__ __align__(16) unsigned char smem[];
+#define WBMM_SW(D, X) stream_wave<Tag, WIN, D, X, DX, HL>(x, dy, tab, dx, dt, part, cnt, a, smem, dtl, partl)
   switch (threadIdx.x >> 6) {
-    case 0: stream_wave<Tag, WIN, 0, -1, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
-    case 1: stream_wave<Tag, WIN, 1, -1, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
-    case 2: stream_wave<Tag, WIN, 2, -1, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
-    case 3: stream_wave<Tag, WIN, 3, -1, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
-    case 4: stream_wave<Tag, WIN, -1, 0, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
-    case 5: stream_wave<Tag, WIN, -1, 1, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
-    case 6: stream_wave<Tag, WIN, -1, 2, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
-    case 7: stream_wave<Tag, WIN, -1, 3, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
-    case 8: stream_wave<Tag, WIN, -1, 4, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
-    case 9: stream_wave<Tag, WIN, -1, 5, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
-    case 10: stream_wave<Tag, WIN, -1, 6, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
-    default: stream_wave<Tag, WIN, -1, 7, DX>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
+    case 0: WBMM_SW(0, -1); break;
+    case 1: WBMM_SW(1, -1); break;
+    case 2: WBMM_SW(2, -1); break;
+    case 3: WBMM_SW(3, -1); break;
+    case 4: WBMM_SW(-1, 0); break;
+    case 5: WBMM_SW(-1, 1); break;
+    case 6: WBMM_SW(-1, 2); break;
+    case 7: WBMM_SW(-1, 3); break;
+    case 8: WBMM_SW(-1, 4); break;
+    case 9: WBMM_SW(-1, 5); break;
+    case 10: WBMM_SW(-1, 6); break;
+    default: WBMM_SW(-1, 7); break;
   }
+#undef WBMM_SW
 }
 
 // ============================================================ host side
@@ -2354,7 +2513,7 @@ static hipError_t run_dtable(const void *x, const void *dy, float *dt, void *ws,
       float *spart = b.tiles_per_ch > 1 ? (float *)((char *)ws + counter_bytes(g.C)) : nullptr;
       constexpr size_t slds = stream_lds_bytes<Tag, WIN>();
       wbmm_bwd_stream_kernel<Tag, WIN, false><<<dim3((unsigned)(g.C * b.tiles_per_ch)), dim3(kStreamThreads), slds, st>>>(
-          (const S *)x, (const S *)dy, nullptr, nullptr, dt, spart, scnt, b);
+          (const S *)x, (const S *)dy, nullptr, nullptr, dt, spart, scnt, b, nullptr, nullptr);
       return hipGetLastError();
     }
   }
@@ -2390,7 +2549,7 @@ static hipError_t run_backward(const void *x, const void *dy, const void *t, voi
       constexpr size_t slds = stream_lds_bytes<Tag, WIN>();
       static_assert(slds <= 160 * 1024, "workgroup LDS above the 160 KB of a compute unit");
       wbmm_bwd_stream_kernel<Tag, WIN, true><<<dim3((unsigned)(g.C * b.tiles_per_ch)), dim3(kStreamThreads), slds, st>>>(
-          (const S *)x, (const S *)dy, (const S *)t, (S *)dx, dt, spart, scnt, b);
+          (const S *)x, (const S *)dy, (const S *)t, (S *)dx, dt, spart, scnt, b, nullptr, nullptr);
       return hipGetLastError();
     }
   }
@@ -2409,6 +2568,45 @@ static hipError_t run_backward(const void *x, const void *dy, const void *t, voi
   wbmm_bwd_kernel<Tag, WIN, false><<<grid, dim3(kThreads), lds, st>>>((const S *)x, (const S *)dy, (const S *)t,
                                                                       (S *)dx, dt, part, cnt, a);
   return hipGetLastError();
+}
+
+// Hierarchical form (global window WIN = 2 wl): both table gradients in one
+// channel-stream pass when it applies (one window row per tile, fixed-offset
+// rows, no more channels than compute units, and the workspace holds both
+// tables' partials); *done tells whether it ran.
+template <class Tag, int WIN>
+static hipError_t run_hier_dtable(const void *x, const void *dy, float *dtg, float *dtl, void *ws, size_t ws_bytes,
+                                  const Geom &g, hipStream_t st, bool *done) {
+  *done = false;
+  if constexpr (WIN % 2 == 0 && rp_of(WIN) == 16) {
+    typedef typename Tag::S S;
+    constexpr int WL = WIN / 2;
+    constexpr int64_t K2 = (2 * WIN - 1) * (2 * WIN - 1), K2L = (2 * WL - 1) * (2 * WL - 1);
+    KArgs a = make_args(g);
+    const DtPlan p = plan_dt<Tag, WIN>(g);
+    a.tile = (int)p.slab_windows;
+    a.tiles_per_ch = (int)p.slabs;
+    set_tiled<WIN, Tag::ES>(g, a, {x, dy});
+    KArgs b = a;
+    if (!stream_plan<Tag, WIN>(g, b)) return hipSuccess;
+    unsigned *cnt = nullptr;
+    float *partg = nullptr, *partl = nullptr;
+    if (b.tiles_per_ch > 1) {
+      const size_t need = counter_bytes(g.C) + (size_t)b.tiles_per_ch * (size_t)g.C * (size_t)(K2 + K2L) * 4;
+      if (ws == nullptr || need > ws_bytes) return hipSuccess;
+      cnt = (unsigned *)ws;
+      partg = (float *)((char *)ws + counter_bytes(g.C));
+      partl = partg + (size_t)b.tiles_per_ch * (size_t)g.C * (size_t)K2;
+    }
+    constexpr size_t slds = stream_lds_bytes<Tag, WIN>();
+    wbmm_bwd_stream_kernel<Tag, WIN, false, WL><<<dim3((unsigned)(g.C * b.tiles_per_ch)), dim3(kStreamThreads), slds, st>>>(
+        (const S *)x, (const S *)dy, nullptr, nullptr, dtg, partg, cnt, b, dtl, partl);
+    *done = true;
+    return hipGetLastError();
+  } else {
+    (void)x; (void)dy; (void)dtg; (void)dtl; (void)ws; (void)ws_bytes; (void)g; (void)st;
+    return hipSuccess;
+  }
 }
 
 }  // namespace wbmm

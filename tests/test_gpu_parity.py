@@ -433,8 +433,13 @@ def test_workspace_counters_reset_between_calls():
 # ------------------------------------------------------------- hierarchical
 
 HIER = [
-    # (B, C, H, W, wl): global windows 2 wl, ragged and padded maps
+    # (B, C, H, W, wl): global windows 2 wl, ragged and padded maps; maps
+    # tiled by 2 wl >= 10 take the one-pass table gradients (one or several
+    # slabs per channel), the others two table-gradient launches
     (2, 3, 28, 28, 7),
+    (16, 3, 28, 28, 7),
+    (16, 1, 32, 32, 8),
+    (4, 2, 20, 20, 5),
     (1, 2, 30, 17, 7),
     (2, 2, 16, 16, 4),
     (1, 2, 21, 35, 5),
@@ -472,11 +477,13 @@ def test_hier_parity(shape, dtype):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
-@pytest.mark.parametrize("wl", [2, 3])
+@pytest.mark.parametrize("wl", [2, 3, 7])
 def test_hier_integer_data_bit_exact(wl, dtype):
     """Small integers in both tables and the data: every sum is exact in fp32
-    and below 256 in magnitude, so the GPU must equal the oracle exactly."""
-    B, C, H, Wd = 3, 2, 5 * wl, 4 * wl + 1
+    and below 256 in magnitude, so the GPU must equal the oracle exactly
+    (wl = 7: a tiled map with several slabs per channel, the one-pass table
+    gradients)."""
+    B, C, H, Wd = (3, 2, 5 * wl, 4 * wl + 1) if wl < 7 else (16, 2, 28, 28)
     r = np.random.default_rng(40 + wl)
     d = {}
     for k, shp in (("x", (B, C, H, Wd)), ("dy", (B, C, H, Wd)), ("t", (C, (4 * wl - 1) ** 2)),
@@ -490,6 +497,36 @@ def test_hier_integer_data_bit_exact(wl, dtype):
     assert np.array_equal(to_f64(dx), oracle.hier_backward_input(d["dy64"], d["t64"], d["tl64"], wl))
     wg_, wl_ = oracle.hier_backward_tables(d["x64"], d["dy64"], wl)
     assert np.array_equal(to_f64(dtg), wg_) and np.array_equal(to_f64(dtl), wl_)
+
+
+@pytest.mark.parametrize("name", list(synth.HIER_WORKLOADS))
+def test_hier_workload_full_size(name):
+    """The hierarchical workloads at full size, as the benchmark launches them;
+    the oracle runs on a channel sample.  The one-pass table gradients also
+    agree with the two single-scale table gradients (other summation order:
+    to 1e-5 of the largest entry)."""
+    wl = synth.HIER_WORKLOADS[name]
+    wloc = wl.w // 2
+    d = synth.draw_workload(wl, seed=0)
+    d["tl"], d["tl64"] = synth.draw_local_table(wl.C, wloc, wl.dtype, seed=0)
+    print("[workload] %s" % name, flush=True)
+    x, tg, tl, dy = (to_device(d[k], wl.dtype) for k in ("x", "t", "tl", "dy"))
+    y = W.wbmm_hier_forward(x, tg, tl, wloc)
+    dx, dtg, dtl = W.wbmm_hier_backward(x, dy, tg, tl, wloc)
+    sg = W.wbmm_backward_table(x, dy, 2 * wloc)
+    sl = W.wbmm_backward_table(x, dy, wloc)
+    torch.cuda.synchronize()
+    for a, b in ((dtg, sg), (dtl, sl)):
+        assert float((a - b).abs().max()) <= 1e-5 * float(b.abs().max())
+    ch = sampled_channels(wl.C)
+    xs, dys = d["x64"][:, ch], d["dy64"][:, ch]
+    tgs, tls = d["t64"][ch], d["tl64"][ch]
+    want = {"fwd": oracle.hier_forward(xs, tgs, tls, wloc), "dx": oracle.hier_backward_input(dys, tgs, tls, wloc)}
+    want["dtg"], want["dtl"] = oracle.hier_backward_tables(xs, dys, wloc)
+    got = {"fwd": to_f64(y)[:, ch], "dx": to_f64(dx)[:, ch], "dtg": to_f64(dtg)[ch], "dtl": to_f64(dtl)[ch]}
+    for k, v in got.items():
+        assert np.isfinite(v).all(), "%s %s: non-finite output" % (name, k)
+    check(got, want, wl.dtype, name)
 
 
 def test_hier_autograd_and_zero_tables():
