@@ -839,10 +839,11 @@ struct ImgCfg {
   static constexpr int RPP = rp_of(WIN) == 8 ? 4 : 2;       // window rows per output-tile pair
 };
 
-template <class Tag, int WIN>
+template <class Tag, int WIN, bool HIER = false>
 __host__ __device__ constexpr size_t fwd_img_lds_bytes() {
   typedef FwdCfg<Tag, WIN> G;
-  return (size_t)kFwdWaves * ImgCfg<WIN>::BUF_BYTES + (size_t)(G::TS_LEN + G::TB_LEN) * Tag::ES;
+  return (size_t)kFwdWaves * ImgCfg<WIN>::BUF_BYTES + (size_t)(G::TS_LEN + G::TB_LEN) * Tag::ES +
+         (HIER ? (size_t)(G::TSL_LEN + G::TBL_LEN) * Tag::ES : 0);
 }
 
 // Byte offset of chunk q of a sub-tile from the sub-tile's first element
@@ -855,9 +856,14 @@ __device__ __attribute__((always_inline)) inline uint32_t img_chunk(const ImgArg
   return q < nch ? off : 0x7fffffffu;
 }
 
-template <class Tag, int WIN, bool REV>
+// HIER: the hierarchical form (WIN = 2 wl, local table tabl): the local
+// sub-window blocks are extra products where input and output rows lie in
+// the same half of the window, and the two identity shortcuts add 2 x in
+// float32 before the single rounding.
+template <class Tag, int WIN, bool REV, bool HIER = false>
 __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_img_kernel(const typename Tag::S *__restrict__ x,
                                                                       const typename Tag::S *__restrict__ tab,
+                                                                      const typename Tag::S *__restrict__ tabl,
                                                                       typename Tag::S *__restrict__ y, KArgs a,
                                                                       ImgArgs ia) {
   typedef typename Tag::S S;
@@ -865,11 +871,14 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_img_kernel(const type
   typedef FwdCfg<Tag, WIN> G;
   typedef ImgCfg<WIN> IC;
   static_assert(Tag::W16, "image layout: 16-bit");
+  static_assert(!HIER || WIN % 2 == 0, "the hierarchical form needs an even window");
   constexpr int RP = G::RP, S_ = G::S, NT = G::NT, NB = G::NB, KC = IC::KC, RPP = IC::RPP;
 
   extern __shared__ __align__(16) unsigned char smem[];
   S *Ts = reinterpret_cast<S *>(smem + kFwdWaves * IC::BUF_BYTES);
   S *TB = Ts + G::TS_LEN;
+  S *Tsl = TB + G::TB_LEN;  // hierarchical form only
+  S *TBL = Tsl + G::TSL_LEN;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -927,11 +936,11 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_img_kernel(const type
     }
   };
 
-  TabRegs<Tag, WIN, false, kFwdThreads> tr;
-  tab_load<Tag, WIN, REV, false, kFwdThreads>(tab, nullptr, c, tid, tr);
+  TabRegs<Tag, WIN, HIER, kFwdThreads> tr;
+  tab_load<Tag, WIN, REV, HIER, kFwdThreads>(tab, tabl, c, tid, tr);
   uint4 nxt[KC];
   if (nsub > 0) load(n0 + first * 16, nxt);
-  fwd_tables<Tag, WIN, REV>(tr, Ts, TB, nullptr, nullptr, tid);
+  fwd_tables<Tag, WIN, REV, HIER>(tr, Ts, TB, Tsl, TBL, tid);
 
   for (int j = 0; j < nsub; ++j) {
     const int64_t m0 = n0 + (first + j) * 16;
@@ -998,6 +1007,12 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_img_kernel(const type
       for (int s = 0; s < S_; ++s) {
         acc0 = mma<Tag>(bf[2 * s - t0 + NT - 1], af[s], acc0);
         if (t0 + 1 < NT) acc1 = mma<Tag>(bf[2 * s - t0 - 1 + NT - 1], af[s], acc1);
+        if constexpr (HIER) {
+          // local sub-window blocks
+          if (fwd_rows_meet<Tag, WIN>(s, t0, true)) acc0 = mma<Tag>(fwd_lfrag<Tag, WIN>(TBL, s, t0, g, ln), af[s], acc0);
+          if (t0 + 1 < NT && fwd_rows_meet<Tag, WIN>(s, t0 + 1, true))
+            acc1 = mma<Tag>(fwd_lfrag<Tag, WIN>(TBL, s, t0 + 1, g, ln), af[s], acc1);
+        }
       }
       // results (M^T X^T): window ln, positions 16 t + 4 g .. + 3, i.e. one
       // window row ho, columns xo0 .. xo0 + 3; columns and rows beyond the
@@ -1010,16 +1025,26 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_img_kernel(const type
         const int ho = RP == 8 ? 2 * t + (g >> 1) : t;
         const int xo0 = RP == 8 ? 4 * (g & 1) : 4 * g;
         const int o = ab + (ho < WIN ? ho : 0) * ia.W + xo0;
-        const uint32_t lo = pack2<Tag>(acc[0], acc[1]);
-        const uint32_t hi = pack2<Tag>(acc[2], acc[3]);
         if constexpr ((WIN & 1) == 0) {
           // even windows: every window row starts at an even element
           uint32_t *o32 = reinterpret_cast<uint32_t *>(raw);
           const int da = (ho < WIN && xo0 < WIN) ? o : IC::DUMMY;
           const int db = (ho < WIN && xo0 + 2 < WIN) ? o + 2 : IC::DUMMY;
-          o32[da >> 1] = lo;
-          o32[db >> 1] = hi;
+          f32x4 r = acc;
+          if constexpr (HIER) {
+            // the two identity shortcuts: + 2 x at the output's own
+            // position, read before the result overwrites it
+            const uint32_t xa = o32[da >> 1], xb = o32[db >> 1];
+            r[0] += 2.f * to_f32<Tag>((u16)(xa & 0xffffu));
+            r[1] += 2.f * to_f32<Tag>((u16)(xa >> 16));
+            r[2] += 2.f * to_f32<Tag>((u16)(xb & 0xffffu));
+            r[3] += 2.f * to_f32<Tag>((u16)(xb >> 16));
+          }
+          o32[da >> 1] = pack2<Tag>(r[0], r[1]);
+          o32[db >> 1] = pack2<Tag>(r[2], r[3]);
         } else {
+          const uint32_t lo = pack2<Tag>(acc[0], acc[1]);
+          const uint32_t hi = pack2<Tag>(acc[2], acc[3]);
           const u16 vals[4] = {(u16)(lo & 0xffffu), (u16)(lo >> 16), (u16)(hi & 0xffffu), (u16)(hi >> 16)};
 #pragma unroll
           for (int rr = 0; rr < 4; ++rr) raw[(ho < WIN && xo0 + rr < WIN) ? o + rr : IC::DUMMY] = vals[rr];
@@ -2407,9 +2432,11 @@ static hipError_t run_forward(const void *x, const void *t, void *y, const Geom 
       constexpr size_t ilds = fwd_img_lds_bytes<Tag, WIN>();
       static_assert(ilds <= 65536, "workgroup LDS above 64 KB");
       if (rev)
-        wbmm_fwd_img_kernel<Tag, WIN, true><<<grid, dim3(kFwdThreads), ilds, st>>>((const S *)x, (const S *)t, (S *)y, a, ia);
+        wbmm_fwd_img_kernel<Tag, WIN, true><<<grid, dim3(kFwdThreads), ilds, st>>>((const S *)x, (const S *)t, nullptr,
+                                                                                  (S *)y, a, ia);
       else
-        wbmm_fwd_img_kernel<Tag, WIN, false><<<grid, dim3(kFwdThreads), ilds, st>>>((const S *)x, (const S *)t, (S *)y, a, ia);
+        wbmm_fwd_img_kernel<Tag, WIN, false><<<grid, dim3(kFwdThreads), ilds, st>>>((const S *)x, (const S *)t, nullptr,
+                                                                                   (S *)y, a, ia);
       return hipGetLastError();
     }
   }
@@ -2449,6 +2476,20 @@ static hipError_t run_hier_forward(const void *x, const void *tg, const void *tl
     a.tile = pick_fwd_tile<Tag, WIN>(g);
     a.tiles_per_ch = (int)cdiv64(g.N, a.tile);
     const dim3 grid((unsigned)(g.C * a.tiles_per_ch));
+    if constexpr (Tag::W16) {
+      ImgArgs ia;
+      if (img_layout<WIN>(g, x, y, ia)) {
+        constexpr size_t ilds = fwd_img_lds_bytes<Tag, WIN, true>();
+        static_assert(ilds <= 65536, "workgroup LDS above 64 KB");
+        if (rev)
+          wbmm_fwd_img_kernel<Tag, WIN, true, true><<<grid, dim3(kFwdThreads), ilds, st>>>(
+              (const S *)x, (const S *)tg, (const S *)tl, (S *)y, a, ia);
+        else
+          wbmm_fwd_img_kernel<Tag, WIN, false, true><<<grid, dim3(kFwdThreads), ilds, st>>>(
+              (const S *)x, (const S *)tg, (const S *)tl, (S *)y, a, ia);
+        return hipGetLastError();
+      }
+    }
     constexpr size_t lds = fwd_lds_bytes<Tag, WIN, true>();
     static_assert(lds <= 160 * 1024, "workgroup LDS above the 160 KB of a compute unit");
     if (rev)
