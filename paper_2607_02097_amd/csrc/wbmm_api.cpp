@@ -245,10 +245,18 @@ wbmm_status wbmm_hier_backward(const void *x, const void *dy, const void *table_
       if (overlap(workspace, (int64_t)need, b.p, b.n)) return WBMM_ERR_INVALID_ARG;
   }
   hipStream_t st = (hipStream_t)stream;
-  hipError_t e = wbmm::launch_hier_forward((Dt)dtype, dy, table_g, table_l, dx, gg, true, st);
-  bool both = false;
-  if (e == hipSuccess) e = wbmm::launch_hier_dtable((Dt)dtype, x, dy, dtable_g, dtable_l, workspace, need, gg, st, &both);
-  if (e == hipSuccess && !both) {
+  // one pass for all three gradients where it applies; else the input
+  // gradient (the forward kernel, tables reversed), then both table
+  // gradients in one pass or two launches
+  bool done = false;
+  hipError_t e = wbmm::launch_hier_stream((Dt)dtype, x, dy, table_g, table_l, dx, dtable_g, dtable_l, workspace,
+                                          need, gg, st, &done);
+  if (e != hipSuccess || done) return from_hip(e);
+  e = wbmm::launch_hier_forward((Dt)dtype, dy, table_g, table_l, dx, gg, true, st);
+  if (e == hipSuccess)
+    e = wbmm::launch_hier_stream((Dt)dtype, x, dy, nullptr, nullptr, nullptr, dtable_g, dtable_l, workspace, need,
+                                 gg, st, &done);
+  if (e == hipSuccess && !done) {
     e = wbmm::launch_dtable((Dt)dtype, x, dy, dtable_g, workspace, gg, st);
     if (e == hipSuccess) e = wbmm::launch_dtable((Dt)dtype, x, dy, dtable_l, workspace, gl, st);
   }

@@ -54,13 +54,14 @@ hipError_t launch_hier_forward(Dt dt, const void *x, const void *table_g, const 
   return e->hier_fwd(x, table_g, table_l, y, g, reverse_tables, stream);
 }
 
-hipError_t launch_hier_dtable(Dt dt, const void *x, const void *dy, float *dtable_g, float *dtable_l,
-                              void *workspace, size_t workspace_bytes, const Geom &g, hipStream_t stream,
-                              bool *done) {
+hipError_t launch_hier_stream(Dt dt, const void *x, const void *dy, const void *table_g, const void *table_l,
+                              void *dx, float *dtable_g, float *dtable_l, void *workspace, size_t workspace_bytes,
+                              const Geom &g, hipStream_t stream, bool *done) {
   *done = false;
   const Entry *e = find(dt, g.w);
   if (!e) return hipErrorInvalidValue;
-  return e->hier_dt(x, dy, dtable_g, dtable_l, workspace, workspace_bytes, g, stream, done);
+  return e->hier_stream(x, dy, table_g, table_l, dx, dtable_g, dtable_l, workspace, workspace_bytes, g, stream,
+                        done);
 }
 
 DtPlan plan_dtable(Dt dt, const Geom &g) {

@@ -23,7 +23,7 @@ namespace wbmm {
         &plan_dt<WBMM_INST_TAG, WBMM_INST_LO + W_>,                            \
         &run_backward<WBMM_INST_TAG, WBMM_INST_LO + W_>,                       \
         &run_hier_forward<WBMM_INST_TAG, WBMM_INST_LO + W_>,                   \
-        &run_hier_dtable<WBMM_INST_TAG, WBMM_INST_LO + W_>}
+        &run_hier_stream<WBMM_INST_TAG, WBMM_INST_LO + W_>}
 
 Entry WBMM_TABLE(WBMM_INST_TAG, WBMM_INST_LO)[8] = {
     WBMM_E(0), WBMM_E(1), WBMM_E(2), WBMM_E(3), WBMM_E(4), WBMM_E(5), WBMM_E(6), WBMM_E(7)};

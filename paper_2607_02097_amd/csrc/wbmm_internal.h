@@ -46,11 +46,13 @@ hipError_t launch_backward(Dt dt, const void *x, const void *dy, const void *tab
 hipError_t launch_hier_forward(Dt dt, const void *x, const void *table_g,
                                const void *table_l, void *y, const Geom &g,
                                bool reverse_tables, hipStream_t stream);
-// Both table gradients of the hierarchical form in one pass where that
-// applies (*done); otherwise nothing is launched and *done is false.
-hipError_t launch_hier_dtable(Dt dt, const void *x, const void *dy, float *dtable_g,
-                              float *dtable_l, void *workspace, size_t workspace_bytes,
-                              const Geom &g, hipStream_t stream, bool *done);
+// Hierarchical form in one pass where that applies (*done): both table
+// gradients, and the input gradient too when dx is not null; otherwise
+// nothing is launched and *done is false.
+hipError_t launch_hier_stream(Dt dt, const void *x, const void *dy, const void *table_g,
+                              const void *table_l, void *dx, float *dtable_g, float *dtable_l,
+                              void *workspace, size_t workspace_bytes, const Geom &g,
+                              hipStream_t stream, bool *done);
 
 // Cached-matrix (dense) form, any w_h x w_w window with d = w_h w_w <= 256
 // (wbmm_dense.hip).  g.w is unused by these.
@@ -71,15 +73,15 @@ typedef DtPlan (*PlanFn)(const Geom &);
 typedef hipError_t (*BwdFn)(const void *, const void *, const void *, void *, float *, void *, const Geom &,
                             hipStream_t);
 typedef hipError_t (*HierFn)(const void *, const void *, const void *, void *, const Geom &, bool, hipStream_t);
-typedef hipError_t (*HierDtFn)(const void *, const void *, float *, float *, void *, size_t, const Geom &,
-                               hipStream_t, bool *);
+typedef hipError_t (*HierStreamFn)(const void *, const void *, const void *, const void *, void *, float *,
+                                   float *, void *, size_t, const Geom &, hipStream_t, bool *);
 struct Entry {
   FwdFn fwd;
   DtFn dtable;
   PlanFn plan;
   BwdFn bwd;
   HierFn hier_fwd;
-  HierDtFn hier_dt;
+  HierStreamFn hier_stream;
 };
 
 }  // namespace wbmm

@@ -536,8 +536,8 @@ __device__ __attribute__((always_inline)) inline void tab_load(const typename Ta
 // stages the local table (-> Tsl) and, for 16-bit, its blocks
 // TBL[dh][x_out][x_in], zero unless x_in and x_out lie in the same half of the
 // window (the same local sub-window column).  Ends with a workgroup barrier.
-template <class Tag, int WIN, bool REV, bool HIER = false>
-__device__ __attribute__((always_inline)) inline void fwd_tables(const TabRegs<Tag, WIN, HIER, kFwdThreads> &tr,
+template <class Tag, int WIN, bool REV, bool HIER = false, int NTH = kFwdThreads>
+__device__ __attribute__((always_inline)) inline void fwd_tables(const TabRegs<Tag, WIN, HIER, NTH> &tr,
                                                                   typename Tag::S *Ts, typename Tag::S *TB,
                                                                   typename Tag::S *Tsl, typename Tag::S *TBL, int tid) {
   typedef typename Tag::S S;
@@ -545,14 +545,14 @@ __device__ __attribute__((always_inline)) inline void fwd_tables(const TabRegs<T
   constexpr int RP = G::RP, K1 = G::K1, K2 = G::K2;
 #pragma unroll
   for (int i = 0; i < tr.N; ++i) {
-    const int k = tid + i * kFwdThreads;
+    const int k = tid + i * NTH;
     if (k < K2) Ts[k] = tr.v[i];
   }
   if constexpr (HIER) {
     constexpr int K2L = G::K2L;
 #pragma unroll
     for (int i = 0; i < tr.NL; ++i) {
-      const int k = tid + i * kFwdThreads;
+      const int k = tid + i * NTH;
       if (k < K2L) Tsl[k] = tr.vl[i];
     }
   }
@@ -560,7 +560,7 @@ __device__ __attribute__((always_inline)) inline void fwd_tables(const TabRegs<T
     __syncthreads();
     constexpr int CPR = RP / 8;               // 8-element chunks per TB row
     constexpr int NCH = K1 * RP * CPR;
-    for (int ch = tid; ch < NCH; ch += kFwdThreads) {
+    for (int ch = tid; ch < NCH; ch += NTH) {
       const int row = ch / CPR;               // = dhi * RP + x_out
       const int xi0 = (ch - row * CPR) * 8;
       const int dhi = row / RP;
@@ -572,7 +572,7 @@ __device__ __attribute__((always_inline)) inline void fwd_tables(const TabRegs<T
     if constexpr (HIER) {
       constexpr int WL = G::WL, K1L = G::K1L;
       constexpr int NCHL = K1L * RP * CPR;
-      for (int ch = tid; ch < NCHL; ch += kFwdThreads) {
+      for (int ch = tid; ch < NCHL; ch += NTH) {
         const int row = ch / CPR;               // = dhl * RP + x_out
         const int xi0 = (ch - row * CPR) * 8;
         const int dhl = row / RP;
@@ -1815,10 +1815,15 @@ __global__ __launch_bounds__(kThreads, 3) void wbmm_dt_kernel(const typename Tag
 // outermost (all its output tiles accumulate at once), each tile's sum over
 // K in the forward's order.  The rounded results go to Obuf (window-major,
 // the x stage, no longer read).
-template <class Tag, int WIN, int WAVE, int NDX = kWaves>
+// HL > 0: the hierarchical form's input gradient (WIN = 2 HL; Tsl / TBL hold
+// the reversed local table and its blocks): per K step the local-block
+// product follows the global one, and 2 dY is added before the rounding, as
+// in the forward kernels, so the result equals theirs bit for bit.
+template <class Tag, int WIN, int WAVE, int NDX = kWaves, int HL = 0>
 __device__ __attribute__((always_inline)) inline void dx_products(const unsigned char *Dbuf, unsigned char *Obuf,
                                                                    const typename Tag::S *Ts, const typename Tag::S *TB,
-                                                                   int lane) {
+                                                                   int lane, const typename Tag::S *Tsl = nullptr,
+                                                                   const typename Tag::S *TBL = nullptr) {
   typedef typename Tag::S S;
   typedef typename Tag::Frag Frag;
   typedef BwdCfg<Tag, WIN> G;
@@ -1860,11 +1865,23 @@ __device__ __attribute__((always_inline)) inline void dx_products(const unsigned
         }
         const Frag af = *reinterpret_cast<const Frag *>(&rowp[ln * LDSW + s * 32 + 8 * g]);
 #pragma unroll
-        for (int j = 0; j < NTW; ++j) acc[j] = mma<Tag>(af, bf[2 * s - (T0 + j) + NT - 1], acc[j]);
+        for (int j = 0; j < NTW; ++j) {
+          acc[j] = mma<Tag>(af, bf[2 * s - (T0 + j) + NT - 1], acc[j]);
+          if constexpr (HL > 0) {
+            if (fwd_rows_meet<Tag, WIN>(s, T0 + j, true))
+              acc[j] = mma<Tag>(af, fwd_lfrag<Tag, WIN>(TBL, s, T0 + j, g, ln), acc[j]);
+          }
+        }
       }
 #pragma unroll
       for (int j = 0; j < NTW; ++j) {
         const int t = T0 + j;
+        if constexpr (HL > 0) {
+          // the two identity shortcuts: + 2 dY at the output's own position
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr)
+            acc[j][rr] += 2.f * to_f32<Tag>(reinterpret_cast<const u16 *>(rowp)[(4 * g + rr) * LDSW + 16 * t + ln]);
+        }
         const uint32_t lo = pack2<Tag>(acc[j][0], acc[j][1]);
         const uint32_t hi = pack2<Tag>(acc[j][2], acc[j][3]);
         outp[0 * LDSW + 16 * t] = (u16)(lo & 0xffffu);
@@ -1886,6 +1903,13 @@ __device__ __attribute__((always_inline)) inline void dx_products(const unsigned
           float bv = 0.f;
           if (xo < WIN && xi < WIN && dh >= -(WIN - 1) && dh <= WIN - 1)
             bv = Ts[(dh + WIN - 1) * K1 + xi - xo + WIN - 1];
+          if constexpr (HL > 0) {
+            // local sub-window entry and the two identity shortcuts
+            constexpr int K1L = 2 * HL - 1;
+            if (xo < WIN && xi < WIN && hi < WIN && ho < WIN && (hi < HL) == (ho < HL) && (xi < HL) == (xo < HL))
+              bv += Tsl[(dh + HL - 1) * K1L + xi - xo + HL - 1];
+            if (hi == ho && xi == xo && xi < WIN && hi < WIN) bv += 2.f;
+          }
           acc[j] = mma<Tag>(af, bv, acc[j]);
         }
       }
@@ -2061,13 +2085,17 @@ struct StreamCfg {
   static constexpr int TS_OFF = O_OFF + 2 * G::BUF;
   static constexpr int TB_OFF = TS_OFF + rup(F::TS_LEN * Tag::ES, 16);
   static constexpr int END = TB_OFF + F::TB_LEN * Tag::ES;
+  // hierarchical form: the local table row and its blocks after them
+  static constexpr int TSL_OFF = rup(END, 16);
+  static constexpr int TBL_OFF = TSL_OFF + rup(F::TSL_LEN * Tag::ES, 16);
+  static constexpr int END_H = TBL_OFF + F::TBL_LEN * Tag::ES;
   static_assert(kStreamWaves % NCP == 0, "whole waves per copy");
   static_assert(bins_lds_bytes<G>() <= O_OFF, "bins must not reach the dX buffers");
 };
 
-template <class Tag, int WIN>
+template <class Tag, int WIN, bool HIER = false>
 __host__ __device__ constexpr size_t stream_lds_bytes() {
-  return (size_t)StreamCfg<Tag, WIN>::END;
+  return (size_t)(HIER ? StreamCfg<Tag, WIN>::END_H : StreamCfg<Tag, WIN>::END);
 }
 
 template <class Tag, int WIN>
@@ -2169,6 +2197,7 @@ template <class Tag, int WIN, int DTW, int DXW, bool DX, int HL>
 __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S *__restrict__ x,
                                                            const typename Tag::S *__restrict__ dy,
                                                            const typename Tag::S *__restrict__ tab,
+                                                           const typename Tag::S *__restrict__ tabl,
                                                            typename Tag::S *__restrict__ dx, float *__restrict__ dt,
                                                            float *__restrict__ part, unsigned *__restrict__ cnt,
                                                            const KArgs &a, unsigned char *smem,
@@ -2188,6 +2217,8 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
   const int nst = (int)((s1 - s0 + CW - 1) / CW);
   S *Ts = reinterpret_cast<S *>(smem + SC::TS_OFF);
   S *TB = reinterpret_cast<S *>(smem + SC::TB_OFF);
+  S *Tsl = reinterpret_cast<S *>(smem + SC::TSL_OFF);  // hierarchical input gradient only
+  S *TBL = reinterpret_cast<S *>(smem + SC::TBL_OFF);
 
   f32x4 acc[SP::na], accl[SP::na];
 #pragma unroll
@@ -2196,11 +2227,14 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
   // the reversed table row and stage 0 in flight (the table first, ahead
   // of the bulk loads); the table row and (16-bit) its Toeplitz blocks ->
   // LDS; stage 0 -> LDS buffer 0, stage 1 in flight
-  TabRegs<Tag, WIN, false, kStreamThreads> tr;
-  if constexpr (DX) tab_load<Tag, WIN, true, false, kStreamThreads>(tab, nullptr, c, tid, tr);
+  constexpr bool HX = DX && HL > 0;  // hierarchical input gradient: both tables
+  TabRegs<Tag, WIN, HX, kStreamThreads> tr;
+  if constexpr (DX) tab_load<Tag, WIN, true, HX, kStreamThreads>(tab, tabl, c, tid, tr);
   StreamRows<Tag, WIN> st;
   stream_load<Tag, WIN>(a, x, dy, c, s0, s1, wave, lane, st);
-  if constexpr (DX) {
+  if constexpr (HX) {
+    fwd_tables<Tag, WIN, true, true, kStreamThreads>(tr, Ts, TB, Tsl, TBL, tid);
+  } else if constexpr (DX) {
 #pragma unroll
     for (int i = 0; i < tr.N; ++i)
       if (tid + i * kStreamThreads < K2) Ts[tid + i * kStreamThreads] = tr.v[i];
@@ -2231,7 +2265,7 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
     if constexpr (DTW >= 0) {
       dt_products_split<Tag, G, DTW, HL>(cur, cur + G::BUF, acc, accl, lane);
     } else if constexpr (DX) {
-      dx_products<Tag, WIN, DXW, kStreamWaves - kStreamDt>(cur + G::BUF, obuf, Ts, TB, lane);
+      dx_products<Tag, WIN, DXW, kStreamWaves - kStreamDt, (HX ? HL : 0)>(cur + G::BUF, obuf, Ts, TB, lane, Tsl, TBL);
     }
     // the next stage into the other buffer (free since the last barrier),
     // the one after it in flight, the previous stage's dX rows out
@@ -2285,20 +2319,21 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
   }
 }
 
-// HL > 0: the hierarchical form's two table gradients (global window WIN,
-// local window HL = WIN / 2) from one pass, DX false.
+// HL > 0: the hierarchical form (global window WIN, local window
+// HL = WIN / 2): both table gradients from one pass, and with DX the input
+// gradient of the fused matrix (tables tab and tabl, read back to front).
 template <class Tag, int WIN, bool DX, int HL = 0>
 __global__ __launch_bounds__(kStreamThreads, 3) void wbmm_bwd_stream_kernel(
     const typename Tag::S *__restrict__ x, const typename Tag::S *__restrict__ dy,
     const typename Tag::S *__restrict__ tab, typename Tag::S *__restrict__ dx, float *__restrict__ dt,
     float *__restrict__ part, unsigned *__restrict__ cnt, KArgs a, float *__restrict__ dtl,
-    float *__restrict__ partl) {
-  static_assert(HL == 0 || (!DX && 2 * HL == WIN), "local table gradient: table gradients only, WIN = 2 HL");
+    float *__restrict__ partl, const typename Tag::S *__restrict__ tabl) {
+  static_assert(HL == 0 || 2 * HL == WIN, "hierarchical form: WIN = 2 HL");
   static_assert(HL == 0 || bins_lds_bytes<BwdCfg<Tag, WIN>>() + (size_t)(2 * HL - 1) * (2 * HL - 1) * 4 <=
                                (size_t)StreamCfg<Tag, WIN>::O_OFF,
                 "both tables' bins within the stage buffers");
   extern __shared__ __align__(16) unsigned char smem[];
-#define WBMM_SW(D, X) stream_wave<Tag, WIN, D, X, DX, HL>(x, dy, tab, dx, dt, part, cnt, a, smem, dtl, partl)
+#define WBMM_SW(D, X) stream_wave<Tag, WIN, D, X, DX, HL>(x, dy, tab, tabl, dx, dt, part, cnt, a, smem, dtl, partl)
   switch (threadIdx.x >> 6) {
     case 0: WBMM_SW(0, -1); break;
     case 1: WBMM_SW(1, -1); break;
@@ -2554,7 +2589,7 @@ static hipError_t run_dtable(const void *x, const void *dy, float *dt, void *ws,
       float *spart = b.tiles_per_ch > 1 ? (float *)((char *)ws + counter_bytes(g.C)) : nullptr;
       constexpr size_t slds = stream_lds_bytes<Tag, WIN>();
       wbmm_bwd_stream_kernel<Tag, WIN, false><<<dim3((unsigned)(g.C * b.tiles_per_ch)), dim3(kStreamThreads), slds, st>>>(
-          (const S *)x, (const S *)dy, nullptr, nullptr, dt, spart, scnt, b, nullptr, nullptr);
+          (const S *)x, (const S *)dy, nullptr, nullptr, dt, spart, scnt, b, nullptr, nullptr, nullptr);
       return hipGetLastError();
     }
   }
@@ -2590,7 +2625,7 @@ static hipError_t run_backward(const void *x, const void *dy, const void *t, voi
       constexpr size_t slds = stream_lds_bytes<Tag, WIN>();
       static_assert(slds <= 160 * 1024, "workgroup LDS above the 160 KB of a compute unit");
       wbmm_bwd_stream_kernel<Tag, WIN, true><<<dim3((unsigned)(g.C * b.tiles_per_ch)), dim3(kStreamThreads), slds, st>>>(
-          (const S *)x, (const S *)dy, (const S *)t, (S *)dx, dt, spart, scnt, b, nullptr, nullptr);
+          (const S *)x, (const S *)dy, (const S *)t, (S *)dx, dt, spart, scnt, b, nullptr, nullptr, nullptr);
       return hipGetLastError();
     }
   }
@@ -2611,13 +2646,14 @@ static hipError_t run_backward(const void *x, const void *dy, const void *t, voi
   return hipGetLastError();
 }
 
-// Hierarchical form (global window WIN = 2 wl): both table gradients in one
-// channel-stream pass when it applies (one window row per tile, fixed-offset
-// rows, no more channels than compute units, and the workspace holds both
-// tables' partials); *done tells whether it ran.
+// Hierarchical form (global window WIN = 2 wl): one channel-stream pass when
+// it applies (one window row per tile, fixed-offset rows, no more channels
+// than compute units, and the workspace holds both tables' partials): both
+// table gradients, and with dx the input gradient too; *done tells whether
+// it ran.
 template <class Tag, int WIN>
-static hipError_t run_hier_dtable(const void *x, const void *dy, float *dtg, float *dtl, void *ws, size_t ws_bytes,
-                                  const Geom &g, hipStream_t st, bool *done) {
+static hipError_t run_hier_stream(const void *x, const void *dy, const void *tg, const void *tl, void *dx, float *dtg,
+                                  float *dtl, void *ws, size_t ws_bytes, const Geom &g, hipStream_t st, bool *done) {
   *done = false;
   if constexpr (WIN % 2 == 0 && rp_of(WIN) == 16) {
     typedef typename Tag::S S;
@@ -2627,7 +2663,8 @@ static hipError_t run_hier_dtable(const void *x, const void *dy, float *dtg, flo
     const DtPlan p = plan_dt<Tag, WIN>(g);
     a.tile = (int)p.slab_windows;
     a.tiles_per_ch = (int)p.slabs;
-    set_tiled<WIN, Tag::ES>(g, a, {x, dy});
+    if (dx) set_tiled<WIN, Tag::ES>(g, a, {x, dy, dx});
+    else set_tiled<WIN, Tag::ES>(g, a, {x, dy});
     KArgs b = a;
     if (!stream_plan<Tag, WIN>(g, b)) return hipSuccess;
     unsigned *cnt = nullptr;
@@ -2639,13 +2676,22 @@ static hipError_t run_hier_dtable(const void *x, const void *dy, float *dtg, flo
       partg = (float *)((char *)ws + counter_bytes(g.C));
       partl = partg + (size_t)b.tiles_per_ch * (size_t)g.C * (size_t)K2;
     }
-    constexpr size_t slds = stream_lds_bytes<Tag, WIN>();
-    wbmm_bwd_stream_kernel<Tag, WIN, false, WL><<<dim3((unsigned)(g.C * b.tiles_per_ch)), dim3(kStreamThreads), slds, st>>>(
-        (const S *)x, (const S *)dy, nullptr, nullptr, dtg, partg, cnt, b, dtl, partl);
+    const dim3 grid((unsigned)(g.C * b.tiles_per_ch));
+    if (dx) {
+      constexpr size_t slds = stream_lds_bytes<Tag, WIN, true>();
+      static_assert(slds <= 160 * 1024, "workgroup LDS above the 160 KB of a compute unit");
+      wbmm_bwd_stream_kernel<Tag, WIN, true, WL><<<grid, dim3(kStreamThreads), slds, st>>>(
+          (const S *)x, (const S *)dy, (const S *)tg, (S *)dx, dtg, partg, cnt, b, dtl, partl, (const S *)tl);
+    } else {
+      constexpr size_t slds = stream_lds_bytes<Tag, WIN>();
+      wbmm_bwd_stream_kernel<Tag, WIN, false, WL><<<grid, dim3(kStreamThreads), slds, st>>>(
+          (const S *)x, (const S *)dy, nullptr, nullptr, dtg, partg, cnt, b, dtl, partl, nullptr);
+    }
     *done = true;
     return hipGetLastError();
   } else {
-    (void)x; (void)dy; (void)dtg; (void)dtl; (void)ws; (void)ws_bytes; (void)g; (void)st;
+    (void)x; (void)dy; (void)tg; (void)tl; (void)dx; (void)dtg; (void)dtl; (void)ws; (void)ws_bytes; (void)g;
+    (void)st;
     return hipSuccess;
   }
 }
