@@ -379,9 +379,10 @@ def main():
     kernel_name = {"fwd": fk + "<%s,%d,false>", "dx": fk + "<%s,%d,true>",
                    "dt": dtk + "<%s,%d," + ("false" if chan_stream else tl) + ">",
                    "bwd": bwk + "<%s,%d," + ("true" if chan_stream else tl) + ">",
-                   "hfwd": "wbmm_fwd_kernel<%s,%d,false,true>",
-                   "hbwd": "wbmm_hier_backward (3 launches) <%s,%d>"}[dom] % ({"bf16": "TagBF16", "f16": "TagF16",
-                                                          "f32": "TagF32"}[wl.dtype], wl.w)
+                   "hfwd": fk + "<%s,%d,false,true>",
+                   "hbwd": ("wbmm_bwd_stream_kernel<%s,%d,true," + str(wl.w // 2) + ">") if chan_stream and wl.w >= 10
+                           else "wbmm_hier_backward (several launches) <%s,%d>"}[dom] % (
+                       {"bf16": "TagBF16", "f16": "TagF16", "f32": "TagF32"}[wl.dtype], wl.w)
     if ai < ridge:
         achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
