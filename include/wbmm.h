@@ -153,17 +153,22 @@ wbmm_status wbmm_hier_backward_input(const void *dy, const void *table_g,
                                      int64_t C, int64_t H, int64_t W, int wl,
                                      wbmm_dtype dtype, void *stream);
 
-/* Workspace for wbmm_hier_backward (the larger of the two table gradients'
- * needs; same rules as for wbmm_backward_table). */
+/* Workspace for wbmm_hier_backward: enough for the two table gradients run
+ * one after the other and for both computed in one pass (per-channel
+ * counters and both tables' slab partials); same rules as for
+ * wbmm_backward_table (counters zero before the first call, left zero). */
 size_t wbmm_hier_backward_workspace_bytes(int64_t B, int64_t C, int64_t H,
                                           int64_t W, int wl, wbmm_dtype dtype);
 
-/* All gradients of the hierarchical form: dx as wbmm_hier_backward_input;
- * dtable_g = the table gradient with windows 2 wl, dtable_l = the table
- * gradient with windows wl (the local sub-windows of the padded global
- * windows are the wl windows of the map); both float32, overwritten.  Three
- * launches on `stream`, sharing the workspace one after the other.  Outputs
- * must not overlap inputs, each other or the workspace. */
+/* All gradients of the hierarchical form: dx as wbmm_hier_backward_input
+ * (bit for bit); dtable_g = the table gradient with windows 2 wl, dtable_l =
+ * the table gradient with windows wl (the local sub-windows of the padded
+ * global windows are the wl windows of the map); both float32, overwritten.
+ * One launch on `stream` where the channel-stream pass applies (2 wl >= 10,
+ * maps tiled by the global window with 4-byte aligned rows, C at most the
+ * device's compute units); otherwise the input gradient, then the two table
+ * gradients in one launch or two.  Outputs must not overlap inputs, each
+ * other or the workspace. */
 wbmm_status wbmm_hier_backward(const void *x, const void *dy,
                                const void *table_g, const void *table_l,
                                void *dx, float *dtable_g, float *dtable_l,

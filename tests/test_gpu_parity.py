@@ -529,6 +529,26 @@ def test_hier_workload_full_size(name):
     check(got, want, wl.dtype, name)
 
 
+def test_hier_workspace_counters_reset_between_calls():
+    """The one-pass hierarchical backward with several slabs per channel
+    leaves its counters at zero: repeated calls on one workspace, and a
+    smaller shape in between, equal a fresh workspace bit for bit."""
+    wl = synth.HIER_WORKLOADS["bf16_b16_c64_112_hier7"]
+    d = synth.draw_workload(wl, seed=6)
+    d["tl"], d["tl64"] = synth.draw_local_table(wl.C, 7, wl.dtype, seed=6)
+    x, tg, tl, dy = (to_device(d[k], wl.dtype) for k in ("x", "t", "tl", "dy"))
+    need = W.wbmm_hier_backward_workspace_bytes(x.shape, 7, x.dtype)
+    ref = W.wbmm_hier_backward(x, dy, tg, tl, 7, workspace=W.new_workspace(need))
+    ws = W.new_workspace(need)
+    for _ in range(3):
+        got = W.wbmm_hier_backward(x, dy, tg, tl, 7, workspace=ws)
+        W.wbmm_hier_backward(x[:4, :16].contiguous(), dy[:4, :16].contiguous(), tg[:16].contiguous(),
+                             tl[:16].contiguous(), 7, workspace=ws)
+        torch.cuda.synchronize()
+        for a, b in zip(got, ref):
+            assert torch.equal(a, b)
+
+
 def test_hier_autograd_and_zero_tables():
     d = draw_hier(2, 3, 14, 21, 7, "f32", seed=33)
     x = to_device(d["x"], "f32").requires_grad_(True)
