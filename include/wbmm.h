@@ -164,10 +164,11 @@ size_t wbmm_hier_backward_workspace_bytes(int64_t B, int64_t C, int64_t H,
  * (bit for bit); dtable_g = the table gradient with windows 2 wl, dtable_l =
  * the table gradient with windows wl (the local sub-windows of the padded
  * global windows are the wl windows of the map); both float32, overwritten.
- * One launch on `stream` where the channel-stream pass applies (2 wl >= 10,
- * maps tiled by the global window with 4-byte aligned rows, C at most the
- * device's compute units); otherwise the input gradient, then the two table
- * gradients in one launch or two.  Outputs must not overlap inputs, each
+ * One launch on `stream` where the channel-stream pass applies (2 wl >= 10;
+ * H and W multiples of 2 wl, a power of two of at most 16 windows per map
+ * row, windows per image a multiple or a divisor of 16; 4-byte aligned
+ * tensors; C at most the device's compute units); otherwise the input
+ * gradient, then the two table gradients in one launch or two.  Outputs must not overlap inputs, each
  * other or the workspace. */
 wbmm_status wbmm_hier_backward(const void *x, const void *dy,
                                const void *table_g, const void *table_l,
