@@ -56,11 +56,11 @@ def parse():
 # on (sha256 of the kernel header); otherwise reported as null.
 TRAFFIC = {
     # (workload, kernel): measured bytes per dispatch (profiles/wbmm_traffic_*.txt)
-    ("bf16_b64_c192_28_w14", "bwd"): {"source": "20674b9b95627877", "bytes": 62608065},
-    ("bf16_b64_c192_28_w14", "fwd"): {"source": "20674b9b95627877", "bytes": 41254879},
-    ("bf16_b64_c192_28_w14", "dx"): {"source": "20674b9b95627877", "bytes": 41199352},
-    ("bf16_b64_c192_28_w14", "dt"): {"source": "20674b9b95627877", "bytes": 42201010},
-    ("bf16_b64_c96_56_w7", "fwd"): {"source": "20674b9b95627877", "bytes": 77530540},
+    ("bf16_b64_c192_28_w14", "bwd"): {"source": "c36f0ddf1fb169d6", "bytes": 62598093},
+    ("bf16_b64_c192_28_w14", "fwd"): {"source": "c36f0ddf1fb169d6", "bytes": 41268863},
+    ("bf16_b64_c192_28_w14", "dx"): {"source": "c36f0ddf1fb169d6", "bytes": 41231065},
+    ("bf16_b64_c192_28_w14", "dt"): {"source": "c36f0ddf1fb169d6", "bytes": 42201521},
+    ("bf16_b64_c96_56_w7", "fwd"): {"source": "c36f0ddf1fb169d6", "bytes": 77496155},
 }
 
 
@@ -376,10 +376,14 @@ def main():
     chan_stream = fixed_offset_rows(wl) and wl.C <= torch.cuda.get_device_properties(0).multi_processor_count
     dtk = "wbmm_bwd_stream_kernel" if chan_stream else "wbmm_dt_kernel"
     bwk = "wbmm_bwd_stream_kernel" if chan_stream else "wbmm_bwd_kernel"
-    kernel_name = {"fwd": fk + "<%s,%d,false>", "dx": fk + "<%s,%d,true>",
-                   "dt": dtk + "<%s,%d," + ("false" if chan_stream else tl) + ">",
-                   "bwd": bwk + "<%s,%d," + ("true" if chan_stream else tl) + ">",
-                   "hfwd": fk + "<%s,%d,false,true>",
+    # names as the profiler prints them (every template argument)
+    img = fk == "wbmm_fwd_img_kernel"
+    fwd_tail = (lambda rev, hier: "<%s,%d," + rev + "," + hier + ">") if img else \
+        (lambda rev, hier: "<%s,%d," + rev + "," + hier + "," + (tl if hier == "false" else "false") + ">")
+    kernel_name = {"fwd": fk + fwd_tail("false", "false"), "dx": fk + fwd_tail("true", "false"),
+                   "dt": dtk + ("<%s,%d,false,0>" if chan_stream else "<%s,%d," + tl + ">"),
+                   "bwd": bwk + ("<%s,%d,true,0>" if chan_stream else "<%s,%d," + tl + ">"),
+                   "hfwd": fk + fwd_tail("false", "true"),
                    "hbwd": ("wbmm_bwd_stream_kernel<%s,%d,true," + str(wl.w // 2) + ">") if chan_stream and wl.w >= 10
                            else "wbmm_hier_backward (several launches) <%s,%d>"}[dom] % (
                        {"bf16": "TagBF16", "f16": "TagF16", "f32": "TagF32"}[wl.dtype], wl.w)
