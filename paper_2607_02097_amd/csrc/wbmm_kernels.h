@@ -1815,15 +1815,32 @@ __global__ __launch_bounds__(kThreads, 3) void wbmm_dt_kernel(const typename Tag
 // outermost (all its output tiles accumulate at once), each tile's sum over
 // K in the forward's order.  The rounded results go to Obuf (window-major,
 // the x stage, no longer read).
+// Input-gradient work of wave WAVE of NDX: sub-tile SUB of the stage,
+// output tiles [T0, T1); 16-bit B fragments q = 2 s - t + NT - 1 of its
+// steps and tiles run over [QLO, QLO + NQ).
+template <class Tag, int WIN, int WAVE, int NDX>
+struct DxSplit {
+  typedef BwdCfg<Tag, WIN> G;
+  typedef FwdCfg<Tag, WIN> F;
+  static constexpr int NT = F::NT, S_ = F::S;
+  static constexpr int WPS = NDX / G::SUBS;  // waves per sub-tile
+  static constexpr int SUB = WAVE % G::SUBS, PART = WAVE / G::SUBS;
+  static constexpr int T0 = PART * NT / WPS, T1 = (PART + 1) * NT / WPS, NTW = T1 - T0;
+  static constexpr int QLO = NT - T1;
+  static constexpr int NQ = NTW > 0 ? 2 * S_ - 2 + NTW : 1;
+};
+
 // HL > 0: the hierarchical form's input gradient (WIN = 2 HL; Tsl / TBL hold
 // the reversed local table and its blocks): per K step the local-block
 // product follows the global one, and 2 dY is added before the rounding, as
-// in the forward kernels, so the result equals theirs bit for bit.
-template <class Tag, int WIN, int WAVE, int NDX = kWaves, int HL = 0>
-__device__ __attribute__((always_inline)) inline void dx_products(const unsigned char *Dbuf, unsigned char *Obuf,
-                                                                   const typename Tag::S *Ts, const typename Tag::S *TB,
-                                                                   int lane, const typename Tag::S *Tsl = nullptr,
-                                                                   const typename Tag::S *TBL = nullptr) {
+// in the forward kernels, so the result equals theirs bit for bit.  PRE:
+// the wave's 16-bit B fragments come preloaded in bfw (the table does not
+// change between stages) instead of being read from TB.
+template <class Tag, int WIN, int WAVE, int NDX = kWaves, int HL = 0, bool PRE = false>
+__device__ __attribute__((always_inline)) inline void dx_products(
+    const unsigned char *Dbuf, unsigned char *Obuf, const typename Tag::S *Ts, const typename Tag::S *TB, int lane,
+    const typename Tag::S *Tsl = nullptr, const typename Tag::S *TBL = nullptr,
+    const typename Tag::Frag (*bfw)[DxSplit<Tag, WIN, WAVE, NDX>::NQ] = nullptr) {
   typedef typename Tag::S S;
   typedef typename Tag::Frag Frag;
   typedef BwdCfg<Tag, WIN> G;
@@ -1853,41 +1870,49 @@ __device__ __attribute__((always_inline)) inline void dx_products(const unsigned
         return Frag{0, 0, 0, 0, 0, 0, 0, 0};
       };
       // fragment q = 2s - t + NT - 1 serves steps s with T0 <= t < T1; it is
-      // read from LDS at the first of them
+      // read from LDS at the first of them (or preloaded)
+      constexpr int QLO = DxSplit<Tag, WIN, WAVE, NDX>::QLO, NQ = DxSplit<Tag, WIN, WAVE, NDX>::NQ;
       Frag bf[NB];
+      if constexpr (PRE) {
+#pragma unroll
+        for (int i = 0; i < NQ; ++i) bf[QLO + i] = (*bfw)[i];
+      }
 #pragma unroll
       for (int s = 0; s < S_; ++s) {
+        if constexpr (!PRE) {
 #pragma unroll
-        for (int q = 0; q < NB; ++q) {
-          const int lo = 2 * s + NT - T1, hi = 2 * s + NT - 1 - T0;  // fragments of step s
-          const bool first = s == 0 ? true : !(q >= lo - 2 && q <= hi - 2);
-          if (q >= lo && q <= hi && first) bf[q] = load_bf(q);
+          for (int q = 0; q < NB; ++q) {
+            const int lo = 2 * s + NT - T1, hi = 2 * s + NT - 1 - T0;  // fragments of step s
+            const bool first = s == 0 ? true : !(q >= lo - 2 && q <= hi - 2);
+            if (q >= lo && q <= hi && first) bf[q] = load_bf(q);
+          }
         }
         const Frag af = *reinterpret_cast<const Frag *>(&rowp[ln * LDSW + s * 32 + 8 * g]);
+        // operands swapped (the product is (dY M^T)^T): a lane's four
+        // results are consecutive positions of one window, as in the forward
 #pragma unroll
         for (int j = 0; j < NTW; ++j) {
-          acc[j] = mma<Tag>(af, bf[2 * s - (T0 + j) + NT - 1], acc[j]);
+          acc[j] = mma<Tag>(bf[2 * s - (T0 + j) + NT - 1], af, acc[j]);
           if constexpr (HL > 0) {
             if (fwd_rows_meet<Tag, WIN>(s, T0 + j, true))
-              acc[j] = mma<Tag>(af, fwd_lfrag<Tag, WIN>(TBL, s, T0 + j, g, ln), acc[j]);
+              acc[j] = mma<Tag>(fwd_lfrag<Tag, WIN>(TBL, s, T0 + j, g, ln), af, acc[j]);
           }
         }
       }
+      // window ln, positions 16 t + 4 g .. + 3: one 8-byte write per tile
+      S *outw = reinterpret_cast<S *>(Obuf) + (SUB * 16 + ln) * LDSW + 4 * g;
 #pragma unroll
       for (int j = 0; j < NTW; ++j) {
         const int t = T0 + j;
         if constexpr (HL > 0) {
           // the two identity shortcuts: + 2 dY at the output's own position
-#pragma unroll
-          for (int rr = 0; rr < 4; ++rr)
-            acc[j][rr] += 2.f * to_f32<Tag>(reinterpret_cast<const u16 *>(rowp)[(4 * g + rr) * LDSW + 16 * t + ln]);
+          const uint2 yv = *reinterpret_cast<const uint2 *>(&rowp[ln * LDSW + 16 * t + 4 * g]);
+          acc[j][0] += 2.f * to_f32<Tag>((u16)(yv.x & 0xffffu));
+          acc[j][1] += 2.f * to_f32<Tag>((u16)(yv.x >> 16));
+          acc[j][2] += 2.f * to_f32<Tag>((u16)(yv.y & 0xffffu));
+          acc[j][3] += 2.f * to_f32<Tag>((u16)(yv.y >> 16));
         }
-        const uint32_t lo = pack2<Tag>(acc[j][0], acc[j][1]);
-        const uint32_t hi = pack2<Tag>(acc[j][2], acc[j][3]);
-        outp[0 * LDSW + 16 * t] = (u16)(lo & 0xffffu);
-        outp[1 * LDSW + 16 * t] = (u16)(lo >> 16);
-        outp[2 * LDSW + 16 * t] = (u16)(hi & 0xffffu);
-        outp[3 * LDSW + 16 * t] = (u16)(hi >> 16);
+        *reinterpret_cast<uint2 *>(outw + 16 * t) = uint2{pack2<Tag>(acc[j][0], acc[j][1]), pack2<Tag>(acc[j][2], acc[j][3])};
       }
     } else {
 #pragma unroll
@@ -1939,13 +1964,18 @@ __device__ __attribute__((always_inline)) inline void dx_store(const KArgs &a, v
       if (vv < 16 && ms + vv < m1) {
         const uint32_t *l4 = reinterpret_cast<const uint32_t *>(Obuf + ((16 * sub + vv) * G::LDSW + hi * G::RP) * Tag::ES);
         uint32_t *p4 = reinterpret_cast<uint32_t *>(reinterpret_cast<char *>(reinterpret_cast<S *>(dx) + tiled_sub_base(a, c, ms)) + off);
+        // the padded row in 16-byte reads (it spans whole 16-byte chunks)
+        constexpr int NDR = (NDV + 3) & ~3;
+        uint32_t d[NDR];
 #pragma unroll
-        for (int i = 0; i + 4 <= NDV; i += 4) {
+        for (int i = 0; i < NDR; i += 4) {
           const uint4 u = *reinterpret_cast<const uint4 *>(l4 + i);
-          *reinterpret_cast<u32x4a *>(p4 + i) = u32x4a{u.x, u.y, u.z, u.w};
+          d[i] = u.x; d[i + 1] = u.y; d[i + 2] = u.z; d[i + 3] = u.w;
         }
 #pragma unroll
-        for (int i = NDV & ~3; i < NDV; ++i) p4[i] = l4[i];
+        for (int i = 0; i + 4 <= NDV; i += 4) *reinterpret_cast<u32x4a *>(p4 + i) = u32x4a{d[i], d[i + 1], d[i + 2], d[i + 3]};
+#pragma unroll
+        for (int i = NDV & ~3; i < NDV; ++i) p4[i] = d[i];
       }
     }
     return;
@@ -2178,13 +2208,18 @@ __device__ __attribute__((always_inline)) inline void stream_store(const KArgs &
       const uint32_t *l4 = reinterpret_cast<const uint32_t *>(Obuf + ((16 * sub + vv) * G::LDSW + hi * G::RP) * Tag::ES);
       uint32_t *p4 = reinterpret_cast<uint32_t *>(reinterpret_cast<char *>(dx + tiled_sub_base(a, c, ms)) +
                                                   tiled_row_off<WIN, Tag::ES>(a, vv, hi));
+      // the padded row in 16-byte reads (it spans whole 16-byte chunks)
+      constexpr int NDR = (NDV + 3) & ~3;
+      uint32_t d[NDR];
 #pragma unroll
-      for (int i = 0; i + 4 <= NDV; i += 4) {
+      for (int i = 0; i < NDR; i += 4) {
         const uint4 u = *reinterpret_cast<const uint4 *>(l4 + i);
-        *reinterpret_cast<u32x4a *>(p4 + i) = u32x4a{u.x, u.y, u.z, u.w};
+        d[i] = u.x; d[i + 1] = u.y; d[i + 2] = u.z; d[i + 3] = u.w;
       }
 #pragma unroll
-      for (int i = NDV & ~3; i < NDV; ++i) p4[i] = l4[i];
+      for (int i = 0; i + 4 <= NDV; i += 4) *reinterpret_cast<u32x4a *>(p4 + i) = u32x4a{d[i], d[i + 1], d[i + 2], d[i + 3]};
+#pragma unroll
+      for (int i = NDV & ~3; i < NDV; ++i) p4[i] = d[i];
     }
   }
 }
@@ -2257,6 +2292,18 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
   if (nst > 1) stream_load<Tag, WIN>(a, x, dy, c, s0 + CW, s1, wave, lane, st);
   __syncthreads();
 
+  // the input-gradient waves' 16-bit B fragments, read once: the table is
+  // the same for every stage
+  constexpr int DXI = DXW >= 0 ? DXW : 0;
+  constexpr bool PRE = DX && DXW >= 0 && Tag::W16;
+  typedef DxSplit<Tag, WIN, DXI, kStreamWaves - kStreamDt> DS;
+  typename Tag::Frag bfw[DS::NQ];
+  if constexpr (PRE) {
+    const int g = lane >> 4, ln = lane & 15;
+#pragma unroll
+    for (int i = 0; i < DS::NQ; ++i) bfw[i] = fwd_bfrag<Tag, WIN>(TB, DS::QLO + i, g, ln);
+  }
+
   for (int s = 0; s < nst; ++s) {
     const int64_t m0 = s0 + (int64_t)s * CW;
     unsigned char *cur = smem + (s & 1) * SC::STAGE;
@@ -2265,7 +2312,8 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
     if constexpr (DTW >= 0) {
       dt_products_split<Tag, G, DTW, HL>(cur, cur + G::BUF, acc, accl, lane);
     } else if constexpr (DX) {
-      dx_products<Tag, WIN, DXW, kStreamWaves - kStreamDt, (HX ? HL : 0)>(cur + G::BUF, obuf, Ts, TB, lane, Tsl, TBL);
+      dx_products<Tag, WIN, DXW, kStreamWaves - kStreamDt, (HX ? HL : 0), PRE>(cur + G::BUF, obuf, Ts, TB, lane, Tsl,
+                                                                                TBL, &bfw);
     }
     // the next stage into the other buffer (free since the last barrier),
     // the one after it in flight, the previous stage's dX rows out
