@@ -1307,9 +1307,15 @@ __device__ __attribute__((always_inline)) inline u16x8 dt_frag16(const unsigned 
   const int g = lane >> 4;
   const int i = lane & 15;
   const int r = i >> 2, q = i & 3;
-  const int e0 = (8 * g + r) * LDSW + 16 * pt + 4 * q;
+  // K index 8 g + 4 h + r (h: first or second read) takes window
+  // 8 g + 2 r + h: the same permutation of the stage's windows for both
+  // operands leaves X^T dY unchanged, and with it the eight windows that one
+  // read cycle serves (lanes of g and g + 1) fall in distinct LDS banks (64
+  // banks for reads) at a row pitch of 232 elements (w = 14); the identity
+  // order put windows r and r + 8 ... on the same banks
+  const int e0 = (8 * g + 2 * r) * LDSW + 16 * pt + 4 * q;
   lds_i16x4 *p0 = (lds_i16x4 *)(buf + 2 * e0);
-  lds_i16x4 *p1 = (lds_i16x4 *)(buf + 2 * (e0 + 4 * LDSW));
+  lds_i16x4 *p1 = (lds_i16x4 *)(buf + 2 * (e0 + LDSW));
   const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(p0);
   const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(p1);
   return __builtin_bit_cast(u16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
