@@ -56,11 +56,11 @@ def parse():
 # on (sha256 of the kernel header); otherwise reported as null.
 TRAFFIC = {
     # (workload, kernel): measured bytes per dispatch (profiles/wbmm_traffic_*.txt)
-    ("bf16_b64_c192_28_w14", "bwd"): {"source": "c36f0ddf1fb169d6", "bytes": 62598093},
-    ("bf16_b64_c192_28_w14", "fwd"): {"source": "c36f0ddf1fb169d6", "bytes": 41268863},
-    ("bf16_b64_c192_28_w14", "dx"): {"source": "c36f0ddf1fb169d6", "bytes": 41231065},
-    ("bf16_b64_c192_28_w14", "dt"): {"source": "c36f0ddf1fb169d6", "bytes": 42201521},
-    ("bf16_b64_c96_56_w7", "fwd"): {"source": "c36f0ddf1fb169d6", "bytes": 77496155},
+    ("bf16_b64_c192_28_w14", "bwd"): {"source": "69c0ad20ea580618", "bytes": 62515762},
+    ("bf16_b64_c192_28_w14", "fwd"): {"source": "69c0ad20ea580618", "bytes": 41235167},
+    ("bf16_b64_c192_28_w14", "dx"): {"source": "69c0ad20ea580618", "bytes": 41261717},
+    ("bf16_b64_c192_28_w14", "dt"): {"source": "69c0ad20ea580618", "bytes": 42242048},
+    ("bf16_b64_c96_56_w7", "fwd"): {"source": "69c0ad20ea580618", "bytes": 77500693},
 }
 
 

@@ -278,7 +278,7 @@ __device__ __attribute__((always_inline)) inline void load_row(const void *base,
 #pragma unroll
     for (int i = 0; i < (WIN + 1) / 2; ++i)
       o.d[i] = (uint32_t)((((uint64_t)(i + 1 < NL ? in[i + 1] : 0u) << 32) | in[i]) >> sh);
-    if (WIN & 1) o.d[WIN / 2] &= 0xffffu;
+    if constexpr ((WIN & 1) != 0) o.d[WIN / 2] &= 0xffffu;
   } else {
     // branch-free: element x reads column min(x, cols - 1), which is inside
     // the row, and is then zeroed when x >= cols
