@@ -355,7 +355,16 @@ struct FwdCfg {
   static constexpr int K1 = 2 * WIN - 1;
   static constexpr int K2 = K1 * K1;
   static constexpr int TS_LEN = rup(K2 + 9, 8);       // + the overrun of tb_chunk's dword reads
-  static constexpr int TB_LEN = Tag::W16 ? K1 * RP * RP : 0;
+  // Toeplitz blocks TB[dh][x_out][x_in] for dh = -(w-1)..w-1, with zero
+  // blocks beyond them for every dh a lane's B fragment can name (dh of
+  // fragment q: q - (NT-1) + g/2 for 16-position rows, 2 (q - (NT-1)) + g -
+  // x_out/8 for 8-position rows), so that the fragment reads need no range
+  // check and their address is a per-lane base plus a constant
+  static constexpr int DHMIN = RP == 16 ? -(NT - 1) : -2 * (NT - 1) - 1;
+  static constexpr int DHMAX = RP == 16 ? 2 * S - 1 : 2 * (NB - NT) + 3;
+  static constexpr int TBLO = -(WIN - 1) - DHMIN > 0 ? -(WIN - 1) - DHMIN : 0;  // zero blocks below
+  static constexpr int TBHI = DHMAX - (WIN - 1) > 0 ? DHMAX - (WIN - 1) : 0;     // and above
+  static constexpr int TB_LEN = Tag::W16 ? (TBLO + K1 + TBHI) * RP * RP : 0;
   // hierarchical form (WIN = 2 wl): the local table of the wl x wl
   // sub-windows and its Toeplitz blocks
   static constexpr int WL = WIN / 2;
@@ -530,6 +539,25 @@ __device__ __attribute__((always_inline)) inline void tab_load(const typename Ta
   }
 }
 
+// The Toeplitz blocks of M_c (16-bit) from the table row in LDS: block
+// TBLO + dh + (w-1) holds TB[dh][x_out][x_in], the pad blocks zero.  NTH
+// threads take part; no barrier inside.
+template <class Tag, int WIN, int NTH>
+__device__ __attribute__((always_inline)) inline void build_tb(const typename Tag::S *Ts, typename Tag::S *TB, int tid) {
+  typedef FwdCfg<Tag, WIN> G;
+  constexpr int RP = G::RP, K1 = G::K1, CPR = RP / 8;  // 8-element chunks per TB row
+  constexpr int NCH = (G::TBLO + K1 + G::TBHI) * RP * CPR;
+  for (int ch = tid; ch < NCH; ch += NTH) {
+    const int row = ch / CPR;  // = block * RP + x_out
+    const int xi0 = (ch - row * CPR) * 8;
+    const int dhi = row / RP - G::TBLO;
+    const int xo = row - (dhi + G::TBLO) * RP;
+    u16x8 v = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+    if (dhi >= 0 && dhi < K1 && xo < WIN) v = tb_chunk<WIN>(Ts, dhi * K1 - xo + WIN - 1, xi0);  // table index of x_in = 0
+    *reinterpret_cast<u16x8 *>(&TB[row * RP + xi0]) = v;
+  }
+}
+
 // The table row of channel c (read back to front for the input gradient)
 // -> Ts with coalesced loads; for 16-bit, the Toeplitz blocks
 // TB[dh][x_out][x_in] of M_c gathered from it.  The hierarchical form also
@@ -558,17 +586,8 @@ __device__ __attribute__((always_inline)) inline void fwd_tables(const TabRegs<T
   }
   if constexpr (Tag::W16) {
     __syncthreads();
-    constexpr int CPR = RP / 8;               // 8-element chunks per TB row
-    constexpr int NCH = K1 * RP * CPR;
-    for (int ch = tid; ch < NCH; ch += NTH) {
-      const int row = ch / CPR;               // = dhi * RP + x_out
-      const int xi0 = (ch - row * CPR) * 8;
-      const int dhi = row / RP;
-      const int xo = row - dhi * RP;
-      u16x8 v = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
-      if (xo < WIN) v = tb_chunk<WIN>(Ts, dhi * K1 - xo + WIN - 1, xi0);  // table index of x_in = 0
-      *reinterpret_cast<u16x8 *>(&TB[row * RP + xi0]) = v;
-    }
+    build_tb<Tag, WIN, NTH>(Ts, TB, tid);
+    constexpr int CPR = RP / 8;  // 8-element chunks per TBL row
     if constexpr (HIER) {
       constexpr int WL = G::WL, K1L = G::K1L;
       constexpr int NCHL = K1L * RP * CPR;
@@ -607,9 +626,7 @@ __device__ __attribute__((always_inline)) inline typename Tag::Frag fwd_bfrag(co
   if (RP == 16) { dh = d0 + (g >> 1); xi0 = 8 * (g & 1); }
   else { dh = 2 * d0 + g - (ln >> 3); xi0 = 0; }
   const int xo = ln & (RP - 1);
-  if (dh >= -(WIN - 1) && dh <= WIN - 1)
-    return *reinterpret_cast<const typename Tag::Frag *>(&TB[((dh + WIN - 1) * RP + xo) * RP + xi0]);
-  return typename Tag::Frag{0, 0, 0, 0, 0, 0, 0, 0};
+  return *reinterpret_cast<const typename Tag::Frag *>(&TB[((dh + G::TBLO + WIN - 1) * RP + xo) * RP + xi0]);
 }
 
 // Hierarchical form, 16-bit: the local-table fragment of K step s and output
@@ -1871,9 +1888,7 @@ __device__ __attribute__((always_inline)) inline void dx_products(
         if (RP == 16) { dh = d0 + (g >> 1); xi0 = 8 * (g & 1); }
         else { dh = 2 * d0 + g - (ln >> 3); xi0 = 0; }
         const int xo = ln & (RP - 1);
-        if (dh >= -(WIN - 1) && dh <= WIN - 1)
-          return *reinterpret_cast<const Frag *>(&TB[((dh + WIN - 1) * RP + xo) * RP + xi0]);
-        return Frag{0, 0, 0, 0, 0, 0, 0, 0};
+        return *reinterpret_cast<const Frag *>(&TB[((dh + F::TBLO + WIN - 1) * RP + xo) * RP + xi0]);
       };
       // fragment q = 2s - t + NT - 1 serves steps s with T0 <= t < T1; it is
       // read from LDS at the first of them (or preloaded)
@@ -2047,17 +2062,7 @@ __device__ __attribute__((always_inline)) void bwd_wave(const typename Tag::S *_
     if constexpr (Tag::W16) {
       __syncthreads();
       S *TB = reinterpret_cast<S *>(smem + G::TB_OFF);
-      constexpr int CPR = RP / 8;
-      constexpr int NCH = K1 * RP * CPR;
-      for (int ch = tid; ch < NCH; ch += kThreads) {
-        const int row = ch / CPR;               // = dhi * RP + x_out
-        const int xi0 = (ch - row * CPR) * 8;
-        const int dhi = row / RP;
-        const int xo = row - dhi * RP;
-        u16x8 v = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
-        if (xo < WIN) v = tb_chunk<WIN>(Ts, dhi * K1 - xo + WIN - 1, xi0);  // table index of x_in = 0
-        *reinterpret_cast<u16x8 *>(&TB[row * RP + xi0]) = v;
-      }
+      build_tb<Tag, WIN, kThreads>(Ts, TB, tid);
     }
   }
 
@@ -2281,17 +2286,7 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
       if (tid + i * kStreamThreads < K2) Ts[tid + i * kStreamThreads] = tr.v[i];
     __syncthreads();
     if constexpr (Tag::W16) {
-      constexpr int CPR = RP / 8;
-      constexpr int NCH = K1 * RP * CPR;
-      for (int ch = tid; ch < NCH; ch += kStreamThreads) {
-        const int row = ch / CPR;  // = dhi * RP + x_out
-        const int xi0 = (ch - row * CPR) * 8;
-        const int dhi = row / RP;
-        const int xo = row - dhi * RP;
-        u16x8 v = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
-        if (xo < WIN) v = tb_chunk<WIN>(Ts, dhi * K1 - xo + WIN - 1, xi0);  // table index of x_in = 0
-        *reinterpret_cast<u16x8 *>(&TB[row * RP + xi0]) = v;
-      }
+      build_tb<Tag, WIN, kStreamThreads>(Ts, TB, tid);
     }
   }
   stream_write<Tag, WIN>(smem, wave, lane, st);
