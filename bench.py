@@ -56,11 +56,11 @@ def parse():
 # on (sha256 of the kernel header); otherwise reported as null.
 TRAFFIC = {
     # (workload, kernel): measured bytes per dispatch (profiles/wbmm_traffic_*.txt)
-    ("bf16_b64_c192_28_w14", "bwd"): {"source": "69c0ad20ea580618", "bytes": 62515762},
-    ("bf16_b64_c192_28_w14", "fwd"): {"source": "69c0ad20ea580618", "bytes": 41235167},
-    ("bf16_b64_c192_28_w14", "dx"): {"source": "69c0ad20ea580618", "bytes": 41261717},
-    ("bf16_b64_c192_28_w14", "dt"): {"source": "69c0ad20ea580618", "bytes": 42242048},
-    ("bf16_b64_c96_56_w7", "fwd"): {"source": "69c0ad20ea580618", "bytes": 77500693},
+    ("bf16_b64_c192_28_w14", "bwd"): {"source": "a63abe0abee7e23f", "bytes": 62505662},
+    ("bf16_b64_c192_28_w14", "fwd"): {"source": "a63abe0abee7e23f", "bytes": 41318730},
+    ("bf16_b64_c192_28_w14", "dx"): {"source": "a63abe0abee7e23f", "bytes": 41239136},
+    ("bf16_b64_c192_28_w14", "dt"): {"source": "a63abe0abee7e23f", "bytes": 42260713},
+    ("bf16_b64_c96_56_w7", "fwd"): {"source": "a63abe0abee7e23f", "bytes": 77499532},
 }
 
 
