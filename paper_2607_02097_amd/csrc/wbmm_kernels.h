@@ -20,32 +20,43 @@
 // Data movement
 // -------------
 // The unit of global traffic is one window row (w consecutive elements of an
-// image row).  Lanes walk rows in memory order (window column fastest, then
-// the row inside the band, then the band), so a wavefront touches one
-// contiguous stretch of the tensor; a row moves as dwords when it is
-// dword-aligned and whole, element by element otherwise (image edges, odd
-// windows).  Forward: rows land in a window-major LDS tile, already padded,
-// so a matrix-core A fragment is one aligned 16-byte LDS read.  Table
-// gradient: rows land position-major (windows contiguous), so fragments of
-// X^T and dY are contiguous too; the write of a row is w 16-bit LDS stores at
-// a constant stride.
+// image row) or, where the windows tile the map, a 16-byte chunk of whole
+// bands or whole images.  Rows land in window-major LDS tiles, already
+// padded, so a matrix-core fragment of one window's positions is one 16-byte
+// LDS read; the table gradient reads the transposed fragments (positions x
+// windows) with the transposing 16-bit LDS reads.  Where the windows tile the
+// map with a power-of-two count per row ("fixed-offset rows"), a row's offset
+// inside its 16-window sub-tile depends only on its place there, so copies
+// need no per-row index arithmetic.
 //
-// Forward / backward-input: one workgroup = (channel, tile of windows).  The
-// table T[c] -> LDS, Toeplitz blocks TB[dh][x_out][x_in] -> LDS, each wave
-// keeps the distinct B fragments in registers and runs 16-window sub-tiles
-// through v_mfma_f32_16x16x32_{bf16,f16} (v_mfma_f32_16x16x4_f32 for
-// float32); results are rounded once and go back through LDS.  The input
-// gradient is the same kernel with the table read back to front, since M_c^T
-// is the matrix of the reversed table.
+// Forward / backward-input: one workgroup = (channel, tile of windows), four
+// waves, each running 16-window sub-tiles.  The table T[c] and its Toeplitz
+// blocks TB[dh][x_out][x_in] go to LDS (zero blocks padded around them so
+// that fragment reads need no range check), and products run through
+// v_mfma_f32_16x16x32_{bf16,f16} (v_mfma_f32_16x16x4_f32 for float32); 16-bit
+// maps that the windows tile take the image-layout kernel (the sub-tile is
+// copied in image layout with 16-byte accesses and the window fragments are
+// gathered from it).  Results are rounded once and go back through LDS.  The
+// input gradient is the same kernel with the table read back to front, since
+// M_c^T is the matrix of the reversed table.
 //
-// Table gradient: one workgroup = (channel, slab of windows), K = windows.
-// The 16x16 block pair (input tile pi, output tile po) only matters through
-// pi - po, so all pairs with equal pi - po share one accumulator (27 16x16
-// fp32 tiles at w = 14), split across the four waves.  The next stage's rows
-// are loaded into registers while the current stage computes.  Diagonal sums
-// of the tiles give dT.  Slabs of one channel are summed in slab order by
-// the channel's last workgroup, found with one atomic ticket per workgroup;
-// the result is bitwise reproducible.
+// Table gradient: K = windows.  The 16x16 block pair (input tile pi, output
+// tile po) only matters through pi - po, so all pairs with equal pi - po
+// share one accumulator (27 16x16 fp32 tiles at w = 14), split across four
+// waves.  Diagonal sums of the tiles give dT.  Slabs of one channel are
+// summed in slab order by the channel's last workgroup, found with one
+// atomic ticket per workgroup; the result is bitwise reproducible.
+//
+// Fused backward: x and dy are read once for both gradients.  With
+// fixed-offset rows and no more channels than compute units, one 12-wave
+// workgroup per channel (or slab) streams the channel's stages through LDS:
+// four waves accumulate the table gradient while eight compute the input
+// gradient of the same stage, the next stage is copied in and the previous
+// stage's dX rows go out, with one workgroup barrier per stage.  Otherwise a
+// four-wave workgroup per (channel, slab) runs the same products in turn.
+// The hierarchical form (global window 2 wl plus local wl sub-windows) adds
+// local-block products to the forward and input gradient and splits the
+// table-gradient accumulators by row halves to bin both tables in one pass.
 #pragma once
 
 #include <hip/hip_runtime.h>
