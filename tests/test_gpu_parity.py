@@ -216,6 +216,39 @@ def test_integer_data_bit_exact(w, dtype):
         assert np.array_equal(got[k], want[k]), k
 
 
+# maps the windows tile, few channels: the channel-stream gradients (one
+# workgroup per channel, or several slabs with a ticket) and the image-layout
+# forward
+TILED_EXACT = [
+    (16, 3, 28, 28, 14),   # one slab per channel
+    (2, 2, 112, 112, 14),  # four slabs per channel, parts summed by ticket
+    (8, 2, 40, 40, 10),
+    (4, 3, 32, 64, 16),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("shape", TILED_EXACT, ids=lambda s: "B%dC%dH%dW%dw%d" % s)
+def test_fixed_offset_integer_data_bit_exact(shape, dtype):
+    """Integers in {-1, 0, 1} on maps the windows tile: every sum is exact in
+    fp32 and every output an integer below 256, so the forward, both
+    gradients and the fused backward must equal the oracle bit for bit."""
+    B, C, H, Wd, w = shape
+    r = np.random.default_rng(11 + w)
+    d = {}
+    for k, shp in (("x", (B, C, H, Wd)), ("dy", (B, C, H, Wd)), ("t", (C, (2 * w - 1) ** 2))):
+        d[k], d[k + "64"] = synth.round_to(r.integers(-1, 2, size=shp).astype(np.float64), dtype)
+    got = run_gpu(d, w, dtype)
+    x, t, dy = (to_device(d[k], dtype) for k in ("x", "t", "dy"))
+    dx, dt = W.wbmm_backward(x, dy, t, w)
+    torch.cuda.synchronize()
+    got["fused dx"], got["fused dt"] = to_f64(dx), to_f64(dt)
+    want = run_oracle(d, w)
+    want["fused dx"], want["fused dt"] = want["dx"], want["dt"]
+    for k in want:
+        assert np.array_equal(got[k], want[k]), k
+
+
 # shapes for the image-layout forward (16-bit, windows tile the map, NW a
 # power of two, a 16-window sub-tile is whole bands of one image or whole
 # images, pieces 16-byte aligned)
