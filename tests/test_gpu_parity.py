@@ -473,6 +473,7 @@ HIER = [
     (16, 3, 28, 28, 7),
     (16, 1, 32, 32, 8),
     (4, 2, 20, 20, 5),
+    (4, 2, 14, 14, 7),     # 196-element images: row-kernel forward, channel-stream backward
     (1, 2, 30, 17, 7),
     (2, 2, 16, 16, 4),
     (1, 2, 21, 35, 5),
