@@ -53,7 +53,8 @@ def parse():
 # HBM traffic of the dominant kernel, from two rocprofv3 --pmc runs (FETCH_SIZE,
 # WRITE_SIZE; KiB per dispatch) scaled by what the same counters read for a
 # plain copy of known size.  Valid only for the kernel source it was measured
-# on (sha256 of the kernel header); otherwise reported as null.
+# on (sha256 of the kernel header's code without comments and blank lines);
+# otherwise reported as null.
 TRAFFIC = {
     # (workload, kernel): measured bytes per dispatch (profiles/wbmm_traffic_*.txt)
     ("bf16_b64_c192_28_w14", "bwd"): {"source": "e801453c85ab7aeb", "bytes": 62505662},
@@ -61,6 +62,10 @@ TRAFFIC = {
     ("bf16_b64_c192_28_w14", "dx"): {"source": "e801453c85ab7aeb", "bytes": 41239136},
     ("bf16_b64_c192_28_w14", "dt"): {"source": "e801453c85ab7aeb", "bytes": 42260713},
     ("bf16_b64_c96_56_w7", "fwd"): {"source": "e801453c85ab7aeb", "bytes": 77499532},
+    ("bf16_b64_c192_28_hier7", "hbwd"): {"source": "e801453c85ab7aeb", "bytes": 63331314},
+    ("bf16_b16_c64_112_hier7", "hbwd"): {"source": "e801453c85ab7aeb", "bytes": 81967587},
+    ("bf16_b128_c384_14_w14", "bwd"): {"source": "e801453c85ab7aeb", "bytes": 78911575},
+    ("bf16_b16_c64_112_w14", "bwd"): {"source": "e801453c85ab7aeb", "bytes": 80823022},
 }
 
 
