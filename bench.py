@@ -57,15 +57,15 @@ def parse():
 # otherwise reported as null.
 TRAFFIC = {
     # (workload, kernel): measured bytes per dispatch (profiles/wbmm_traffic_*.txt)
-    ("bf16_b64_c192_28_w14", "bwd"): {"source": "e801453c85ab7aeb", "bytes": 62505662},
-    ("bf16_b64_c192_28_w14", "fwd"): {"source": "e801453c85ab7aeb", "bytes": 41318730},
-    ("bf16_b64_c192_28_w14", "dx"): {"source": "e801453c85ab7aeb", "bytes": 41239136},
-    ("bf16_b64_c192_28_w14", "dt"): {"source": "e801453c85ab7aeb", "bytes": 42260713},
-    ("bf16_b64_c96_56_w7", "fwd"): {"source": "e801453c85ab7aeb", "bytes": 77499532},
-    ("bf16_b64_c192_28_hier7", "hbwd"): {"source": "e801453c85ab7aeb", "bytes": 63331314},
-    ("bf16_b16_c64_112_hier7", "hbwd"): {"source": "e801453c85ab7aeb", "bytes": 81967587},
-    ("bf16_b128_c384_14_w14", "bwd"): {"source": "e801453c85ab7aeb", "bytes": 78911575},
-    ("bf16_b16_c64_112_w14", "bwd"): {"source": "e801453c85ab7aeb", "bytes": 80823022},
+    ("bf16_b64_c192_28_w14", "bwd"): {"source": "c221d03bff73e888", "bytes": 62505279},
+    ("bf16_b64_c192_28_w14", "fwd"): {"source": "c221d03bff73e888", "bytes": 41317002},
+    ("bf16_b64_c192_28_w14", "dx"): {"source": "c221d03bff73e888", "bytes": 41240608},
+    ("bf16_b64_c192_28_w14", "dt"): {"source": "c221d03bff73e888", "bytes": 42259690},
+    ("bf16_b64_c96_56_w7", "fwd"): {"source": "c221d03bff73e888", "bytes": 77499596},
+    ("bf16_b64_c192_28_hier7", "hbwd"): {"source": "c221d03bff73e888", "bytes": 63325433},
+    ("bf16_b16_c64_112_hier7", "hbwd"): {"source": "c221d03bff73e888", "bytes": 81969760},
+    ("bf16_b128_c384_14_w14", "bwd"): {"source": "c221d03bff73e888", "bytes": 78907740},
+    ("bf16_b16_c64_112_w14", "bwd"): {"source": "c221d03bff73e888", "bytes": 80830886},
 }
 
 

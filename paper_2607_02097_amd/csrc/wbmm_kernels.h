@@ -1021,24 +1021,28 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_img_kernel(const type
         *reinterpret_cast<uint4 *>(dst + soff + 2u * (uint32_t)(r0 * ia.W)) = val;
       }
     };
+    // output tiles per step: a pair, or one in the hierarchical form (whose
+    // local fragments leave no registers for a second accumulator chain);
+    // each tile takes the same products in the same order either way
+    constexpr int TS = HIER ? 1 : 2;
     Frag bf[NB];
 #pragma unroll
-    for (int t0 = 0; t0 < NT; t0 += 2) {
+    for (int t0 = 0; t0 < NT; t0 += TS) {
 #pragma unroll
       for (int q = 0; q < NB; ++q) {
         const int tf = NT - 1 - q;
         const int first_t = tf >= 0 ? tf : (((-tf) & 1) ? 1 : 0);
-        if (first_t == t0 || first_t == t0 + 1) bf[q] = fwd_bfrag<Tag, WIN>(TB, q, g, ln);
+        if (first_t == t0 || (TS == 2 && first_t == t0 + 1)) bf[q] = fwd_bfrag<Tag, WIN>(TB, q, g, ln);
       }
       f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < S_; ++s) {
         acc0 = mma<Tag>(bf[2 * s - t0 + NT - 1], af[s], acc0);
-        if (t0 + 1 < NT) acc1 = mma<Tag>(bf[2 * s - t0 - 1 + NT - 1], af[s], acc1);
+        if (TS == 2 && t0 + 1 < NT) acc1 = mma<Tag>(bf[2 * s - t0 - 1 + NT - 1], af[s], acc1);
         if constexpr (HIER) {
           // local sub-window blocks
           if (fwd_rows_meet<Tag, WIN>(s, t0, true)) acc0 = mma<Tag>(fwd_lfrag<Tag, WIN>(TBL, s, t0, g, ln), af[s], acc0);
-          if (t0 + 1 < NT && fwd_rows_meet<Tag, WIN>(s, t0 + 1, true))
+          if (TS == 2 && t0 + 1 < NT && fwd_rows_meet<Tag, WIN>(s, t0 + 1, true))
             acc1 = mma<Tag>(fwd_lfrag<Tag, WIN>(TBL, s, t0 + 1, g, ln), af[s], acc1);
         }
       }
@@ -1046,7 +1050,7 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_img_kernel(const type
       // window row ho, columns xo0 .. xo0 + 3; columns and rows beyond the
       // window go to the dummy element
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
+      for (int h = 0; h < TS; ++h) {
         const int t = t0 + h;
         if (t >= NT) continue;
         const f32x4 acc = h ? acc1 : acc0;
@@ -1078,7 +1082,8 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_img_kernel(const type
           for (int rr = 0; rr < 4; ++rr) raw[(ho < WIN && xo0 + rr < WIN) ? o + rr : IC::DUMMY] = vals[rr];
         }
       }
-      if (ia.pair_store) {
+      // rows are stored per output-tile pair, once both tiles are written
+      if (ia.pair_store && (TS == 2 || (t0 & 1) || t0 + 1 >= NT)) {
         wave_lds_sync();
         const int r0 = RPP * (t0 / 2);
         const int r1 = r0 + RPP < WIN ? r0 + RPP : WIN;
