@@ -132,6 +132,29 @@ def calibrate_copy(nbytes, steps):
                       "bytes_written": b.numel() * 2, "launches": steps}))
 
 
+def kernel_names(wl, ncu):
+    """Name of each pass's kernel as the profiler prints it (every template
+    argument), from the dispatch rules of the library."""
+    fk = "wbmm_fwd_img_kernel" if image_layout(wl) else "wbmm_fwd_kernel"
+    tl = "true" if fixed_offset_rows(wl) else "false"
+    # channel-stream gradients: fixed-offset rows and no more channels than
+    # compute units
+    chan_stream = fixed_offset_rows(wl) and wl.C <= ncu
+    dtk = "wbmm_bwd_stream_kernel" if chan_stream else "wbmm_dt_kernel"
+    bwk = "wbmm_bwd_stream_kernel" if chan_stream else "wbmm_bwd_kernel"
+    img = fk == "wbmm_fwd_img_kernel"
+    fwd_tail = (lambda rev, hier: "<%s,%d," + rev + "," + hier + ">") if img else \
+        (lambda rev, hier: "<%s,%d," + rev + "," + hier + "," + (tl if hier == "false" else "false") + ">")
+    tag = {"bf16": "TagBF16", "f16": "TagF16", "f32": "TagF32"}[wl.dtype]
+    names = {"fwd": fk + fwd_tail("false", "false"), "dx": fk + fwd_tail("true", "false"),
+             "dt": dtk + ("<%s,%d,false,0>" if chan_stream else "<%s,%d," + tl + ">"),
+             "bwd": bwk + ("<%s,%d,true,0>" if chan_stream else "<%s,%d," + tl + ">"),
+             "hfwd": fk + fwd_tail("false", "true"),
+             "hbwd": ("wbmm_bwd_stream_kernel<%s,%d,true," + str(wl.w // 2) + ">") if chan_stream and wl.w >= 10
+                     else "wbmm_hier_backward (several launches) <%s,%d>"}
+    return {k: v % (tag, wl.w) for k, v in names.items()}
+
+
 def pass_bytes(wl, p, es):
     """Algorithmic bytes of one kernel (each tensor touched once)."""
     act = wl.B * wl.C * wl.H * wl.W * es
@@ -211,27 +234,31 @@ def main():
             return torch.from_numpy(a.view(np.int16).copy()).view(torch.bfloat16).to(dev)
         return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
 
-    nsets = 1
-    if args.cold:
-        per = 4 * wl.B * wl.C * wl.H * wl.W * es  # x, dy, y, dx
-        nsets = max(2, int(np.ceil(2 * 256e6 / per)) + 1)
     wloc = wl.w // 2  # local window of the hierarchical form
     if wl.hier:
         d["tl"], d["tl64"] = synth.draw_local_table(wl.C, wloc, wl.dtype, seed=0)
-    sets = []
-    for i in range(nsets):
-        x, t, dy = put(d["x"]), put(d["t"]), put(d["dy"])
-        y, dx = torch.empty_like(x), torch.empty_like(dy)
-        dtab = torch.empty((wl.C, wl.table_len), dtype=torch.float32, device=dev)
-        if wl.hier:
-            tl = put(d["tl"])
-            dtl = torch.empty((wl.C, (2 * wloc - 1) ** 2), dtype=torch.float32, device=dev)
-            need = W.wbmm_hier_backward_workspace_bytes(x.shape, wloc, tdt)
-        else:
-            tl = dtl = None
-            need = W.wbmm_backward_table_workspace_bytes(x.shape, wl.w, tdt)
-        ws = W.new_workspace(need, dev)  # counters start at zero, stay zero
-        sets.append((x, t, dy, y, dx, dtab, ws, tl, dtl))
+
+    def make_sets(nsets):
+        sets = []
+        for _ in range(nsets):
+            x, t, dy = put(d["x"]), put(d["t"]), put(d["dy"])
+            y, dx = torch.empty_like(x), torch.empty_like(dy)
+            dtab = torch.empty((wl.C, wl.table_len), dtype=torch.float32, device=dev)
+            if wl.hier:
+                tl = put(d["tl"])
+                dtl = torch.empty((wl.C, (2 * wloc - 1) ** 2), dtype=torch.float32, device=dev)
+                need = W.wbmm_hier_backward_workspace_bytes(x.shape, wloc, tdt)
+            else:
+                tl = dtl = None
+                need = W.wbmm_backward_table_workspace_bytes(x.shape, wl.w, tdt)
+            ws = W.new_workspace(need, dev)  # counters start at zero, stay zero
+            sets.append((x, t, dy, y, dx, dtab, ws, tl, dtl))
+        return sets
+
+    # cold mode: enough input sets (x, dy, y, dx each) that the rotation
+    # spans more than twice the 256 MB Infinity Cache
+    per_set = 4 * wl.B * wl.C * wl.H * wl.W * es
+    n_cold = max(2, int(np.ceil(2 * 256e6 / per_set)) + 1)
 
     passes = wl.passes
     # kernels of one step: the fused backward covers the two gradients
@@ -243,11 +270,12 @@ def main():
     code = W.DTYPE_CODES[tdt]
     import ctypes
     vp = ctypes.c_void_p
+    stream = torch.cuda.current_stream(dev)
 
-    def launch(p, i):
+    def launch(sets, p, i):
         """One pass through the C ABI on torch's current stream (raw pointers,
         no per-call Python checks: the shapes were validated above)."""
-        x, t, dy, y, dx, dtab, ws, tl, dtl = sets[i % nsets]
+        x, t, dy, y, dx, dtab, ws, tl, dtl = sets[i % len(sets)]
         st = vp(torch.cuda.current_stream(dev).cuda_stream)
         dims = (wl.B, wl.C, wl.H, wl.W, wl.w, code, st)
         hdims = (wl.B, wl.C, wl.H, wl.W, wloc, code, st)
@@ -272,79 +300,78 @@ def main():
         if r != 0:
             raise RuntimeError("%s failed: %s" % (p, W.wbmm_status_string(r)))
 
-    # warm-up, eager
-    for i in range(args.warmup):
-        for p in timed:
-            launch(p, i)
-    torch.cuda.synchronize()
-
-    # eager timing (includes host launch overhead; reported, not the value)
-    stream = torch.cuda.current_stream(dev)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    n_eager = min(args.steps, 50)
-    e0.record(stream)
-    for i in range(n_eager):
-        for p in step_kernels:
-            launch(p, i)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    eager_ms = e0.elapsed_time(e1) / n_eager
-
-    # HIP graphs: R consecutive steps per graph (and R launches per pass graph)
-    R = 10
+    R = 10  # steps per graph (and launches per pass graph)
     reps = max(1, args.steps // R)
     steps = reps * R
+    act_bytes = wl.B * wl.C * wl.H * wl.W * es
 
-    if args.eager:
-        # plain stream launches (hardware-counter runs serialise dispatches)
-        t_start = torch.cuda.Event(enable_timing=True)
-        t_end = torch.cuda.Event(enable_timing=True)
-        marks, bounds = run_marks(steps)
-        torch.cuda.synchronize()
-        t_start.record(stream)
-        i = 0
-        for mk, bd in zip(marks, bounds):
-            while i < bd:
-                for p in step_kernels:
-                    launch(p, i)
-                i += 1
-            mk.record(stream)
-        t_end.record(stream)
-        torch.cuda.synchronize()
-        ms_step = t_start.elapsed_time(t_end) / steps
-        run_ms = run_times(t_start, marks, bounds, 1)
-        per_pass = {}
-        for p in timed:
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record(stream)
-            for i in range(steps):
-                launch(p, i)
-            b.record(stream)
-            torch.cuda.synchronize()
-            per_pass[p] = a.elapsed_time(b) / steps
-    else:
-        def capture(seq, per_step):
-            g = torch.cuda.CUDAGraph()
-            cs = torch.cuda.Stream(dev)
-            cs.wait_stream(stream)
-            with torch.cuda.graph(g, stream=cs):
-                for i, p in enumerate(seq):
-                    launch(p, i // per_step)
-            stream.wait_stream(cs)
-            torch.cuda.synchronize()
-            return g
-
-        g_step = capture([p for _ in range(R) for p in step_kernels], len(step_kernels))
-        g_pass = {p: capture([p] * R, 1) for p in timed}
-        for _ in range(3):
-            g_step.replay()
+    def measure(sets):
+        """Warm-up, then exactly `steps` timed steps (HIP-graph replay, or
+        eager launches), per-pass kernel times and a device copy, all on the
+        input sets given (one set: cache-warm; several: rotated, cold)."""
+        nsets = len(sets)
+        for i in range(args.warmup):
             for p in timed:
-                g_pass[p].replay()
+                launch(sets, p, i)
+        torch.cuda.synchronize()
+        # eager timing (includes host launch overhead; reported, not the value)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        n_eager = min(steps, 50)
+        e0.record(stream)
+        for i in range(n_eager):
+            for p in step_kernels:
+                launch(sets, p, i)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        eager_ms = e0.elapsed_time(e1) / n_eager
+
+        if args.eager:
+            # plain stream launches (hardware-counter runs serialise dispatches)
+            def run_step_block(i0):
+                for i in range(i0, i0 + R):
+                    for p in step_kernels:
+                        launch(sets, p, i)
+
+            def run_pass_block(p, i0):
+                for i in range(i0, i0 + R):
+                    launch(sets, p, i)
+        else:
+            def capture(seq, per_step, i0):
+                g = torch.cuda.CUDAGraph()
+                cs = torch.cuda.Stream(dev)
+                cs.wait_stream(stream)
+                with torch.cuda.graph(g, stream=cs):
+                    for i, p in enumerate(seq):
+                        launch(sets, p, i0 + i // per_step)
+                stream.wait_stream(cs)
+                torch.cuda.synchronize()
+                return g
+
+            # one graph per distinct rotation phase of the input sets
+            nph = nsets if nsets > 1 else 1
+            g_step = [capture([p for _ in range(R) for p in step_kernels], len(step_kernels), ph * R)
+                      for ph in range(nph)]
+            g_pass = {p: [capture([p] * R, 1, ph * R) for ph in range(nph)] for p in timed}
+
+            def run_step_block(i0):
+                g_step[(i0 // R) % nph].replay()
+
+            def run_pass_block(p, i0):
+                g_pass[p][(i0 // R) % nph].replay()
+
+        # settle: the step replayed for at least 0.2 s (untimed), so the
+        # timed region starts at steady clocks
+        t_settle = time.perf_counter()
+        i = 0
+        while time.perf_counter() - t_settle < 0.2:
+            run_step_block(i * R)
+            i += 1
+            if i % 20 == 0:
+                torch.cuda.synchronize()
         torch.cuda.synchronize()
 
-        # timed region: K steps = K/R replays of the step graph, bracketed by
-        # synchronisation; then each pass graph timed with HIP events on the
-        # same stream to get the average duration of each kernel launch
+        # timed region: exactly `steps` steps bracketed by synchronisation;
+        # events on the stream split it into runs
         t_start = torch.cuda.Event(enable_timing=True)
         t_end = torch.cuda.Event(enable_timing=True)
         marks, bounds = run_marks(reps)
@@ -353,23 +380,63 @@ def main():
         i = 0
         for mk, bd in zip(marks, bounds):
             while i < bd:
-                g_step.replay()
+                run_step_block(i * R)
                 i += 1
             mk.record(stream)
         t_end.record(stream)
         torch.cuda.synchronize()
         ms_step = t_start.elapsed_time(t_end) / steps
         run_ms = run_times(t_start, marks, bounds, R)
+        # each pass alone, timed with HIP events on the stream it runs on:
+        # the average duration of one launch of its kernel
         per_pass = {}
         for p in timed:
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record(stream)
-            for _ in range(reps):
-                g_pass[p].replay()
+            for k in range(reps):
+                run_pass_block(p, k * R)
             b.record(stream)
             torch.cuda.synchronize()
             per_pass[p] = a.elapsed_time(b) / (reps * R)
+        # a plain device copy of one activation tensor, rotated like the inputs
+        scratch = torch.empty_like(sets[0][0])
+        ncopy = 10
+
+        def copies():
+            for k in range(ncopy):
+                scratch.copy_(sets[k % nsets][0])
+        if not args.eager:
+            g_copy = torch.cuda.CUDAGraph()
+            cs = torch.cuda.Stream(dev)
+            cs.wait_stream(stream)
+            with torch.cuda.graph(g_copy, stream=cs):
+                copies()
+            stream.wait_stream(cs)
+            torch.cuda.synchronize()
+            copies = g_copy.replay
+        copies()
+        torch.cuda.synchronize()
+        ca, cb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ncr = max(1, min(reps, 100))
+        ca.record(stream)
+        for _ in range(ncr):
+            copies()
+        cb.record(stream)
+        torch.cuda.synchronize()
+        copy_ms = ca.elapsed_time(cb) / (ncr * ncopy)
+        return {"ms_step": ms_step, "run_ms": run_ms, "per_pass": per_pass, "eager_ms": eager_ms,
+                "copy_gbps": 2 * act_bytes / (copy_ms * 1e-3) / 1e9, "nsets": nsets}
+
+    # the headline mode first (cache-warm; --cold makes the rotated sets the
+    # headline), then the other mode
+    warm_sets = make_sets(1)
+    cold_sets = warm_sets + make_sets(n_cold - 1)
+    first = measure(cold_sets if args.cold else warm_sets)
+    other = measure(warm_sets if args.cold else cold_sets)
+    main_m, warm_m, cold_m = first, (other if args.cold else first), (first if args.cold else other)
     args.steps = steps
+    ms_step, run_ms, per_pass = main_m["ms_step"], main_m["run_ms"], main_m["per_pass"]
+    nsets = main_m["nsets"]
 
     flops = wl.flops()
     tflops = flops / (ms_step * 1e-3) / 1e12
@@ -382,24 +449,7 @@ def main():
     dom_flops = pass_flops(wl, dom)
     ai = dom_flops / dom_bytes
     ridge = peak * 1e12 / (HBM_PEAK_GBS * 1e9)
-    fk = "wbmm_fwd_img_kernel" if image_layout(wl) else "wbmm_fwd_kernel"
-    tl = "true" if fixed_offset_rows(wl) else "false"
-    # channel-stream gradients: fixed-offset rows and no more channels than
-    # compute units (256 on MI355X)
-    chan_stream = fixed_offset_rows(wl) and wl.C <= torch.cuda.get_device_properties(0).multi_processor_count
-    dtk = "wbmm_bwd_stream_kernel" if chan_stream else "wbmm_dt_kernel"
-    bwk = "wbmm_bwd_stream_kernel" if chan_stream else "wbmm_bwd_kernel"
-    # names as the profiler prints them (every template argument)
-    img = fk == "wbmm_fwd_img_kernel"
-    fwd_tail = (lambda rev, hier: "<%s,%d," + rev + "," + hier + ">") if img else \
-        (lambda rev, hier: "<%s,%d," + rev + "," + hier + "," + (tl if hier == "false" else "false") + ">")
-    kernel_name = {"fwd": fk + fwd_tail("false", "false"), "dx": fk + fwd_tail("true", "false"),
-                   "dt": dtk + ("<%s,%d,false,0>" if chan_stream else "<%s,%d," + tl + ">"),
-                   "bwd": bwk + ("<%s,%d,true,0>" if chan_stream else "<%s,%d," + tl + ">"),
-                   "hfwd": fk + fwd_tail("false", "true"),
-                   "hbwd": ("wbmm_bwd_stream_kernel<%s,%d,true," + str(wl.w // 2) + ">") if chan_stream and wl.w >= 10
-                           else "wbmm_hier_backward (several launches) <%s,%d>"}[dom] % (
-                       {"bf16": "TagBF16", "f16": "TagF16", "f32": "TagF32"}[wl.dtype], wl.w)
+    kernel_name = kernel_names(wl, torch.cuda.get_device_properties(0).multi_processor_count)[dom]
     if ai < ridge:
         achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
@@ -415,38 +465,7 @@ def main():
     roof.update({"traffic": traffic, "kernel": kernel_name, "pass": dom,
                  "avg_ms": round(dom_ms, 5), "algorithmic_bytes": dom_bytes,
                  "algorithmic_flops": dom_flops})
-
-    # the bandwidth a plain device copy of one activation tensor reaches on
-    # this GPU, in the same cache mode (the same input sets rotated), as a
-    # measured ceiling beside the nominal HBM peak
-    act_bytes = wl.B * wl.C * wl.H * wl.W * es
-    scratch = torch.empty_like(sets[0][0])
-    ncopy = 10
-    if args.eager:
-        def copies():
-            for i in range(ncopy):
-                scratch.copy_(sets[i % nsets][0])
-    else:
-        g_copy = torch.cuda.CUDAGraph()
-        cs = torch.cuda.Stream(dev)
-        cs.wait_stream(stream)
-        with torch.cuda.graph(g_copy, stream=cs):
-            for i in range(ncopy):
-                scratch.copy_(sets[i % nsets][0])
-        stream.wait_stream(cs)
-        torch.cuda.synchronize()
-        copies = g_copy.replay
-    copies()
-    torch.cuda.synchronize()
-    ca, cb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    ncr = max(1, min(reps, 100))
-    ca.record(stream)
-    for _ in range(ncr):
-        copies()
-    cb.record(stream)
-    torch.cuda.synchronize()
-    copy_ms = ca.elapsed_time(cb) / (ncr * ncopy)
-    copy_gbps = 2 * act_bytes / (copy_ms * 1e-3) / 1e9
+    copy_gbps = main_m["copy_gbps"]
     roof["copy_gbps"] = round(copy_gbps, 1)
     if roof["bound"] == "hbm":
         roof["frac_of_copy"] = round(roof["achieved"] / copy_gbps, 4)
@@ -462,6 +481,20 @@ def main():
     med, q1, q3 = quartiles(run_ms)
     runs = {"n": len(run_ms), "ms_per_step": [round(v, 5) for v in run_ms],
             "median_ms": round(med, 5), "iqr_ms": [round(q1, 5), round(q3, 5)]}
+
+    def mode_summary(m):
+        """Step and dominant-kernel figures of one cache mode."""
+        t = flops / (m["ms_step"] * 1e-3) / 1e12
+        dms = m["per_pass"][dom]
+        ach = dom_bytes / (dms * 1e-3) / 1e9
+        mmed, mq1, mq3 = quartiles(m["run_ms"])
+        return {"input_sets": m["nsets"], "ms_per_step": round(m["ms_step"], 5), "value": round(t, 3),
+                "pct_bf16_mfma_peak": round(100 * t / peak, 3),
+                "per_pass_ms": {k: round(v, 5) for k, v in m["per_pass"].items()},
+                "runs_median_ms": round(mmed, 5), "runs_iqr_ms": [round(mq1, 5), round(mq3, 5)],
+                "dominant": {"kernel": kernel_name, "avg_ms": round(dms, 5), "achieved_gbps": round(ach, 1),
+                             "frac_hbm": round(ach / HBM_PEAK_GBS, 4), "copy_gbps": round(m["copy_gbps"], 1),
+                             "frac_of_copy": round(ach / m["copy_gbps"], 4)}}
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -506,10 +539,12 @@ def main():
         "pct_bf16_mfma_peak": round(100 * tflops / peak, 3),
         "per_pass_ms": {k: round(v, 5) for k, v in per_pass.items()},
         "launch": "eager stream launches" if args.eager else "HIP graph replay, %d steps per graph" % R,
-        "eager_ms_per_step": round(eager_ms, 5),
+        "eager_ms_per_step": round(main_m["eager_ms"], 5),
         "roofline": roof,
         "step_roofline": step_roof,
         "runs": runs,
+        "warm": mode_summary(warm_m),
+        "cold": mode_summary(cold_m),
         "cpu_baseline": cpu,
     }
     print(json.dumps(out))

@@ -72,8 +72,12 @@ wbmm_status wbmm_forward(const void *x, const void *table, void *y,
                          wbmm_dtype dtype, void *stream);
 
 /* Gradient with respect to the input for upstream gradient dy: per window,
- * dx = dy * M_c^T.  Because I[j,i] = (2w-1)^2 - 1 - I[i,j], M_c^T is the
- * matrix of the reversed table, so this runs the forward kernels with the
+ * dx = dy * M_c^T.  The paper does not write the backward pass out; this is
+ * the chain rule applied to the per-window product Y_b = X_b M of Alg. 1 and
+ * Theorem 3.2 (row-vector convention, i = input, j = output), with padded
+ * positions (Sec. "Handling Arbitrary Input Sizes") receiving nothing.
+ * Because I[j,i] = (2w-1)^2 - 1 - I[i,j] (eq. index_computation), M_c^T is
+ * the matrix of the reversed table, so this runs the forward kernels with the
  * table read back to front.  dy, dx: [B,C,H,W] in dtype. */
 wbmm_status wbmm_backward_input(const void *dy, const void *table, void *dx,
                                 int64_t B, int64_t C, int64_t H, int64_t W,
@@ -89,9 +93,12 @@ size_t wbmm_backward_table_workspace_bytes(int64_t B, int64_t C, int64_t H,
 /* Gradient with respect to the table:
  *   dtable[c, k] = sum over images, windows and (input i, output j) pairs with
  *                  I[i, j] = k of x[.., i] * dy[.., j]
- * (the scatter-add of the per-window products X^T dY over the relative-offset
- * index).  x, dy: [B,C,H,W] in dtype; dtable: float32 [C,(2w-1)^2],
- * overwritten.
+ * i.e. the per-window products X^T dY scattered back onto the table through
+ * the index of eq. index_select (M_c = T[c, I]).  The paper states that
+ * during training the gradients flow through the table and M is rebuilt on
+ * every forward pass (Sec. "Inference Caching Mechanism"); the formula is the
+ * chain rule on Alg. 1 and Theorem 3.2.  x, dy: [B,C,H,W] in dtype; dtable:
+ * float32 [C,(2w-1)^2], overwritten.
  *
  * workspace: device buffer of at least wbmm_backward_table_workspace_bytes()
  * bytes (may be NULL when that is 0).  It starts with one 32-bit counter per
@@ -118,7 +125,9 @@ size_t wbmm_backward_workspace_bytes(int64_t B, int64_t C, int64_t H, int64_t W,
                                      int w, wbmm_dtype dtype);
 
 /* Both gradients in one pass (the input gradient of wbmm_backward_input and
- * the table gradient of wbmm_backward_table): every window of x and dy is
+ * the table gradient of wbmm_backward_table, the chain rule on Alg. 1 and
+ * Theorem 3.2 for the training mode of Sec. "Inference Caching Mechanism",
+ * where gradients flow through the table): every window of x and dy is
  * read once.  Results equal those of the two separate calls bit for bit.
  * x, dy, dx: [B,C,H,W] in dtype; table: [C,(2w-1)^2] in dtype; dtable: float32
  * [C,(2w-1)^2], overwritten.  dx and dtable must not overlap any input, each

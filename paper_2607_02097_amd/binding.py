@@ -173,16 +173,27 @@ def wbmm_backward_table_workspace_bytes(shape, w: int, dtype) -> int:
 _WS_CACHE = {}
 
 
+def _torch_stream(device, stream):
+    """The torch stream object of the stream a call is enqueued on."""
+    if stream is None:
+        return torch.cuda.current_stream(device)
+    if isinstance(stream, torch.cuda.Stream):
+        return stream
+    return torch.cuda.ExternalStream(int(stream), device=device)
+
+
 def _cached_workspace(device, nbytes, stream, shape_key):
     """A zero-filled workspace kept per (device, stream, call shape).  The
     library leaves its counters at zero after every call, so a workspace is
-    zero-filled once, when it is created for a new shape."""
-    st = torch.cuda.current_stream(device).cuda_stream if stream is None else \
-        int(getattr(stream, "cuda_stream", stream))
-    key = (str(device), st, shape_key)
+    zero-filled once, when it is created for a new shape.  It is allocated and
+    zero-filled on the stream the call is enqueued on, so the fill is ordered
+    before the kernel that reads the counters whatever the current stream is."""
+    ts = _torch_stream(device, stream)
+    key = (str(device), ts.cuda_stream, shape_key)
     ws = _WS_CACHE.get(key)
     if ws is None:
-        ws = torch.zeros(nbytes, dtype=torch.uint8, device=device)
+        with torch.cuda.stream(ts):
+            ws = torch.zeros(nbytes, dtype=torch.uint8, device=device)
         _WS_CACHE[key] = ws
     return ws
 

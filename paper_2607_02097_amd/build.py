@@ -1,13 +1,20 @@
 """Build the WBMM HIP library (libwbmm.so) in-tree for gfx950 with hipcc.
 
 Usage: python -m paper_2607_02097_amd.build   (or call build()).
+
+After compiling, the device code of every HIP object is disassembled and the
+build fails if any instruction reaches memory through the flat address space:
+the kernels address on-chip LDS with ds_* instructions and device memory with
+global_* instructions only (a flat access to LDS beyond 64 KB faults).
 """
 from __future__ import annotations
 
 import os
+import re
 import shutil
 import subprocess
 import sys
+import tempfile
 import time
 from concurrent.futures import ThreadPoolExecutor
 
@@ -17,6 +24,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libwbmm.so")
 OBJ_DIR = os.path.join(PKG, "_build")
+LLVM_BIN = "/opt/rocm/llvm/bin"
 
 ARCH = "gfx950"
 # Packed fp32 VALU forms are kept out of generated code on purpose.
@@ -25,9 +33,10 @@ HIP_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++20", "-fPIC",
              "-I" + INCLUDE, "-I" + CSRC]
 
 # (source, extra defines): the kernel templates are instantiated once per
-# (dtype, window range) so the translation units compile in parallel.
+# (dtype, range of four window sizes) so the translation units compile in
+# parallel; the largest windows (slowest units) first.
 UNITS = [("wbmm_inst.hip", ["-DWBMM_INST_TAG=%s" % tag, "-DWBMM_INST_LO=%d" % lo])
-         for tag in ("TagBF16", "TagF32", "TagF16") for lo in (9, 1)]
+         for lo in (13, 9, 5, 1) for tag in ("TagBF16", "TagF16", "TagF32")]
 UNITS += [("wbmm_dense.hip", []), ("wbmm_dispatch.cpp", []), ("wbmm_api.cpp", [])]
 
 
@@ -52,12 +61,54 @@ def _compile(unit) -> str:
     return obj
 
 
+def device_disassembly(obj: str) -> str:
+    """The gfx950 device code of one HIP object file, disassembled."""
+    tool = lambda n: os.path.join(LLVM_BIN, n)
+    with tempfile.TemporaryDirectory() as td:
+        fb, co = os.path.join(td, "fatbin"), os.path.join(td, "dev.co")
+        subprocess.run([tool("llvm-objcopy"), "--dump-section=.hip_fatbin=" + fb, obj],
+                       check=True, capture_output=True)
+        subprocess.run([tool("clang-offload-bundler"), "--unbundle", "--type=o", "--input=" + fb,
+                        "--targets=hipv4-amdgcn-amd-amdhsa--" + ARCH, "--output=" + co],
+                       check=True, capture_output=True)
+        r = subprocess.run([tool("llvm-objdump"), "-d", "--mcpu=" + ARCH, co],
+                           check=True, capture_output=True, text=True)
+        return r.stdout
+
+
+def flat_accesses(disasm: str) -> list:
+    """(kernel symbol, instruction) of every flat-address-space access."""
+    out, sym = [], "?"
+    for line in disasm.splitlines():
+        m = re.match(r"^[0-9a-f]+ <(.+)>:$", line)
+        if m:
+            sym = m.group(1)
+            continue
+        m = re.search(r"\b(flat_[a-z0-9_]+)\b", line)
+        if m:
+            out.append((sym, m.group(1)))
+    return out
+
+
+def check_no_flat(objs) -> None:
+    bad = []
+    for o in objs:
+        if o.endswith(".hip.o") or ".hip." in os.path.basename(o):
+            bad += [(os.path.basename(o),) + f for f in flat_accesses(device_disassembly(o))]
+    if bad:
+        lines = "\n".join("  %s: %s in %s" % (o, ins, sym) for o, sym, ins in bad[:20])
+        raise RuntimeError("device code reaches memory through flat instructions "
+                           "(%d found); every LDS pointer must stay in the local "
+                           "address space:\n%s" % (len(bad), lines))
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(OBJ_DIR, exist_ok=True)
     t0 = time.time()
     jobs = max(1, min(len(UNITS), int(os.environ.get("MAX_JOBS", os.cpu_count() or 4))))
     with ThreadPoolExecutor(max_workers=jobs) as ex:
         objs = list(ex.map(_compile, UNITS))
+    check_no_flat(objs)
     tmp = LIB + ".tmp%d" % os.getpid()
     cmd = [hipcc(), "--offload-arch=" + ARCH, "-shared", "-fPIC"] + objs + ["-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -6,20 +6,26 @@
 
 namespace wbmm {
 
-extern Entry entries_TagF32_1[8], entries_TagF32_9[8];
-extern Entry entries_TagBF16_1[8], entries_TagBF16_9[8];
-extern Entry entries_TagF16_1[8], entries_TagF16_9[8];
+#define WBMM_TABLES(tag)                                                                  \
+  extern Entry entries_##tag##_1[kInstWindows], entries_##tag##_5[kInstWindows],          \
+      entries_##tag##_9[kInstWindows], entries_##tag##_13[kInstWindows];                 \
+  static Entry *const tables_##tag[4] = {entries_##tag##_1, entries_##tag##_5, entries_##tag##_9, \
+                                         entries_##tag##_13};
+WBMM_TABLES(TagF32)
+WBMM_TABLES(TagBF16)
+WBMM_TABLES(TagF16)
+#undef WBMM_TABLES
 
 namespace {
 
 const Entry *find(Dt dt, int w) {
   if (w < kMinWindow || w > kMaxWindow) return nullptr;
-  const int hi = w > 8;
-  const int k = hi ? w - 9 : w - 1;
+  const int u = (w - 1) / kInstWindows;
+  const int k = (w - 1) % kInstWindows;
   switch (dt) {
-    case Dt::F32: return hi ? &entries_TagF32_9[k] : &entries_TagF32_1[k];
-    case Dt::BF16: return hi ? &entries_TagBF16_9[k] : &entries_TagBF16_1[k];
-    case Dt::F16: return hi ? &entries_TagF16_9[k] : &entries_TagF16_1[k];
+    case Dt::F32: return &tables_TagF32[u][k];
+    case Dt::BF16: return &tables_TagBF16[u][k];
+    case Dt::F16: return &tables_TagF16[u][k];
   }
   return nullptr;
 }

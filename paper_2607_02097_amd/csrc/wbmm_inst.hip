@@ -1,5 +1,5 @@
 // One translation unit of kernel instantiations: dtype WBMM_INST_TAG
-// (TagF32 / TagBF16 / TagF16) and window sizes WBMM_INST_LO..WBMM_INST_LO+7.
+// (TagF32 / TagBF16 / TagF16) and window sizes WBMM_INST_LO..WBMM_INST_LO+3.
 // The build compiles this file once per (dtype, window range) so the
 // instantiations compile in parallel; wbmm_dispatch.cpp collects the tables.
 #include "wbmm_kernels.h"
@@ -25,7 +25,6 @@ namespace wbmm {
         &run_hier_forward<WBMM_INST_TAG, WBMM_INST_LO + W_>,                   \
         &run_hier_stream<WBMM_INST_TAG, WBMM_INST_LO + W_>}
 
-Entry WBMM_TABLE(WBMM_INST_TAG, WBMM_INST_LO)[8] = {
-    WBMM_E(0), WBMM_E(1), WBMM_E(2), WBMM_E(3), WBMM_E(4), WBMM_E(5), WBMM_E(6), WBMM_E(7)};
+Entry WBMM_TABLE(WBMM_INST_TAG, WBMM_INST_LO)[kInstWindows] = {WBMM_E(0), WBMM_E(1), WBMM_E(2), WBMM_E(3)};
 
 }  // namespace wbmm

@@ -21,6 +21,8 @@ struct Geom {
 
 constexpr int kMinWindow = 1;
 constexpr int kMaxWindow = 16;
+// window sizes per instantiation unit (wbmm_inst.hip)
+constexpr int kInstWindows = 4;
 
 // Launch plan of the dtable pass: windows per slab and number of slabs; one
 // workgroup per (channel, slab).  Slabs > 1 need a float32 workspace of

@@ -1634,6 +1634,27 @@ __device__ __attribute__((always_inline)) inline void dt_bin_sum_local(const flo
   }
 }
 
+// Ticket of the slab workgroups of channel c: every thread publishes its
+// partial-sum stores at device scope (release fence), one thread takes the
+// ticket with an acquire-release increment of the channel's counter, and the
+// channel's last workgroup (ticket nslab - 1) acquires at device scope before
+// any of its threads reads the other slabs' partials.  Returns true in every
+// thread of that last workgroup.  smem[0..3] holds the flag.
+__device__ __attribute__((always_inline)) inline bool slab_ticket_last(unsigned char *smem, unsigned *__restrict__ cnt,
+                                                                        int64_t c, int nslab) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __syncthreads();
+  int *flag = reinterpret_cast<int *>(smem);
+  if (threadIdx.x == 0) {
+    const unsigned ticket = __hip_atomic_fetch_add(&cnt[c], 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    *flag = ticket == (unsigned)(nslab - 1);
+  }
+  __syncthreads();
+  if (*flag == 0) return false;
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  return true;
+}
+
 // Hierarchical form: both table gradients of the slab from their bins (one
 // window row per tile: bin k of either table is its entry k); with several
 // slabs per channel one ticket per workgroup, and the channel's last
@@ -1663,15 +1684,7 @@ __device__ __attribute__((always_inline)) inline void dt_reduce_hier(unsigned ch
     }
   }
   if (single) return;
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  int *flag = reinterpret_cast<int *>(smem);
-  if (tid == 0) {
-    const unsigned ticket = __hip_atomic_fetch_add(&cnt[c], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    *flag = ticket == (unsigned)(a.tiles_per_ch - 1);
-  }
-  __syncthreads();
-  if (*flag == 0) return;
+  if (!slab_ticket_last(smem, cnt, c, a.tiles_per_ch)) return;
   constexpr int SG = 8;
   for (int k = tid; k < KT; k += NTH) {
     const bool loc = k >= K2;
@@ -1743,18 +1756,7 @@ __device__ __attribute__((always_inline)) inline void dt_reduce(unsigned char *s
   // Several slabs per channel: the last workgroup of the channel to finish
   // (ticket from the channel's counter) sums the slabs' partials in slab
   // order and resets the counter, so the result does not depend on timing.
-  // The partial stores are device-coherent; waiting for their completion
-  // before the barrier orders them before the ticket without a cache
-  // write-back.
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  int *flag = reinterpret_cast<int *>(smem);
-  if (tid == 0) {
-    const unsigned ticket = __hip_atomic_fetch_add(&cnt[c], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    *flag = ticket == (unsigned)(a.tiles_per_ch - 1);
-  }
-  __syncthreads();
-  if (*flag == 0) return;
+  if (!slab_ticket_last(smem, cnt, c, a.tiles_per_ch)) return;
   // all loads of a group of slabs are issued before the sums, which keep
   // the slab order
   constexpr int KPT = cdiv(K2, NTH);

@@ -198,3 +198,22 @@ def test_dense_rejects_bad_arguments(lib):
     assert lib.wbmm_bin_matrix(vp(FAKE), vp(FAKE + 64), 2, 3, 5, None) == E   # overlap
     assert lib.wbmm_bin_matrix(vp(0), vp(FAKE * 8), 2, 3, 5, None) == E
     assert lib.wbmm_bin_matrix(vp(FAKE), vp(FAKE * 8), 2, 3, 0, None) == E
+
+
+def test_build_rejects_flat_memory_instructions():
+    """The build's guard finds flat-address-space accesses in a disassembly
+    and names their kernel; ds_*, global_* and buffer_* accesses pass."""
+    from paper_2607_02097_amd import build as B
+    listing = "\n".join([
+        "0000000000001000 <_ZN4wbmm6kernelILi1EEEvv>:",
+        "\tds_read_b128 v[0:3], v4",
+        "\tglobal_load_dwordx4 v[0:3], v[4:5], off",
+        "\tbuffer_load_dword v1, off, s[0:3], 0",
+        "0000000000002000 <_ZN4wbmm6kernelILi2EEEvv>:",
+        "\tflat_load_dwordx4 v[0:3], v[4:5]",
+        "\tflat_store_dword v[4:5], v1",
+    ])
+    found = B.flat_accesses(listing)
+    assert found == [("_ZN4wbmm6kernelILi2EEEvv", "flat_load_dwordx4"),
+                     ("_ZN4wbmm6kernelILi2EEEvv", "flat_store_dword")]
+    assert B.flat_accesses(listing.split("0000000000002000")[0]) == []

@@ -6,7 +6,9 @@ mathematics, independent of the oracle's own loops:
   counts, translation);
 * Theorem 3.1/3.2: inside one window WBMM is a depthwise cross-correlation with
   a (2w-1)x(2w-1) kernel and zero padding w-1 -> torch's conv2d in fp64;
-* Alg. 1's matrix form (index-select M, partition, batched matmul) in numpy;
+* the operator as a sum over relative offsets (linearity in the table: each
+  offset shifts every window by itself), in numpy, and its gradients through
+  torch autograd;
 * one-hot tables: the output is exactly a shifted copy of the input;
 * the backward passes: exact finite differences on integer data (the operator
   is bilinear, so a step-1 central difference has no truncation error), the
@@ -108,20 +110,40 @@ def conv_reference(x, t, wh, ww):
     return out.reshape(B, C, NH * wh, NW * ww)[:, :, :H, :W]
 
 
-def matrix_form(x, t, wh, ww):
-    """Alg. 1 written with numpy: I from its defining equation, M = T[:, I],
-    partition to [C, N, d], Y_batch = X_batch @ M, inverse reshape."""
+def shift_sum_form(x, t, wh, ww, xp=np):
+    """The operator as a sum over relative offsets (linearity in the table):
+    for each offset (dh, dw) = input - output, every output position p of a
+    window receives T[c, k(dh, dw)] * X[p + (dh, dw)] when p + (dh, dw) lies
+    in the same (zero-padded) window.  Written as slices of the windowed
+    array, one offset at a time; works on numpy arrays or, with xp=torch, on
+    torch tensors (differentiable)."""
     B, C, H, W = x.shape
     NH, NW = -(-H // wh), -(-W // ww)
-    hh, xx = np.divmod(np.arange(wh * ww), ww)
-    I = (hh[:, None] - hh[None, :] + wh - 1) * (2 * ww - 1) + (xx[:, None] - xx[None, :] + ww - 1)
-    M = t[:, I.ravel()].reshape(C, wh * ww, wh * ww)
-    xp = np.zeros((B, C, NH * wh, NW * ww))
-    xp[:, :, :H, :W] = x
-    xb = xp.reshape(B, C, NH, wh, NW, ww).transpose(1, 0, 2, 4, 3, 5).reshape(C, -1, wh * ww)
-    yb = np.matmul(xb, M)
-    y = yb.reshape(C, B, NH, NW, wh, ww).transpose(1, 0, 2, 4, 3, 5).reshape(B, C, NH * wh, NW * ww)
-    return y[:, :, :H, :W]
+    K1w = 2 * ww - 1
+    if xp is np:
+        pad = np.zeros((B, C, NH * wh, NW * ww))
+        pad[:, :, :H, :W] = x
+        y = np.zeros_like(pad)
+    else:
+        pad = torch.nn.functional.pad(x, (0, NW * ww - W, 0, NH * wh - H))
+        y = torch.zeros_like(pad)
+    win = pad.reshape(B, C, NH, wh, NW, ww)
+    yw = y.reshape(B, C, NH, wh, NW, ww)
+    for dh in range(-(wh - 1), wh):
+        for dw in range(-(ww - 1), ww):
+            k = (dh + wh - 1) * K1w + (dw + ww - 1)
+            # outputs ho with 0 <= ho + dh < wh, xo with 0 <= xo + dw < ww
+            ho0, ho1 = max(0, -dh), min(wh, wh - dh)
+            xo0, xo1 = max(0, -dw), min(ww, ww - dw)
+            coef = t[:, k].reshape(1, C, 1, 1, 1, 1)
+            src = win[:, :, :, ho0 + dh:ho1 + dh, :, xo0 + dw:xo1 + dw]
+            if xp is np:
+                yw[:, :, :, ho0:ho1, :, xo0:xo1] += coef * src
+            else:
+                upd = torch.zeros_like(yw)
+                upd[:, :, :, ho0:ho1, :, xo0:xo1] = coef * src
+                yw = yw + upd
+    return yw.reshape(B, C, NH * wh, NW * ww)[:, :, :H, :W]
 
 
 @pytest.mark.parametrize("shape,w", [
@@ -138,7 +160,7 @@ def test_forward_equals_windowed_depthwise_conv(olib, shape, w):
     t = r.standard_normal((shape[1], (2 * wh - 1) * (2 * ww - 1)))
     y = oracle.forward(x, t, w, lib=olib)
     assert rel_err(y, conv_reference(x, t, wh, ww)) < 1e-13
-    assert rel_err(y, matrix_form(x, t, wh, ww)) < 1e-13
+    assert rel_err(y, shift_sum_form(x, t, wh, ww)) < 1e-13
 
 
 def test_single_window_is_plain_depthwise_conv(olib):
@@ -232,8 +254,9 @@ def test_backward_input_is_forward_with_reversed_table(olib):
         assert rel_err(a, b) < 1e-14
 
 
-def test_backward_table_matches_autograd_of_matrix_form(olib):
-    """dT of Alg. 1 through torch autograd (gather + bmm) in fp64."""
+def test_gradients_match_autograd_of_shift_sum_form(olib):
+    """dX and dT of the shift-and-add form through torch autograd (fp64): an
+    independent formulation of the operator differentiated by the library."""
     r = rng(8)
     B, C, H, W, w = 2, 3, 10, 12, 5
     x = r.standard_normal((B, C, H, W))
@@ -241,14 +264,8 @@ def test_backward_table_matches_autograd_of_matrix_form(olib):
     t = r.standard_normal((C, (2 * w - 1) ** 2))
     tt = torch.tensor(t, requires_grad=True)
     xx = torch.tensor(x, requires_grad=True)
-    hh, ww = np.divmod(np.arange(w * w), w)
-    I = torch.from_numpy((hh[:, None] - hh[None, :] + w - 1) * (2 * w - 1) + (ww[:, None] - ww[None, :] + w - 1))
-    M = tt[:, I.reshape(-1)].reshape(C, w * w, w * w)
-    NH, NW = -(-H // w), -(-W // w)
-    xp = torch.nn.functional.pad(xx, (0, NW * w - W, 0, NH * w - H))
-    xb = xp.reshape(B, C, NH, w, NW, w).permute(1, 0, 2, 4, 3, 5).reshape(C, -1, w * w)
-    yb = torch.bmm(xb, M)
-    y = yb.reshape(C, B, NH, NW, w, w).permute(1, 0, 2, 4, 3, 5).reshape(B, C, NH * w, NW * w)[:, :, :H, :W]
+    y = shift_sum_form(xx, tt, w, w, xp=torch)
+    assert rel_err(y.detach().numpy(), oracle.forward(x, t, w, lib=olib)) < 1e-13
     (y * torch.from_numpy(dy)).sum().backward()
     assert rel_err(oracle.backward_table(x, dy, w, lib=olib), tt.grad.numpy()) < 1e-13
     assert rel_err(oracle.backward_input(dy, t, w, lib=olib), xx.grad.numpy()) < 1e-13
