@@ -43,6 +43,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cold", action="store_true",
                    help="rotate through enough input sets to defeat the 256 MB Infinity Cache")
+    p.add_argument("--one-mode", action="store_true",
+                   help="measure only the headline cache mode (hardware-counter runs)")
     p.add_argument("--eager", action="store_true",
                    help="launch without HIP graphs (for hardware-counter runs)")
     p.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
@@ -430,9 +432,9 @@ def main():
     # the headline mode first (cache-warm; --cold makes the rotated sets the
     # headline), then the other mode
     warm_sets = make_sets(1)
-    cold_sets = warm_sets + make_sets(n_cold - 1)
+    cold_sets = warm_sets + make_sets(n_cold - 1) if (args.cold or not args.one_mode) else None
     first = measure(cold_sets if args.cold else warm_sets)
-    other = measure(warm_sets if args.cold else cold_sets)
+    other = None if args.one_mode else measure(warm_sets if args.cold else cold_sets)
     main_m, warm_m, cold_m = first, (other if args.cold else first), (first if args.cold else other)
     args.steps = steps
     ms_step, run_ms, per_pass = main_m["ms_step"], main_m["run_ms"], main_m["per_pass"]
@@ -543,8 +545,8 @@ def main():
         "roofline": roof,
         "step_roofline": step_roof,
         "runs": runs,
-        "warm": mode_summary(warm_m),
-        "cold": mode_summary(cold_m),
+        "warm": mode_summary(warm_m) if warm_m else None,
+        "cold": mode_summary(cold_m) if cold_m else None,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out))

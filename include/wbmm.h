@@ -101,26 +101,22 @@ size_t wbmm_backward_table_workspace_bytes(int64_t B, int64_t C, int64_t H,
  * float32 [C,(2w-1)^2], overwritten.
  *
  * workspace: device buffer of at least wbmm_backward_table_workspace_bytes()
- * bytes (may be NULL when that is 0).  It starts with one 32-bit counter per
- * channel (the first ceil(4C/256)*256 bytes), followed by per-slab partial
- * sums.  The counters must be ZERO when a call starts: zero-fill the
- * workspace before its first use.  Every call that completes leaves its
- * counters at zero again, so repeated calls with the same shape (or with fewer
- * channels) reuse the workspace as it is; before a call with more channels,
- * zero the first ceil(4C/256)*256 bytes again (they may hold partial sums of
- * earlier calls).  Calls that run concurrently must not share a workspace.
- * The partial-sum area may hold anything on entry.
+ * bytes (may be NULL when that is 0), 4-byte aligned.  When a channel's
+ * windows are split into several slabs, each slab writes its partial table
+ * gradient there ([slabs, C, (2w-1)^2] float32) and a second kernel, enqueued
+ * on the same stream, sums the partials into dtable.  The workspace may hold
+ * anything on entry and is left holding partial sums; calls that can run
+ * concurrently must not share one.
  *
- * The reduction has a fixed order (slab partials are summed in slab order by
- * the last workgroup of each channel): the result is bitwise reproducible for
- * a given shape. */
+ * The reduction has a fixed order (slab partials are summed in slab order):
+ * the result is bitwise reproducible for a given shape. */
 wbmm_status wbmm_backward_table(const void *x, const void *dy, float *dtable,
                                 void *workspace, size_t workspace_bytes,
                                 int64_t B, int64_t C, int64_t H, int64_t W,
                                 int w, wbmm_dtype dtype, void *stream);
 
 /* Size in bytes of the device workspace wbmm_backward needs for this shape;
- * equal to wbmm_backward_table_workspace_bytes() (same layout and rules). */
+ * equal to wbmm_backward_table_workspace_bytes() (same use and rules). */
 size_t wbmm_backward_workspace_bytes(int64_t B, int64_t C, int64_t H, int64_t W,
                                      int w, wbmm_dtype dtype);
 
@@ -132,8 +128,7 @@ size_t wbmm_backward_workspace_bytes(int64_t B, int64_t C, int64_t H, int64_t W,
  * x, dy, dx: [B,C,H,W] in dtype; table: [C,(2w-1)^2] in dtype; dtable: float32
  * [C,(2w-1)^2], overwritten.  dx and dtable must not overlap any input, each
  * other or the workspace.  workspace / workspace_bytes: as for
- * wbmm_backward_table (counters zero at the start of a call, left zero at
- * its end; no concurrent sharing). */
+ * wbmm_backward_table (any contents on entry; no concurrent sharing). */
 wbmm_status wbmm_backward(const void *x, const void *dy, const void *table,
                           void *dx, float *dtable, void *workspace,
                           size_t workspace_bytes, int64_t B, int64_t C,
@@ -163,9 +158,9 @@ wbmm_status wbmm_hier_backward_input(const void *dy, const void *table_g,
                                      wbmm_dtype dtype, void *stream);
 
 /* Workspace for wbmm_hier_backward: enough for the two table gradients run
- * one after the other and for both computed in one pass (per-channel
- * counters and both tables' slab partials); same rules as for
- * wbmm_backward_table (counters zero before the first call, left zero). */
+ * one after the other and for both computed in one pass (both tables' slab
+ * partials); same rules as for wbmm_backward_table (any contents on entry,
+ * no concurrent sharing). */
 size_t wbmm_hier_backward_workspace_bytes(int64_t B, int64_t C, int64_t H,
                                           int64_t W, int wl, wbmm_dtype dtype);
 

@@ -183,33 +183,33 @@ def _torch_stream(device, stream):
 
 
 def _cached_workspace(device, nbytes, stream, shape_key):
-    """A zero-filled workspace kept per (device, stream, call shape).  The
-    library leaves its counters at zero after every call, so a workspace is
-    zero-filled once, when it is created for a new shape.  It is allocated and
-    zero-filled on the stream the call is enqueued on, so the fill is ordered
-    before the kernel that reads the counters whatever the current stream is."""
+    """A workspace kept per (device, stream, call shape).  The library writes
+    the partial sums it holds before reading them, so its contents on entry
+    do not matter; it is allocated on the stream the call is enqueued on."""
     ts = _torch_stream(device, stream)
     key = (str(device), ts.cuda_stream, shape_key)
     ws = _WS_CACHE.get(key)
     if ws is None:
         with torch.cuda.stream(ts):
-            ws = torch.zeros(nbytes, dtype=torch.uint8, device=device)
+            ws = torch.empty(nbytes, dtype=torch.uint8, device=device)
         _WS_CACHE[key] = ws
     return ws
 
 
 def new_workspace(nbytes: int, device="cuda") -> torch.Tensor:
-    """A zero-filled workspace for wbmm_backward_table (see include/wbmm.h)."""
-    return torch.zeros(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+    """A workspace for wbmm_backward_table / wbmm_backward (see
+    include/wbmm.h); any contents."""
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
 
 
 def wbmm_backward_table(x: torch.Tensor, dy: torch.Tensor, w: int, out=None, workspace=None,
                         stream=None):
     """dtable (float32 [C,(2w-1)^2], overwritten) for input x and gradient dy.
 
-    ``workspace``: a uint8 device tensor whose counter area is zero (see
-    include/wbmm.h; ``new_workspace`` makes one).  When omitted, a zeroed
-    workspace cached per (device, stream, shape) is used."""
+    ``workspace``: a uint8 device tensor of at least
+    wbmm_backward_table_workspace_bytes() bytes, any contents (see
+    include/wbmm.h; ``new_workspace`` makes one).  When omitted, a workspace
+    cached per (device, stream, shape) is used."""
     _check_tensor(x, "x")
     _check_tensor(dy, "dy")
     if dy.shape != x.shape or dy.dtype != x.dtype or dy.device != x.device:

@@ -82,6 +82,30 @@ wbmm_status forward_like(const void *in, const void *table, void *out, int64_t B
 
 }  // namespace
 
+namespace wbmm {
+
+wbmm_status check_backward_args(const void *x, const void *dy, const void *table, const void *dx,
+                                const float *dtable, int64_t B, int64_t C, int64_t H, int64_t W, int w,
+                                wbmm_dtype dtype, Geom *g, int64_t *bytes) {
+  wbmm_status s = check_shape(B, C, H, W, w, dtype, g, bytes);
+  if (s != WBMM_OK) return s;
+  if (!x || !dy || !table || !dx || !dtable) return WBMM_ERR_INVALID_ARG;
+  const size_t es = elem_size(dtype);
+  if (!aligned(x, es) || !aligned(dy, es) || !aligned(table, es) || !aligned(dx, es) || !aligned(dtable, 4))
+    return WBMM_ERR_INVALID_ARG;
+  const int64_t k2 = (int64_t)(2 * w - 1) * (2 * w - 1);
+  const int64_t tbytes = C * k2 * (int64_t)es;  // table
+  const int64_t gbytes = C * k2 * 4;            // dtable
+  const int64_t n = *bytes;
+  // outputs overlap neither inputs nor each other
+  if (overlap(dx, n, x, n) || overlap(dx, n, dy, n) || overlap(dx, n, table, tbytes) || overlap(dx, n, dtable, gbytes) ||
+      overlap(dtable, gbytes, x, n) || overlap(dtable, gbytes, dy, n) || overlap(dtable, gbytes, table, tbytes))
+    return WBMM_ERR_INVALID_ARG;
+  return WBMM_OK;
+}
+
+}  // namespace wbmm
+
 extern "C" {
 
 wbmm_status wbmm_forward(const void *x, const void *table, void *y, int64_t B, int64_t C, int64_t H,
@@ -134,20 +158,12 @@ wbmm_status wbmm_backward(const void *x, const void *dy, const void *table, void
                           int64_t W, int w, wbmm_dtype dtype, void *stream) {
   Geom g;
   int64_t bytes = 0;
-  wbmm_status s = check_shape(B, C, H, W, w, dtype, &g, &bytes);
+  wbmm_status s = wbmm::check_backward_args(x, dy, table, dx, dtable, B, C, H, W, w, dtype, &g, &bytes);
   if (s != WBMM_OK) return s;
-  if (!x || !dy || !table || !dx || !dtable) return WBMM_ERR_INVALID_ARG;
   const size_t es = elem_size(dtype);
-  if (!aligned(x, es) || !aligned(dy, es) || !aligned(table, es) || !aligned(dx, es) || !aligned(dtable, 4))
-    return WBMM_ERR_INVALID_ARG;
   const int64_t k2 = (int64_t)(2 * w - 1) * (2 * w - 1);
   const int64_t tbytes = C * k2 * (int64_t)es;  // table
   const int64_t gbytes = C * k2 * 4;            // dtable
-  // outputs overlap neither inputs nor each other
-  if (overlap(dx, bytes, x, bytes) || overlap(dx, bytes, dy, bytes) || overlap(dx, bytes, table, tbytes) ||
-      overlap(dx, bytes, dtable, gbytes) || overlap(dtable, gbytes, x, bytes) ||
-      overlap(dtable, gbytes, dy, bytes) || overlap(dtable, gbytes, table, tbytes))
-    return WBMM_ERR_INVALID_ARG;
   const size_t need = wbmm::dtable_workspace_bytes((Dt)dtype, g);
   if (need > 0) {
     if (!workspace || workspace_bytes < need || !aligned(workspace, 4)) return WBMM_ERR_INVALID_ARG;
@@ -203,12 +219,12 @@ size_t wbmm_hier_backward_workspace_bytes(int64_t B, int64_t C, int64_t H, int64
   if (hier_shapes(B, C, H, W, wl, dtype, &gg, &gl, &bytes) != WBMM_OK) return 0;
   const size_t a = wbmm::dtable_workspace_bytes((Dt)dtype, gg), b = wbmm::dtable_workspace_bytes((Dt)dtype, gl);
   size_t need = a > b ? a : b;
-  // one pass over both tables: counters and both tables' partials, for at
-  // most the slabs of the global table's plan
+  // one pass over both tables: both tables' partials, for at most the
+  // slabs of the global table's plan
   const wbmm::DtPlan p = wbmm::plan_dtable((Dt)dtype, gg);
   if (p.slabs > 1) {
     const int64_t kg = (int64_t)(4 * wl - 1) * (4 * wl - 1), kl = (int64_t)(2 * wl - 1) * (2 * wl - 1);
-    const size_t both = (size_t)((C * 4 + 255) / 256 * 256) + (size_t)p.slabs * (size_t)C * (size_t)(kg + kl) * 4;
+    const size_t both = (size_t)p.slabs * (size_t)C * (size_t)(kg + kl) * 4;
     if (both > need) need = both;
   }
   return need;

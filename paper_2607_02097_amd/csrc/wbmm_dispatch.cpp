@@ -80,8 +80,7 @@ size_t dtable_workspace_bytes(Dt dt, const Geom &g) {
   const DtPlan p = plan_dtable(dt, g);
   if (p.slabs <= 1) return 0;
   const int64_t k1 = 2 * g.w - 1;
-  const size_t counters = (size_t)((g.C * 4 + 255) / 256 * 256);
-  return counters + (size_t)p.slabs * (size_t)g.C * (size_t)(k1 * k1) * sizeof(float);
+  return (size_t)p.slabs * (size_t)g.C * (size_t)(k1 * k1) * sizeof(float);
 }
 
 }  // namespace wbmm

@@ -7,6 +7,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include "wbmm.h"
+
 namespace wbmm {
 
 enum class Dt { F32 = 0, BF16 = 1, F16 = 2 };
@@ -34,6 +36,20 @@ struct DtPlan {
 
 DtPlan plan_dtable(Dt dt, const Geom &g);
 size_t dtable_workspace_bytes(Dt dt, const Geom &g);
+
+// Table gradients from per-slab partial sums (wbmm_reduce.hip): after the
+// kernel that wrote them, on the same stream, dt[i] = sum over slabs s, in
+// slab order, of part[s * n + i], for i < n; the same for part2 / dt2 / n2
+// when n2 > 0 (the second table of the hierarchical form).
+hipError_t launch_dt_sum(const float *part, float *dt, int64_t n, const float *part2, float *dt2, int64_t n2,
+                         int slabs, hipStream_t stream);
+
+// Host-side validation of wbmm_backward's tensor arguments (shape, pointers,
+// alignment, overlaps; not the workspace); fills g and the bytes of one
+// [B,C,H,W] tensor (wbmm_api.cpp).
+wbmm_status check_backward_args(const void *x, const void *dy, const void *table, const void *dx,
+                                const float *dtable, int64_t B, int64_t C, int64_t H, int64_t W, int w,
+                                wbmm_dtype dtype, Geom *g, int64_t *bytes);
 
 // Each returns hipSuccess or the error of the launch.
 hipError_t launch_forward(Dt dt, const void *x, const void *table, void *y,

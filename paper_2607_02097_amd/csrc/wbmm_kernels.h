@@ -1634,98 +1634,45 @@ __device__ __attribute__((always_inline)) inline void dt_bin_sum_local(const flo
   }
 }
 
-// Ticket of the slab workgroups of channel c: every thread publishes its
-// partial-sum stores at device scope (release fence), one thread takes the
-// ticket with an acquire-release increment of the channel's counter, and the
-// channel's last workgroup (ticket nslab - 1) acquires at device scope before
-// any of its threads reads the other slabs' partials.  Returns true in every
-// thread of that last workgroup.  smem[0..3] holds the flag.
-__device__ __attribute__((always_inline)) inline bool slab_ticket_last(unsigned char *smem, unsigned *__restrict__ cnt,
-                                                                        int64_t c, int nslab) {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-  __syncthreads();
-  int *flag = reinterpret_cast<int *>(smem);
-  if (threadIdx.x == 0) {
-    const unsigned ticket = __hip_atomic_fetch_add(&cnt[c], 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    *flag = ticket == (unsigned)(nslab - 1);
-  }
-  __syncthreads();
-  if (*flag == 0) return false;
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-  return true;
-}
-
 // Hierarchical form: both table gradients of the slab from their bins (one
-// window row per tile: bin k of either table is its entry k); with several
-// slabs per channel one ticket per workgroup, and the channel's last
-// workgroup sums the partials of both tables in slab order and resets the
-// counter.
+// window row per tile: bin k of either table is its entry k), written as the
+// tables (one slab per channel) or as this slab's partial sums, which the
+// sum kernel adds in slab order once this kernel has finished.
 template <class G, int HL, int NTH>
-__device__ __attribute__((always_inline)) inline void dt_reduce_hier(unsigned char *smem, const float *bing,
-                                                                      const float *binl, float *__restrict__ dtg,
-                                                                      float *__restrict__ dtl, float *__restrict__ partg,
-                                                                      float *__restrict__ partl,
-                                                                      unsigned *__restrict__ cnt, const KArgs &a,
+__device__ __attribute__((always_inline)) inline void dt_reduce_hier(const float *bing, const float *binl,
+                                                                      float *__restrict__ dtg, float *__restrict__ dtl,
+                                                                      float *__restrict__ partg,
+                                                                      float *__restrict__ partl, const KArgs &a,
                                                                       int64_t c, int64_t slab) {
   static_assert(G::R == 1, "one window row per tile");
   constexpr int K2 = G::K2, K2L = (2 * HL - 1) * (2 * HL - 1), KT = K2 + K2L;
   const int tid = threadIdx.x;
   const bool single = a.tiles_per_ch == 1;
+  float *og = single ? dtg + c * K2 : partg + (slab * a.C + c) * K2;
+  float *ol = single ? dtl + c * K2L : partl + (slab * a.C + c) * K2L;
   for (int k = tid; k < KT; k += NTH) {
-    const bool loc = k >= K2;
-    const int kk = loc ? k - K2 : k;
-    const float s = loc ? binl[kk] : bing[kk];
-    if (single) {
-      if (loc) dtl[c * K2L + kk] = s;
-      else dtg[c * K2 + kk] = s;
-    } else {
-      float *dst = loc ? &partl[(slab * a.C + c) * K2L + kk] : &partg[(slab * a.C + c) * K2 + kk];
-      __hip_atomic_store(dst, s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
+    if (k >= K2) ol[k - K2] = binl[k - K2];
+    else og[k] = bing[k];
   }
-  if (single) return;
-  if (!slab_ticket_last(smem, cnt, c, a.tiles_per_ch)) return;
-  constexpr int SG = 8;
-  for (int k = tid; k < KT; k += NTH) {
-    const bool loc = k >= K2;
-    const int kk = loc ? k - K2 : k;
-    float s = 0.f;
-    for (int j0 = 0; j0 < a.tiles_per_ch; j0 += SG) {
-      float v[SG];
-#pragma unroll
-      for (int j = 0; j < SG; ++j) {
-        const int64_t sl = j0 + j;
-        v[j] = sl < a.tiles_per_ch
-                   ? __hip_atomic_load(loc ? &partl[(sl * a.C + c) * K2L + kk] : &partg[(sl * a.C + c) * K2 + kk],
-                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                   : 0.f;
-      }
-#pragma unroll
-      for (int j = 0; j < SG; ++j)
-        if (j0 + j < a.tiles_per_ch) s += v[j];
-    }
-    if (loc) dtl[c * K2L + kk] = s;
-    else dtg[c * K2 + kk] = s;
-  }
-  if (tid == 0) __hip_atomic_store(&cnt[c], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// This slab's table gradient from the bins (a fixed-order combine); with
-// several slabs per channel the channel's last workgroup sums the partials.
+// This slab's table gradient from the bins (a fixed-order combine), written
+// as the table gradient (one slab per channel) or as the slab's partial sums,
+// which the sum kernel adds in slab order once this kernel has finished.
 // NTH threads take part; starts after a workgroup barrier that follows the
 // binning.
 template <class Tag, int WIN, class G, int NTH>
 __device__ __attribute__((always_inline)) inline void dt_reduce(unsigned char *smem, float *__restrict__ dt,
-                                                                 float *__restrict__ part, unsigned *__restrict__ cnt,
-                                                                 const KArgs &a, int64_t c, int64_t slab) {
+                                                                 float *__restrict__ part, const KArgs &a, int64_t c,
+                                                                 int64_t slab) {
   constexpr int NPT = G::NPT, R = G::R;
   constexpr int K1 = G::K1, K2 = G::K2, NBT = G::NBT;
   constexpr int NPM = max_tiles_per_wave<NPT>();
   const int tid = threadIdx.x;
-  float *binsum = reinterpret_cast<float *>(smem) + kWaves * NPM * 272;
-  // this slab's table gradient: combine the (P, sub-row offset) bins of each
-  // offset (dh, dw) in a fixed order
-  const bool single = a.tiles_per_ch == 1;
+  const float *binsum = reinterpret_cast<const float *>(smem) + kWaves * NPM * 272;
+  float *out = a.tiles_per_ch == 1 ? dt + c * K2 : part + (slab * a.C + c) * K2;
+  // combine the (P, sub-row offset) bins of each offset (dh, dw) in a fixed
+  // order
   for (int k = tid; k < K2; k += NTH) {
     float s = 0.f;
     if constexpr (R == 1) {
@@ -1745,70 +1692,28 @@ __device__ __attribute__((always_inline)) inline void dt_reduce(unsigned char *s
         s += binsum[(P + NPT - 1) * NBT + (dh - P * R + R - 1) * K1 + dwi];
       }
     }
-    if (single) {
-      dt[c * K2 + k] = s;
-    } else {
-      // device-coherent store: written through to where every XCD reads it
-      __hip_atomic_store(&part[(slab * a.C + c) * K2 + k], s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
+    out[k] = s;
   }
-  if (single) return;
-  // Several slabs per channel: the last workgroup of the channel to finish
-  // (ticket from the channel's counter) sums the slabs' partials in slab
-  // order and resets the counter, so the result does not depend on timing.
-  if (!slab_ticket_last(smem, cnt, c, a.tiles_per_ch)) return;
-  // all loads of a group of slabs are issued before the sums, which keep
-  // the slab order
-  constexpr int KPT = cdiv(K2, NTH);
-  constexpr int SG = 8;
-  float s[KPT];
-#pragma unroll
-  for (int i = 0; i < KPT; ++i) s[i] = 0.f;
-  for (int j0 = 0; j0 < a.tiles_per_ch; j0 += SG) {
-    float v[KPT][SG];
-#pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int k = tid + i * NTH;
-#pragma unroll
-      for (int j = 0; j < SG; ++j)
-        v[i][j] = (k < K2 && j0 + j < a.tiles_per_ch)
-                      ? __hip_atomic_load(&part[((int64_t)(j0 + j) * a.C + c) * K2 + k], __ATOMIC_RELAXED,
-                                          __HIP_MEMORY_SCOPE_AGENT)
-                      : 0.f;
-    }
-#pragma unroll
-    for (int i = 0; i < KPT; ++i)
-#pragma unroll
-      for (int j = 0; j < SG; ++j)
-        if (j0 + j < a.tiles_per_ch) s[i] += v[i][j];
-  }
-#pragma unroll
-  for (int i = 0; i < KPT; ++i) {
-    const int k = tid + i * NTH;
-    if (k < K2) dt[c * K2 + k] = s[i];
-  }
-  if (tid == 0) __hip_atomic_store(&cnt[c], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Table gradient of the workgroup's slab from the accumulators: diagonal
-// bins, then the slab's dT; with several slabs per channel the channel's
-// last workgroup sums the partials.  Starts with a workgroup barrier (the
-// bins reuse the LDS of the stages).
+// bins, then the slab's dT (or its partial sums).  Starts with a workgroup
+// barrier (the bins reuse the LDS of the stages).
 template <class Tag, int WIN, class G, int WAVE>
 __device__ __attribute__((always_inline)) inline void dt_finish(const f32x4 (&acc)[PSpan<G::NPT, WAVE>::na],
                                                                  unsigned char *smem, float *__restrict__ dt,
-                                                                 float *__restrict__ part, unsigned *__restrict__ cnt,
-                                                                 const KArgs &a, int64_t c, int64_t slab) {
+                                                                 float *__restrict__ part, const KArgs &a, int64_t c,
+                                                                 int64_t slab) {
   __syncthreads();
   dt_bin<Tag, WIN, G, WAVE>(acc, smem);
   __syncthreads();
-  dt_reduce<Tag, WIN, G, kThreads>(smem, dt, part, cnt, a, c, slab);
+  dt_reduce<Tag, WIN, G, kThreads>(smem, dt, part, a, c, slab);
 }
 
 template <class Tag, int WIN, int WAVE, bool TILED>
 __device__ __attribute__((always_inline)) void dt_wave(const typename Tag::S *__restrict__ x, const typename Tag::S *__restrict__ dy,
-                        float *__restrict__ dt, float *__restrict__ part, unsigned *__restrict__ cnt,
-                        const KArgs &a, unsigned char *smem) {
+                        float *__restrict__ dt, float *__restrict__ part, const KArgs &a,
+                        unsigned char *smem) {
   typedef DtCfg<Tag, WIN> G;
   typedef PSpan<G::NPT, WAVE> SP;
   const int tid = threadIdx.x;
@@ -1831,20 +1736,20 @@ __device__ __attribute__((always_inline)) void dt_wave(const typename Tag::S *__
     if (m0 + G::CW < s1) stage_load<Tag, WIN, G, TILED>(a, x, dy, c, m0 + G::CW, s1, tid, st);
     dt_products<Tag, G, WAVE>(smem, smem + G::BUF, acc, lane);
   }
-  dt_finish<Tag, WIN, G, WAVE>(acc, smem, dt, part, cnt, a, c, slab);
+  dt_finish<Tag, WIN, G, WAVE>(acc, smem, dt, part, a, c, slab);
 }
 
 template <class Tag, int WIN, bool TILED>
 __global__ __launch_bounds__(kThreads, 3) void wbmm_dt_kernel(const typename Tag::S *__restrict__ x,
                                                               const typename Tag::S *__restrict__ dy,
                                                               float *__restrict__ dt, float *__restrict__ part,
-                                                              unsigned *__restrict__ cnt, KArgs a) {
+                                                              KArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   switch (threadIdx.x >> 6) {
-    case 0: dt_wave<Tag, WIN, 0, TILED>(x, dy, dt, part, cnt, a, smem); break;
-    case 1: dt_wave<Tag, WIN, 1, TILED>(x, dy, dt, part, cnt, a, smem); break;
-    case 2: dt_wave<Tag, WIN, 2, TILED>(x, dy, dt, part, cnt, a, smem); break;
-    default: dt_wave<Tag, WIN, 3, TILED>(x, dy, dt, part, cnt, a, smem); break;
+    case 0: dt_wave<Tag, WIN, 0, TILED>(x, dy, dt, part, a, smem); break;
+    case 1: dt_wave<Tag, WIN, 1, TILED>(x, dy, dt, part, a, smem); break;
+    case 2: dt_wave<Tag, WIN, 2, TILED>(x, dy, dt, part, a, smem); break;
+    default: dt_wave<Tag, WIN, 3, TILED>(x, dy, dt, part, a, smem); break;
   }
 }
 
@@ -2046,8 +1951,8 @@ __device__ __attribute__((always_inline)) void bwd_wave(const typename Tag::S *_
                                                         const typename Tag::S *__restrict__ dy,
                                                         const typename Tag::S *__restrict__ tab,
                                                         typename Tag::S *__restrict__ dx, float *__restrict__ dt,
-                                                        float *__restrict__ part, unsigned *__restrict__ cnt,
-                                                        const KArgs &a, unsigned char *smem) {
+                                                        float *__restrict__ part, const KArgs &a,
+                                                        unsigned char *smem) {
   typedef typename Tag::S S;
   typedef BwdCfg<Tag, WIN> G;
   typedef PSpan<G::NPT, WAVE> SP;
@@ -2096,7 +2001,7 @@ __device__ __attribute__((always_inline)) void bwd_wave(const typename Tag::S *_
     __syncthreads();
     dx_store<Tag, WIN, TILED>(a, dx, c, m0, s1, tid, Xt);
   }
-  dt_finish<Tag, WIN, G, WAVE>(acc, smem, dt, part, cnt, a, c, slab);
+  dt_finish<Tag, WIN, G, WAVE>(acc, smem, dt, part, a, c, slab);
 }
 
 template <class Tag, int WIN, bool TILED>
@@ -2105,13 +2010,13 @@ __global__ __launch_bounds__(kThreads, (TILED ? 3 : 2)) void wbmm_bwd_kernel(con
                                                                const typename Tag::S *__restrict__ tab,
                                                                typename Tag::S *__restrict__ dx,
                                                                float *__restrict__ dt, float *__restrict__ part,
-                                                               unsigned *__restrict__ cnt, KArgs a) {
+                                                               KArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   switch (threadIdx.x >> 6) {
-    case 0: bwd_wave<Tag, WIN, 0, TILED>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
-    case 1: bwd_wave<Tag, WIN, 1, TILED>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
-    case 2: bwd_wave<Tag, WIN, 2, TILED>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
-    default: bwd_wave<Tag, WIN, 3, TILED>(x, dy, tab, dx, dt, part, cnt, a, smem); break;
+    case 0: bwd_wave<Tag, WIN, 0, TILED>(x, dy, tab, dx, dt, part, a, smem); break;
+    case 1: bwd_wave<Tag, WIN, 1, TILED>(x, dy, tab, dx, dt, part, a, smem); break;
+    case 2: bwd_wave<Tag, WIN, 2, TILED>(x, dy, tab, dx, dt, part, a, smem); break;
+    default: bwd_wave<Tag, WIN, 3, TILED>(x, dy, tab, dx, dt, part, a, smem); break;
   }
 }
 
@@ -2263,8 +2168,8 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
                                                            const typename Tag::S *__restrict__ tab,
                                                            const typename Tag::S *__restrict__ tabl,
                                                            typename Tag::S *__restrict__ dx, float *__restrict__ dt,
-                                                           float *__restrict__ part, unsigned *__restrict__ cnt,
-                                                           const KArgs &a, unsigned char *smem,
+                                                           float *__restrict__ part, const KArgs &a,
+                                                           unsigned char *smem,
                                                            float *__restrict__ dtl, float *__restrict__ partl) {
   typedef typename Tag::S S;
   typedef StreamCfg<Tag, WIN> SC;
@@ -2376,13 +2281,13 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
     __syncthreads();
     dt_bin_sum_local<G, HL, kStreamThreads>(scr, binl, tid);
     __syncthreads();
-    dt_reduce_hier<G, HL, kStreamThreads>(smem, bing, binl, dt, dtl, part, partl, cnt, a, c, slab);
+    dt_reduce_hier<G, HL, kStreamThreads>(bing, binl, dt, dtl, part, partl, a, c, slab);
   } else {
     if constexpr (DTW >= 0) dt_bin_write<Tag, WIN, G, DTW>(acc, scr + DTW * NPM * kBinTile);
     __syncthreads();
     dt_bin_sum_all<Tag, WIN, G, kStreamThreads>(scr, bing, tid);
     __syncthreads();
-    dt_reduce<Tag, WIN, G, kStreamThreads>(smem, dt, part, cnt, a, c, slab);
+    dt_reduce<Tag, WIN, G, kStreamThreads>(smem, dt, part, a, c, slab);
   }
 }
 
@@ -2393,14 +2298,14 @@ template <class Tag, int WIN, bool DX, int HL = 0>
 __global__ __launch_bounds__(kStreamThreads, 3) void wbmm_bwd_stream_kernel(
     const typename Tag::S *__restrict__ x, const typename Tag::S *__restrict__ dy,
     const typename Tag::S *__restrict__ tab, typename Tag::S *__restrict__ dx, float *__restrict__ dt,
-    float *__restrict__ part, unsigned *__restrict__ cnt, KArgs a, float *__restrict__ dtl,
+    float *__restrict__ part, KArgs a, float *__restrict__ dtl,
     float *__restrict__ partl, const typename Tag::S *__restrict__ tabl) {
   static_assert(HL == 0 || 2 * HL == WIN, "hierarchical form: WIN = 2 HL");
   static_assert(HL == 0 || bins_lds_bytes<BwdCfg<Tag, WIN>>() + (size_t)(2 * HL - 1) * (2 * HL - 1) * 4 <=
                                (size_t)StreamCfg<Tag, WIN>::O_OFF,
                 "both tables' bins within the stage buffers");
   extern __shared__ __align__(16) unsigned char smem[];
-#define WBMM_SW(D, X) stream_wave<Tag, WIN, D, X, DX, HL>(x, dy, tab, tabl, dx, dt, part, cnt, a, smem, dtl, partl)
+#define WBMM_SW(D, X) stream_wave<Tag, WIN, D, X, DX, HL>(x, dy, tab, tabl, dx, dt, part, a, smem, dtl, partl)
   switch (threadIdx.x >> 6) {
     case 0: WBMM_SW(0, -1); break;
     case 1: WBMM_SW(1, -1); break;
@@ -2617,9 +2522,6 @@ static DtPlan plan_dt(const Geom &g) {
   return p;
 }
 
-// Workspace of the table gradient: per-channel counters (zero between calls)
-// followed by the per-slab partial sums.
-static size_t counter_bytes(int64_t C) { return (size_t)((C * 4 + 255) / 256 * 256); }
 
 // Launch plan of the channel-stream kernel (fixed-offset rows, no more
 // channels than compute units): one workgroup per (channel, slab), at most
@@ -2639,6 +2541,18 @@ static bool stream_plan(const Geom &g, KArgs &b) {
   return true;
 }
 
+template <int WIN>
+constexpr int64_t table_len() { return (int64_t)(2 * WIN - 1) * (2 * WIN - 1); }
+
+// After a launch: its error, else (several slabs per channel) the launch of
+// the kernel that sums the slab partials into the table gradient(s).
+static hipError_t sum_slabs(const float *part, float *dt, int64_t n, const float *part2, float *dt2, int64_t n2,
+                            int64_t slabs, hipStream_t st) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || slabs <= 1) return e;
+  return launch_dt_sum(part, dt, n, part2, dt2, n2, (int)slabs, st);
+}
+
 template <class Tag, int WIN>
 static hipError_t run_dtable(const void *x, const void *dy, float *dt, void *ws, const Geom &g,
                              hipStream_t st) {
@@ -2652,27 +2566,25 @@ static hipError_t run_dtable(const void *x, const void *dy, float *dt, void *ws,
     KArgs b = a;
     if (stream_plan<Tag, WIN>(g, b)) {
       // the same stages, bins and sums as the fused pass
-      unsigned *scnt = b.tiles_per_ch > 1 ? (unsigned *)ws : nullptr;
-      float *spart = b.tiles_per_ch > 1 ? (float *)((char *)ws + counter_bytes(g.C)) : nullptr;
+      float *spart = b.tiles_per_ch > 1 ? (float *)ws : nullptr;
       constexpr size_t slds = stream_lds_bytes<Tag, WIN>();
       wbmm_bwd_stream_kernel<Tag, WIN, false><<<dim3((unsigned)(g.C * b.tiles_per_ch)), dim3(kStreamThreads), slds, st>>>(
-          (const S *)x, (const S *)dy, nullptr, nullptr, dt, spart, scnt, b, nullptr, nullptr, nullptr);
-      return hipGetLastError();
+          (const S *)x, (const S *)dy, nullptr, nullptr, dt, spart, b, nullptr, nullptr, nullptr);
+      return sum_slabs(spart, dt, g.C * table_len<WIN>(), nullptr, nullptr, 0, b.tiles_per_ch, st);
     }
   }
-  unsigned *cnt = p.slabs > 1 ? (unsigned *)ws : nullptr;
-  float *part = p.slabs > 1 ? (float *)((char *)ws + counter_bytes(g.C)) : nullptr;
+  float *part = p.slabs > 1 ? (float *)ws : nullptr;
   constexpr size_t lds = dt_lds_bytes<Tag, WIN>();
   static_assert(lds <= 65536, "workgroup LDS above 64 KB");
   const dim3 grid((unsigned)(g.C * p.slabs));
   if constexpr (Tag::ES == 4 || WIN % 2 == 0) {
     if (a.tiled) {
-      wbmm_dt_kernel<Tag, WIN, true><<<grid, dim3(kThreads), lds, st>>>((const S *)x, (const S *)dy, dt, part, cnt, a);
-      return hipGetLastError();
+      wbmm_dt_kernel<Tag, WIN, true><<<grid, dim3(kThreads), lds, st>>>((const S *)x, (const S *)dy, dt, part, a);
+      return sum_slabs(part, dt, g.C * table_len<WIN>(), nullptr, nullptr, 0, p.slabs, st);
     }
   }
-  wbmm_dt_kernel<Tag, WIN, false><<<grid, dim3(kThreads), lds, st>>>((const S *)x, (const S *)dy, dt, part, cnt, a);
-  return hipGetLastError();
+  wbmm_dt_kernel<Tag, WIN, false><<<grid, dim3(kThreads), lds, st>>>((const S *)x, (const S *)dy, dt, part, a);
+  return sum_slabs(part, dt, g.C * table_len<WIN>(), nullptr, nullptr, 0, p.slabs, st);
 }
 
 template <class Tag, int WIN>
@@ -2687,30 +2599,28 @@ static hipError_t run_backward(const void *x, const void *dy, const void *t, voi
   if constexpr (Tag::ES == 4 || WIN % 2 == 0) {
     KArgs b = a;
     if (stream_plan<Tag, WIN>(g, b)) {
-      unsigned *scnt = b.tiles_per_ch > 1 ? (unsigned *)ws : nullptr;
-      float *spart = b.tiles_per_ch > 1 ? (float *)((char *)ws + counter_bytes(g.C)) : nullptr;
+      float *spart = b.tiles_per_ch > 1 ? (float *)ws : nullptr;
       constexpr size_t slds = stream_lds_bytes<Tag, WIN>();
       static_assert(slds <= 160 * 1024, "workgroup LDS above the 160 KB of a compute unit");
       wbmm_bwd_stream_kernel<Tag, WIN, true><<<dim3((unsigned)(g.C * b.tiles_per_ch)), dim3(kStreamThreads), slds, st>>>(
-          (const S *)x, (const S *)dy, (const S *)t, (S *)dx, dt, spart, scnt, b, nullptr, nullptr, nullptr);
-      return hipGetLastError();
+          (const S *)x, (const S *)dy, (const S *)t, (S *)dx, dt, spart, b, nullptr, nullptr, nullptr);
+      return sum_slabs(spart, dt, g.C * table_len<WIN>(), nullptr, nullptr, 0, b.tiles_per_ch, st);
     }
   }
-  unsigned *cnt = p.slabs > 1 ? (unsigned *)ws : nullptr;
-  float *part = p.slabs > 1 ? (float *)((char *)ws + counter_bytes(g.C)) : nullptr;
+  float *part = p.slabs > 1 ? (float *)ws : nullptr;
   constexpr size_t lds = bwd_lds_bytes<Tag, WIN>();
   static_assert(lds <= 65536, "workgroup LDS above 64 KB");
   const dim3 grid((unsigned)(g.C * p.slabs));
   if constexpr (Tag::ES == 4 || WIN % 2 == 0) {
     if (a.tiled) {
       wbmm_bwd_kernel<Tag, WIN, true><<<grid, dim3(kThreads), lds, st>>>((const S *)x, (const S *)dy, (const S *)t,
-                                                                         (S *)dx, dt, part, cnt, a);
-      return hipGetLastError();
+                                                                         (S *)dx, dt, part, a);
+      return sum_slabs(part, dt, g.C * table_len<WIN>(), nullptr, nullptr, 0, p.slabs, st);
     }
   }
   wbmm_bwd_kernel<Tag, WIN, false><<<grid, dim3(kThreads), lds, st>>>((const S *)x, (const S *)dy, (const S *)t,
-                                                                      (S *)dx, dt, part, cnt, a);
-  return hipGetLastError();
+                                                                      (S *)dx, dt, part, a);
+  return sum_slabs(part, dt, g.C * table_len<WIN>(), nullptr, nullptr, 0, p.slabs, st);
 }
 
 // Hierarchical form (global window WIN = 2 wl): one channel-stream pass when
@@ -2734,13 +2644,11 @@ static hipError_t run_hier_stream(const void *x, const void *dy, const void *tg,
     else set_tiled<WIN, Tag::ES>(g, a, {x, dy});
     KArgs b = a;
     if (!stream_plan<Tag, WIN>(g, b)) return hipSuccess;
-    unsigned *cnt = nullptr;
     float *partg = nullptr, *partl = nullptr;
     if (b.tiles_per_ch > 1) {
-      const size_t need = counter_bytes(g.C) + (size_t)b.tiles_per_ch * (size_t)g.C * (size_t)(K2 + K2L) * 4;
+      const size_t need = (size_t)b.tiles_per_ch * (size_t)g.C * (size_t)(K2 + K2L) * 4;
       if (ws == nullptr || need > ws_bytes) return hipSuccess;
-      cnt = (unsigned *)ws;
-      partg = (float *)((char *)ws + counter_bytes(g.C));
+      partg = (float *)ws;
       partl = partg + (size_t)b.tiles_per_ch * (size_t)g.C * (size_t)K2;
     }
     const dim3 grid((unsigned)(g.C * b.tiles_per_ch));
@@ -2748,14 +2656,14 @@ static hipError_t run_hier_stream(const void *x, const void *dy, const void *tg,
       constexpr size_t slds = stream_lds_bytes<Tag, WIN, true>();
       static_assert(slds <= 160 * 1024, "workgroup LDS above the 160 KB of a compute unit");
       wbmm_bwd_stream_kernel<Tag, WIN, true, WL><<<grid, dim3(kStreamThreads), slds, st>>>(
-          (const S *)x, (const S *)dy, (const S *)tg, (S *)dx, dtg, partg, cnt, b, dtl, partl, (const S *)tl);
+          (const S *)x, (const S *)dy, (const S *)tg, (S *)dx, dtg, partg, b, dtl, partl, (const S *)tl);
     } else {
       constexpr size_t slds = stream_lds_bytes<Tag, WIN>();
       wbmm_bwd_stream_kernel<Tag, WIN, false, WL><<<grid, dim3(kStreamThreads), slds, st>>>(
-          (const S *)x, (const S *)dy, nullptr, nullptr, dtg, partg, cnt, b, dtl, partl, nullptr);
+          (const S *)x, (const S *)dy, nullptr, nullptr, dtg, partg, b, dtl, partl, nullptr);
     }
     *done = true;
-    return hipGetLastError();
+    return sum_slabs(partg, dtg, g.C * K2, partl, dtl, g.C * K2L, b.tiles_per_ch, st);
   } else {
     (void)x; (void)dy; (void)tg; (void)tl; (void)dx; (void)dtg; (void)dtl; (void)ws; (void)ws_bytes; (void)g;
     (void)st;

@@ -103,8 +103,7 @@ def test_workspace_query(lib):
     assert lib.wbmm_backward_table_workspace_bytes(0, 1, 1, 1, 7, 1) == 0
     assert lib.wbmm_backward_table_workspace_bytes(1, 8, 28, 28, 7, 0) == 0  # one slab
     n = lib.wbmm_backward_table_workspace_bytes(64, 192, 28, 28, 14, 1)
-    counters = (192 * 4 + 255) // 256 * 256  # one 32-bit counter per channel
-    assert n > counters and (n - counters) % (192 * 729 * 4) == 0
+    assert n > 0 and n % (192 * 729 * 4) == 0  # [slabs, C, (2w-1)^2] float32 partial sums
 
 
 def test_backward_rejects_bad_arguments(lib):
