@@ -62,7 +62,9 @@ typedef enum {
   WBMM_ERR_INVALID_ARG = 1, /* null pointer, non-positive size, overlap,
                                misalignment, too-small workspace, overflow */
   WBMM_ERR_UNSUPPORTED = 2, /* window size or dtype without a kernel       */
-  WBMM_ERR_HIP = 3          /* the HIP runtime refused the launch          */
+  WBMM_ERR_HIP = 3,         /* the HIP runtime refused the launch          */
+  WBMM_ERR_SCRATCH = 4      /* wbmm_backward_noalloc: the shape needs more
+                               scratch than the library's static buffer   */
 } wbmm_status;
 
 /* Forward pass, Alg. 1: y = WBMM(x; table, w).
@@ -134,6 +136,33 @@ wbmm_status wbmm_backward(const void *x, const void *dy, const void *table,
                           size_t workspace_bytes, int64_t B, int64_t C,
                           int64_t H, int64_t W, int w, wbmm_dtype dtype,
                           void *stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the fused
+ * backward of wbmm_backward (the same kernels, the same results bit for bit)
+ * with its table-gradient scratch -- the per-slab partial sums that
+ * wbmm_backward keeps in the caller's workspace -- held in a static device
+ * buffer of this library instead.  No workspace argument;
+ * x, dy, table, dx, dtable and every other argument as for wbmm_backward.
+ *
+ * - The buffer holds WBMM_NOALLOC_SCRATCH_BYTES (4 MiB) per device; each
+ *   device the library runs on keeps its own copy until the process ends.
+ *   A shape whose scratch would exceed it (wbmm_backward_workspace_bytes()
+ *   greater than that) is rejected with WBMM_ERR_SCRATCH before any GPU
+ *   work is enqueued.
+ * - The call allocates nothing: no hipMalloc, no hipFree, no allocating
+ *   library routine.  The first call on a device looks up the buffer's device
+ *   address (hipGetSymbolAddress, with that device current) and keeps it.
+ * - A call writes the partial sums before it reads them, so nothing carries
+ *   over between calls and the buffer is never cleared.
+ * - All calls on one device share that device's buffer: calls that overlap
+ *   in time on one GPU (on different streams, or from different threads
+ *   without ordering) race and give wrong results.  Serialise them. */
+#define WBMM_NOALLOC_SCRATCH_BYTES ((size_t)4 << 20)
+wbmm_status wbmm_backward_noalloc(const void *x, const void *dy,
+                                  const void *table, void *dx, float *dtable,
+                                  int64_t B, int64_t C, int64_t H, int64_t W,
+                                  int w, wbmm_dtype dtype, void *stream);
 
 /* ---- Hierarchical (global + local) form (Sec. "Hierarchical Window
  * Reparameterization" and the appendix algorithms of its training and

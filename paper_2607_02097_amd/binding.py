@@ -28,12 +28,14 @@ WBMM_OK = 0
 WBMM_ERR_INVALID_ARG = 1
 WBMM_ERR_UNSUPPORTED = 2
 WBMM_ERR_HIP = 3
+WBMM_ERR_SCRATCH = 4
+NOALLOC_SCRATCH_BYTES = 4 << 20  # WBMM_NOALLOC_SCRATCH_BYTES of include/wbmm.h
 
 DTYPE_CODES = {torch.float32: 0, torch.bfloat16: 1, torch.float16: 2}
 
 EXPORTED = ("wbmm_forward", "wbmm_backward_input", "wbmm_backward_table",
             "wbmm_backward_table_workspace_bytes", "wbmm_backward",
-            "wbmm_backward_workspace_bytes", "wbmm_hier_forward",
+            "wbmm_backward_workspace_bytes", "wbmm_backward_noalloc", "wbmm_hier_forward",
             "wbmm_hier_backward_input", "wbmm_hier_backward",
             "wbmm_hier_backward_workspace_bytes", "wbmm_build_matrix",
             "wbmm_dense_forward", "wbmm_dense_backward_input",
@@ -72,6 +74,8 @@ def load_library(path: str = LIB_PATH):
     lib.wbmm_backward_workspace_bytes.restype = ctypes.c_size_t
     lib.wbmm_backward.argtypes = [vp, vp, vp, vp, vp, vp, ctypes.c_size_t] + shape
     lib.wbmm_backward.restype = st
+    lib.wbmm_backward_noalloc.argtypes = [vp, vp, vp, vp, vp] + shape
+    lib.wbmm_backward_noalloc.restype = st
     lib.wbmm_hier_forward.argtypes = [vp, vp, vp, vp] + shape
     lib.wbmm_hier_forward.restype = st
     lib.wbmm_hier_backward_input.argtypes = [vp, vp, vp, vp] + shape
@@ -278,6 +282,26 @@ def wbmm_backward(x: torch.Tensor, dy: torch.Tensor, table: torch.Tensor, w: int
                                           _stream(x, stream))
     if st != WBMM_OK:
         raise WbmmError(st, "wbmm_backward")
+    return dx, dtable
+
+
+def wbmm_backward_noalloc(x: torch.Tensor, dy: torch.Tensor, table: torch.Tensor, w: int, dx: torch.Tensor,
+                          dtable: torch.Tensor, stream=None):
+    """wbmm_backward without a workspace: the library's static scratch holds
+    the table gradient's partial sums (see include/wbmm.h).  The
+    caller passes the outputs; nothing is allocated."""
+    for t, n in ((x, "x"), (dy, "dy"), (table, "table"), (dx, "dx"), (dtable, "dtable")):
+        _check_tensor(t, n)
+    if dy.shape != x.shape or dy.dtype != x.dtype or dx.shape != x.shape or dx.dtype != x.dtype:
+        raise ValueError("dy and dx must match x's shape and dtype")
+    if table.dtype != x.dtype or dtable.dtype != torch.float32:
+        raise ValueError("table in x's dtype, dtable float32")
+    B, C, H, W = x.shape
+    with torch.cuda.device(x.device):
+        st = load_library().wbmm_backward_noalloc(_ptr(x), _ptr(dy), _ptr(table), _ptr(dx), _ptr(dtable),
+                                                  B, C, H, W, int(w), _code(x.dtype), _stream(x, stream))
+    if st != WBMM_OK:
+        raise WbmmError(st, "wbmm_backward_noalloc")
     return dx, dtable
 
 

@@ -37,7 +37,7 @@ HIP_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++20", "-fPIC",
 # parallel; the largest windows (slowest units) first.
 UNITS = [("wbmm_inst.hip", ["-DWBMM_INST_TAG=%s" % tag, "-DWBMM_INST_LO=%d" % lo])
          for lo in (13, 9, 5, 1) for tag in ("TagBF16", "TagF16", "TagF32")]
-UNITS += [("wbmm_dense.hip", []), ("wbmm_reduce.hip", []), ("wbmm_dispatch.cpp", []), ("wbmm_api.cpp", [])]
+UNITS += [("wbmm_dense.hip", []), ("wbmm_reduce.hip", []), ("wbmm_noalloc.hip", []), ("wbmm_dispatch.cpp", []), ("wbmm_api.cpp", [])]
 
 
 def hipcc() -> str:

@@ -376,6 +376,7 @@ const char *wbmm_status_string(wbmm_status s) {
     case WBMM_ERR_INVALID_ARG: return "WBMM_ERR_INVALID_ARG: invalid argument";
     case WBMM_ERR_UNSUPPORTED: return "WBMM_ERR_UNSUPPORTED: unsupported window size or dtype";
     case WBMM_ERR_HIP: return "WBMM_ERR_HIP: HIP runtime error";
+    case WBMM_ERR_SCRATCH: return "WBMM_ERR_SCRATCH: the shape needs more than the library's static scratch";
   }
   return "WBMM: unknown status";
 }

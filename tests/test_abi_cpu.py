@@ -34,7 +34,7 @@ def test_library_exports_every_declared_function(lib):
 
 
 def test_status_strings(lib):
-    for s in (0, 1, 2, 3):
+    for s in (0, 1, 2, 3, 4):
         assert W.wbmm_status_string(s).startswith("WBMM")
     assert "unknown" in W.wbmm_status_string(77)
     assert W.wbmm_version().count(".") == 2
@@ -216,3 +216,21 @@ def test_build_rejects_flat_memory_instructions():
     assert found == [("_ZN4wbmm6kernelILi2EEEvv", "flat_load_dwordx4"),
                      ("_ZN4wbmm6kernelILi2EEEvv", "flat_store_dword")]
     assert B.flat_accesses(listing.split("0000000000002000")[0]) == []
+
+
+def test_noalloc_validates_on_the_host(lib):
+    """wbmm_backward_noalloc rejects bad arguments, and shapes whose scratch
+    exceeds the static buffer, before any GPU work (no kernel launch here)."""
+    vp = ctypes.c_void_p
+    G = 1 << 32  # far-apart fake device addresses: the tensors do not overlap
+
+    def call(x=G, dy=2 * G, t=3 * G, dx=4 * G, dt=5 * G, B=33, C=700, H=16, Wd=16, w=16, d=1):
+        return lib.wbmm_backward_noalloc(vp(x), vp(dy), vp(t), vp(dx), vp(dt), B, C, H, Wd, w, d, None)
+
+    need = lib.wbmm_backward_workspace_bytes(33, 700, 16, 16, 16, 1)
+    assert need > W.NOALLOC_SCRATCH_BYTES
+    assert call() == W.WBMM_ERR_SCRATCH
+    assert call(x=0) == W.WBMM_ERR_INVALID_ARG
+    assert call(dx=G) == W.WBMM_ERR_INVALID_ARG  # dx aliases x
+    assert call(w=17) == W.WBMM_ERR_UNSUPPORTED
+    assert "scratch" in W.wbmm_status_string(W.WBMM_ERR_SCRATCH)
