@@ -2021,19 +2021,23 @@ __global__ __launch_bounds__(kThreads, (TILED ? 3 : 2)) void wbmm_bwd_kernel(con
 }
 
 // ------------------------------------------ fused backward, channel stream
-// Fixed-offset rows, few channels per compute unit: one 12-wave workgroup
-// per (channel, slab) and at most one workgroup per compute unit, streaming
-// the slab's stages through double-buffered LDS (x and dy tiles, and the
+// Fixed-offset rows, few channels per compute unit: one workgroup per
+// (channel, slab) and at most one workgroup per compute unit, streaming the
+// slab's stages through double-buffered LDS (x and dy tiles, and the
 // input-gradient results) with one workgroup barrier per stage.  Waves 0-3
 // take the table-gradient products (the P ranges of the 4-wave kernel),
 // waves 4-11 the input-gradient products (four waves per 16-window
-// sub-tile); at any time every wave copies the next stage into LDS, the
-// stage after it into registers and the previous stage's dX rows to HBM.
-// Products, bins and sums are those of wbmm_bwd_kernel, so the results are
-// bitwise the same.
-constexpr int kStreamWaves = 12;
-constexpr int kStreamThreads = 64 * kStreamWaves;
-constexpr int kStreamDt = 4;  // table-gradient waves
+// sub-tile).  The copies -- the next stage into LDS, the stage after it into
+// registers, the previous stage's dX rows to HBM -- are made either by NCW
+// dedicated copy waves (waves 12 .. 11 + NCW) while the twelve compute waves
+// multiply, or, with NCW = 0, by the compute waves themselves after their
+// products.  Products, bins and sums are those of wbmm_bwd_kernel, so the
+// results are bitwise the same.
+constexpr int kStreamCompute = 12;  // compute waves
+constexpr int kStreamDt = 4;        // of which table-gradient waves
+
+template <int NCW>
+__host__ __device__ constexpr int stream_threads() { return 64 * (kStreamCompute + NCW); }
 
 template <class Tag, int WIN>
 struct StreamCfg {
@@ -2041,9 +2045,7 @@ struct StreamCfg {
   typedef FwdCfg<Tag, WIN> F;
   static constexpr int SUBS = G::SUBS;                     // 16-window sub-tiles per stage
   static constexpr int NCP = 2 * SUBS;                     // row copies: (tensor, sub-tile)
-  static constexpr int WPC = kStreamWaves / NCP;           // waves per copy
   static constexpr int RC = 16 * G::KR;                    // rows per copy
-  static constexpr int IT = cdiv(RC, WPC * 64);            // rows per thread and copy
   static constexpr int STAGE = 2 * G::BUF;                 // x tile + dy tile
   static constexpr int O_OFF = 2 * STAGE;                  // two dX result buffers of G::BUF
   static constexpr int TS_OFF = O_OFF + 2 * G::BUF;
@@ -2053,8 +2055,17 @@ struct StreamCfg {
   static constexpr int TSL_OFF = rup(END, 16);
   static constexpr int TBL_OFF = TSL_OFF + rup(F::TSL_LEN * Tag::ES, 16);
   static constexpr int END_H = TBL_OFF + F::TBL_LEN * Tag::ES;
-  static_assert(kStreamWaves % NCP == 0, "whole waves per copy");
   static_assert(bins_lds_bytes<G>() <= O_OFF, "bins must not reach the dX buffers");
+};
+
+// How NC copying waves split a stage's row copies: WPC waves per (tensor,
+// sub-tile) copy, IT rows per thread of it.
+template <class Tag, int WIN, int NC>
+struct StreamCopy {
+  typedef StreamCfg<Tag, WIN> SC;
+  static constexpr int WPC = NC / SC::NCP;
+  static constexpr int IT = cdiv(SC::RC, WPC * 64);
+  static_assert(NC % SC::NCP == 0, "whole waves per copy");
 };
 
 template <class Tag, int WIN, bool HIER = false>
@@ -2062,27 +2073,29 @@ __host__ __device__ constexpr size_t stream_lds_bytes() {
   return (size_t)(HIER ? StreamCfg<Tag, WIN>::END_H : StreamCfg<Tag, WIN>::END);
 }
 
-template <class Tag, int WIN>
+template <class Tag, int WIN, int NC>
 struct StreamRows {
-  RowData<WIN, Tag::ES> rd[StreamCfg<Tag, WIN>::IT];
+  RowData<WIN, Tag::ES> rd[StreamCopy<Tag, WIN, NC>::IT];
 };
 
-// Rows of this wave's copy (tensor, sub-tile) of the stage at m0 -> registers.
-template <class Tag, int WIN>
+// Rows of copying wave cw's copy (tensor, sub-tile) of the stage at m0 ->
+// registers (NC copying waves).
+template <class Tag, int WIN, int NC>
 __device__ __attribute__((always_inline)) inline void stream_load(const KArgs &a, const typename Tag::S *x,
                                                                    const typename Tag::S *dy, int64_t c, int64_t m0,
-                                                                   int64_t m1, int wave, int lane,
-                                                                   StreamRows<Tag, WIN> &st) {
+                                                                   int64_t m1, int cw, int lane,
+                                                                   StreamRows<Tag, WIN, NC> &st) {
   typedef StreamCfg<Tag, WIN> SC;
+  typedef StreamCopy<Tag, WIN, NC> CP;
   typedef BwdCfg<Tag, WIN> G;
   constexpr int NDV = (WIN * Tag::ES) / 4;
-  const int cp = wave / SC::WPC;
+  const int cp = cw / CP::WPC;
   const int tens = cp / SC::SUBS, sub = cp % SC::SUBS;
   const int64_t ms = m0 + 16 * sub;
   const char *base = reinterpret_cast<const char *>((tens ? dy : x) + tiled_sub_base(a, c, ms));
 #pragma unroll
-  for (int k = 0; k < SC::IT; ++k) {
-    const int t = (wave % SC::WPC) * 64 + lane + k * SC::WPC * 64;
+  for (int k = 0; k < CP::IT; ++k) {
+    const int t = (cw % CP::WPC) * 64 + lane + k * CP::WPC * 64;
     const int vv = t / G::KR;
     const int hi = t - vv * G::KR;
 #pragma unroll
@@ -2101,17 +2114,18 @@ __device__ __attribute__((always_inline)) inline void stream_load(const KArgs &a
 }
 
 // The loaded rows -> window-major padded rows of one stage buffer.
-template <class Tag, int WIN>
-__device__ __attribute__((always_inline)) inline void stream_write(unsigned char *stage, int wave, int lane,
-                                                                    const StreamRows<Tag, WIN> &st) {
+template <class Tag, int WIN, int NC>
+__device__ __attribute__((always_inline)) inline void stream_write(unsigned char *stage, int cw, int lane,
+                                                                    const StreamRows<Tag, WIN, NC> &st) {
   typedef StreamCfg<Tag, WIN> SC;
+  typedef StreamCopy<Tag, WIN, NC> CP;
   typedef BwdCfg<Tag, WIN> G;
   typedef RowData<WIN, Tag::ES> RD;
-  const int cp = wave / SC::WPC;
+  const int cp = cw / CP::WPC;
   const int tens = cp / SC::SUBS, sub = cp % SC::SUBS;
 #pragma unroll
-  for (int k = 0; k < SC::IT; ++k) {
-    const int t = (wave % SC::WPC) * 64 + lane + k * SC::WPC * 64;
+  for (int k = 0; k < CP::IT; ++k) {
+    const int t = (cw % CP::WPC) * 64 + lane + k * CP::WPC * 64;
     const int vv = t / G::KR;
     const int hi = t - vv * G::KR;
     if (t < SC::RC) {
@@ -2123,16 +2137,17 @@ __device__ __attribute__((always_inline)) inline void stream_write(unsigned char
   }
 }
 
-// The dX rows of the stage at m0 (window-major in Obuf) -> dx.
-template <class Tag, int WIN>
+// The dX rows of the stage at m0 (window-major in Obuf) -> dx, by NCT
+// copying threads (ct = this thread's index among them).
+template <class Tag, int WIN, int NCT>
 __device__ __attribute__((always_inline)) inline void stream_store(const KArgs &a, typename Tag::S *dx, int64_t c,
-                                                                    int64_t m0, int64_t m1, int tid,
+                                                                    int64_t m0, int64_t m1, int ct,
                                                                     const unsigned char *Obuf) {
   typedef BwdCfg<Tag, WIN> G;
   constexpr int NDV = (WIN * Tag::ES) / 4, RS = 16 * WIN;  // rows per sub-tile
 #pragma unroll
-  for (int k = 0; k < cdiv(G::SUBS * RS, kStreamThreads); ++k) {
-    const int q = tid + k * kStreamThreads;
+  for (int k = 0; k < cdiv(G::SUBS * RS, NCT); ++k) {
+    const int q = ct + k * NCT;
     const int sub = q / RS;
     const int r = q - sub * RS;
     const int vv = r / WIN;
@@ -2161,8 +2176,9 @@ __device__ __attribute__((always_inline)) inline void stream_store(const KArgs &
 // One wave of the stream kernel: DTW >= 0 is a table-gradient wave (its P
 // range), else DXW >= 0 an input-gradient wave (idle but for the copies
 // when DX is false: the table gradient alone, with the same stages, bins and
-// sums as the fused pass).
-template <class Tag, int WIN, int DTW, int DXW, bool DX, int HL>
+// sums as the fused pass), else a copy wave.  With NCW = 0 every wave copies
+// (after its products); otherwise only the NCW copy waves do.
+template <class Tag, int WIN, int DTW, int DXW, bool DX, int HL, int NCW>
 __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S *__restrict__ x,
                                                            const typename Tag::S *__restrict__ dy,
                                                            const typename Tag::S *__restrict__ tab,
@@ -2176,9 +2192,13 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
   typedef BwdCfg<Tag, WIN> G;
   typedef PSpan<G::NPT, (DTW >= 0 ? DTW : 0)> SP;
   constexpr int RP = G::RP, K1 = G::K1, K2 = G::K2, CW = G::CW;
+  constexpr int NTH = stream_threads<NCW>();
+  constexpr int NC = NCW > 0 ? NCW : kStreamCompute;    // copying waves
+  constexpr bool COPY = NCW == 0 || (DTW < 0 && DXW < 0);  // this wave copies
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
+  const int cw = NCW > 0 ? wave - kStreamCompute : wave;  // index among the copying waves
   const int64_t c = blockIdx.x / a.tiles_per_ch;
   const int64_t slab = blockIdx.x - c * a.tiles_per_ch;
   const int64_t s0 = slab * a.tile;
@@ -2197,30 +2217,32 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
   // of the bulk loads); the table row and (16-bit) its Toeplitz blocks ->
   // LDS; stage 0 -> LDS buffer 0, stage 1 in flight
   constexpr bool HX = DX && HL > 0;  // hierarchical input gradient: both tables
-  TabRegs<Tag, WIN, HX, kStreamThreads> tr;
-  if constexpr (DX) tab_load<Tag, WIN, true, HX, kStreamThreads>(tab, tabl, c, tid, tr);
-  StreamRows<Tag, WIN> st;
-  stream_load<Tag, WIN>(a, x, dy, c, s0, s1, wave, lane, st);
+  TabRegs<Tag, WIN, HX, NTH> tr;
+  if constexpr (DX) tab_load<Tag, WIN, true, HX, NTH>(tab, tabl, c, tid, tr);
+  StreamRows<Tag, WIN, NC> st;
+  if constexpr (COPY) stream_load<Tag, WIN, NC>(a, x, dy, c, s0, s1, cw, lane, st);
   if constexpr (HX) {
-    fwd_tables<Tag, WIN, true, true, kStreamThreads>(tr, Ts, TB, Tsl, TBL, tid);
+    fwd_tables<Tag, WIN, true, true, NTH>(tr, Ts, TB, Tsl, TBL, tid);
   } else if constexpr (DX) {
 #pragma unroll
     for (int i = 0; i < tr.N; ++i)
-      if (tid + i * kStreamThreads < K2) Ts[tid + i * kStreamThreads] = tr.v[i];
+      if (tid + i * NTH < K2) Ts[tid + i * NTH] = tr.v[i];
     __syncthreads();
     if constexpr (Tag::W16) {
-      build_tb<Tag, WIN, kStreamThreads>(Ts, TB, tid);
+      build_tb<Tag, WIN, NTH>(Ts, TB, tid);
     }
   }
-  stream_write<Tag, WIN>(smem, wave, lane, st);
-  if (nst > 1) stream_load<Tag, WIN>(a, x, dy, c, s0 + CW, s1, wave, lane, st);
+  if constexpr (COPY) {
+    stream_write<Tag, WIN, NC>(smem, cw, lane, st);
+    if (nst > 1) stream_load<Tag, WIN, NC>(a, x, dy, c, s0 + CW, s1, cw, lane, st);
+  }
   __syncthreads();
 
   // the input-gradient waves' 16-bit B fragments, read once: the table is
   // the same for every stage
   constexpr int DXI = DXW >= 0 ? DXW : 0;
   constexpr bool PRE = DX && DXW >= 0 && Tag::W16;
-  typedef DxSplit<Tag, WIN, DXI, kStreamWaves - kStreamDt> DS;
+  typedef DxSplit<Tag, WIN, DXI, kStreamCompute - kStreamDt> DS;
   typename Tag::Frag bfw[DS::NQ];
   if constexpr (PRE) {
     const int g = lane >> 4, ln = lane & 15;
@@ -2235,24 +2257,28 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
     // this stage's products
     if constexpr (DTW >= 0) {
       dt_products_split<Tag, G, DTW, HL>(cur, cur + G::BUF, acc, accl, lane);
-    } else if constexpr (DX) {
-      dx_products<Tag, WIN, DXW, kStreamWaves - kStreamDt, (HX ? HL : 0), PRE>(cur + G::BUF, obuf, Ts, TB, lane, Tsl,
-                                                                                TBL, &bfw);
+    } else if constexpr (DX && DXW >= 0) {
+      dx_products<Tag, WIN, DXW, kStreamCompute - kStreamDt, (HX ? HL : 0), PRE>(cur + G::BUF, obuf, Ts, TB, lane,
+                                                                                  Tsl, TBL, &bfw);
     }
     // the next stage into the other buffer (free since the last barrier),
     // the one after it in flight, the previous stage's dX rows out
-    if (s + 1 < nst) stream_write<Tag, WIN>(smem + ((s + 1) & 1) * SC::STAGE, wave, lane, st);
-    if (s + 2 < nst) stream_load<Tag, WIN>(a, x, dy, c, m0 + 2 * CW, s1, wave, lane, st);
-    if (DX && s > 0) stream_store<Tag, WIN>(a, dx, c, m0 - CW, s1, tid, smem + SC::O_OFF + ((s - 1) & 1) * G::BUF);
+    if constexpr (COPY) {
+      if (s + 1 < nst) stream_write<Tag, WIN, NC>(smem + ((s + 1) & 1) * SC::STAGE, cw, lane, st);
+      if (s + 2 < nst) stream_load<Tag, WIN, NC>(a, x, dy, c, m0 + 2 * CW, s1, cw, lane, st);
+      if (DX && s > 0)
+        stream_store<Tag, WIN, NC * 64>(a, dx, c, m0 - CW, s1, cw * 64 + lane,
+                                        smem + SC::O_OFF + ((s - 1) & 1) * G::BUF);
+    }
     __syncthreads();
   }
   // the last stage's dX rows out while the table-gradient waves bin their
   // tiles (the bins lie below the dX buffers)
-  if constexpr (DX)
-    stream_store<Tag, WIN>(a, dx, c, s0 + (int64_t)(nst - 1) * CW, s1, tid,
-                           smem + SC::O_OFF + ((nst - 1) & 1) * G::BUF);
+  if constexpr (DX && COPY)
+    stream_store<Tag, WIN, NC * 64>(a, dx, c, s0 + (int64_t)(nst - 1) * CW, s1, cw * 64 + lane,
+                                    smem + SC::O_OFF + ((nst - 1) & 1) * G::BUF);
   // the table-gradient waves' tiles to the scratch, then the bins summed by
-  // all twelve waves
+  // all the waves
   constexpr int NPM = bin_tiles_per_wave<G>();
   float *scr = reinterpret_cast<float *>(smem);
   float *bing = scr + kWaves * NPM * kBinTile;
@@ -2275,27 +2301,28 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
       dt_bin_write<Tag, WIN, G, DTW>(tot, scr + DTW * NPM * kBinTile);
     }
     __syncthreads();
-    dt_bin_sum_all<Tag, WIN, G, kStreamThreads>(scr, bing, tid);
+    dt_bin_sum_all<Tag, WIN, G, NTH>(scr, bing, tid);
     __syncthreads();
     if constexpr (DTW >= 0) dt_bin_write<Tag, WIN, G, DTW>(accl, scr + DTW * NPM * kBinTile);
     __syncthreads();
-    dt_bin_sum_local<G, HL, kStreamThreads>(scr, binl, tid);
+    dt_bin_sum_local<G, HL, NTH>(scr, binl, tid);
     __syncthreads();
-    dt_reduce_hier<G, HL, kStreamThreads>(bing, binl, dt, dtl, part, partl, a, c, slab);
+    dt_reduce_hier<G, HL, NTH>(bing, binl, dt, dtl, part, partl, a, c, slab);
   } else {
     if constexpr (DTW >= 0) dt_bin_write<Tag, WIN, G, DTW>(acc, scr + DTW * NPM * kBinTile);
     __syncthreads();
-    dt_bin_sum_all<Tag, WIN, G, kStreamThreads>(scr, bing, tid);
+    dt_bin_sum_all<Tag, WIN, G, NTH>(scr, bing, tid);
     __syncthreads();
-    dt_reduce<Tag, WIN, G, kStreamThreads>(smem, dt, part, a, c, slab);
+    dt_reduce<Tag, WIN, G, NTH>(smem, dt, part, a, c, slab);
   }
 }
 
 // HL > 0: the hierarchical form (global window WIN, local window
 // HL = WIN / 2): both table gradients from one pass, and with DX the input
 // gradient of the fused matrix (tables tab and tabl, read back to front).
-template <class Tag, int WIN, bool DX, int HL = 0>
-__global__ __launch_bounds__(kStreamThreads, 3) void wbmm_bwd_stream_kernel(
+// NCW: dedicated copy waves (0 or 4).
+template <class Tag, int WIN, bool DX, int HL = 0, int NCW = 0>
+__global__ __launch_bounds__(stream_threads<NCW>(), (kStreamCompute + NCW) / 4) void wbmm_bwd_stream_kernel(
     const typename Tag::S *__restrict__ x, const typename Tag::S *__restrict__ dy,
     const typename Tag::S *__restrict__ tab, typename Tag::S *__restrict__ dx, float *__restrict__ dt,
     float *__restrict__ part, KArgs a, float *__restrict__ dtl,
@@ -2304,8 +2331,9 @@ __global__ __launch_bounds__(kStreamThreads, 3) void wbmm_bwd_stream_kernel(
   static_assert(HL == 0 || bins_lds_bytes<BwdCfg<Tag, WIN>>() + (size_t)(2 * HL - 1) * (2 * HL - 1) * 4 <=
                                (size_t)StreamCfg<Tag, WIN>::O_OFF,
                 "both tables' bins within the stage buffers");
+  static_assert(NCW == 0 || NCW == 4, "copy waves: none or one per SIMD");
   extern __shared__ __align__(16) unsigned char smem[];
-#define WBMM_SW(D, X) stream_wave<Tag, WIN, D, X, DX, HL>(x, dy, tab, tabl, dx, dt, part, a, smem, dtl, partl)
+#define WBMM_SW(D, X) stream_wave<Tag, WIN, D, X, DX, HL, NCW>(x, dy, tab, tabl, dx, dt, part, a, smem, dtl, partl)
   switch (threadIdx.x >> 6) {
     case 0: WBMM_SW(0, -1); break;
     case 1: WBMM_SW(1, -1); break;
@@ -2318,12 +2346,18 @@ __global__ __launch_bounds__(kStreamThreads, 3) void wbmm_bwd_stream_kernel(
     case 8: WBMM_SW(-1, 4); break;
     case 9: WBMM_SW(-1, 5); break;
     case 10: WBMM_SW(-1, 6); break;
-    default: WBMM_SW(-1, 7); break;
+    case 11: WBMM_SW(-1, 7); break;
+    default:
+      if constexpr (NCW > 0) WBMM_SW(-1, -1);
+      break;
   }
 #undef WBMM_SW
 }
 
 // ============================================================ host side
+
+// Dedicated copy waves of the (plain) channel-stream kernel.
+constexpr int kCopyWaves = 4;
 
 static int64_t cdiv64(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
@@ -2568,7 +2602,9 @@ static hipError_t run_dtable(const void *x, const void *dy, float *dt, void *ws,
       // the same stages, bins and sums as the fused pass
       float *spart = b.tiles_per_ch > 1 ? (float *)ws : nullptr;
       constexpr size_t slds = stream_lds_bytes<Tag, WIN>();
-      wbmm_bwd_stream_kernel<Tag, WIN, false><<<dim3((unsigned)(g.C * b.tiles_per_ch)), dim3(kStreamThreads), slds, st>>>(
+      // (no input-gradient products: the eight idle waves copy as well)
+      wbmm_bwd_stream_kernel<Tag, WIN, false, 0, 0><<<dim3((unsigned)(g.C * b.tiles_per_ch)),
+                                                      dim3(stream_threads<0>()), slds, st>>>(
           (const S *)x, (const S *)dy, nullptr, nullptr, dt, spart, b, nullptr, nullptr, nullptr);
       return sum_slabs(spart, dt, g.C * table_len<WIN>(), nullptr, nullptr, 0, b.tiles_per_ch, st);
     }
@@ -2602,7 +2638,8 @@ static hipError_t run_backward(const void *x, const void *dy, const void *t, voi
       float *spart = b.tiles_per_ch > 1 ? (float *)ws : nullptr;
       constexpr size_t slds = stream_lds_bytes<Tag, WIN>();
       static_assert(slds <= 160 * 1024, "workgroup LDS above the 160 KB of a compute unit");
-      wbmm_bwd_stream_kernel<Tag, WIN, true><<<dim3((unsigned)(g.C * b.tiles_per_ch)), dim3(kStreamThreads), slds, st>>>(
+      wbmm_bwd_stream_kernel<Tag, WIN, true, 0, kCopyWaves><<<dim3((unsigned)(g.C * b.tiles_per_ch)),
+                                                               dim3(stream_threads<kCopyWaves>()), slds, st>>>(
           (const S *)x, (const S *)dy, (const S *)t, (S *)dx, dt, spart, b, nullptr, nullptr, nullptr);
       return sum_slabs(spart, dt, g.C * table_len<WIN>(), nullptr, nullptr, 0, b.tiles_per_ch, st);
     }
@@ -2655,11 +2692,11 @@ static hipError_t run_hier_stream(const void *x, const void *dy, const void *tg,
     if (dx) {
       constexpr size_t slds = stream_lds_bytes<Tag, WIN, true>();
       static_assert(slds <= 160 * 1024, "workgroup LDS above the 160 KB of a compute unit");
-      wbmm_bwd_stream_kernel<Tag, WIN, true, WL><<<grid, dim3(kStreamThreads), slds, st>>>(
+      wbmm_bwd_stream_kernel<Tag, WIN, true, WL><<<grid, dim3(stream_threads<0>()), slds, st>>>(
           (const S *)x, (const S *)dy, (const S *)tg, (S *)dx, dtg, partg, b, dtl, partl, (const S *)tl);
     } else {
       constexpr size_t slds = stream_lds_bytes<Tag, WIN>();
-      wbmm_bwd_stream_kernel<Tag, WIN, false, WL><<<grid, dim3(kStreamThreads), slds, st>>>(
+      wbmm_bwd_stream_kernel<Tag, WIN, false, WL><<<grid, dim3(stream_threads<0>()), slds, st>>>(
           (const S *)x, (const S *)dy, nullptr, nullptr, dtg, partg, b, dtl, partl, nullptr);
     }
     *done = true;
