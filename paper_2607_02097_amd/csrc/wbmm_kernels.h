@@ -43,16 +43,17 @@
 // Table gradient: K = windows.  The 16x16 block pair (input tile pi, output
 // tile po) only matters through pi - po, so all pairs with equal pi - po
 // share one accumulator (27 16x16 fp32 tiles at w = 14), split across four
-// waves.  Diagonal sums of the tiles give dT.  Slabs of one channel are
-// summed in slab order by the channel's last workgroup, found with one
-// atomic ticket per workgroup; the result is bitwise reproducible.
+// waves.  Diagonal sums of the tiles give dT.  A channel split into slabs
+// writes one partial table per slab; a second kernel adds the partials in
+// slab order, so the result is bitwise reproducible.
 //
 // Fused backward: x and dy are read once for both gradients.  With
-// fixed-offset rows and no more channels than compute units, one 12-wave
+// fixed-offset rows and no more channels than compute units, one 16-wave
 // workgroup per channel (or slab) streams the channel's stages through LDS:
 // four waves accumulate the table gradient while eight compute the input
-// gradient of the same stage, the next stage is copied in and the previous
-// stage's dX rows go out, with one workgroup barrier per stage.  Otherwise a
+// gradient of the same stage, and four copy waves bring the next stage in
+// and send the previous stage's dX rows out, with one workgroup barrier per
+// stage.  Otherwise a
 // four-wave workgroup per (channel, slab) runs the same products in turn.
 // The hierarchical form (global window 2 wl plus local wl sub-windows) adds
 // local-block products to the forward and input gradient and splits the

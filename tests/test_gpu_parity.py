@@ -364,15 +364,11 @@ def test_more_channels_than_compute_units(shape, dtype):
     check({"fwd": to_f64(y)}, run_oracle(d, w, ("fwd",)), dtype, "channels>CUs %s %s" % (dtype, shape))
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
-@pytest.mark.parametrize("shape", MANY_CH, ids=lambda s: "B%dC%dH%dW%dw%d" % s)
-def test_more_channels_integer_data_bit_exact(shape, dtype):
-    """Integers in {-1, 0, 1} with more channels than compute units: every sum
-    is exact, so the forward, both gradients (separate and fused) equal the
-    oracle bit for bit."""
+def check_integer_exact(shape, dtype, seed):
+    """Integers in {-1, 0, 1}: every sum is exact, so the forward and both
+    gradients (separate and fused) equal the oracle bit for bit."""
     B, C, H, Wd, w = shape
-    assert C > compute_units()
-    r = np.random.default_rng(71 + w)
+    r = np.random.default_rng(seed)
     d = {}
     for k, shp in (("x", (B, C, H, Wd)), ("dy", (B, C, H, Wd)), ("t", (C, (2 * w - 1) ** 2))):
         d[k], d[k + "64"] = synth.round_to(r.integers(-1, 2, size=shp).astype(np.float64), dtype)
@@ -385,6 +381,36 @@ def test_more_channels_integer_data_bit_exact(shape, dtype):
     want["fused dx"], want["fused dt"] = want["dx"], want["dt"]
     for k in want:
         assert np.array_equal(got[k], want[k]), k
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("shape", MANY_CH, ids=lambda s: "B%dC%dH%dW%dw%d" % s)
+def test_more_channels_integer_data_bit_exact(shape, dtype):
+    assert shape[1] > compute_units()
+    check_integer_exact(shape, dtype, 71 + shape[4])
+
+
+# few stages per channel and fewer channels than compute units: the fused
+# gradients split each channel's windows into slabs of one or two stages
+# each, so most slabs are short and the last one is ragged
+SHORT_SLABS = [
+    (40, 60, 28, 28, 14),  # 16-bit: 5 stages per channel in slabs of 2, 2, 1; float32: 10 in 3, 3, 3, 1
+    (24, 90, 24, 24, 12),  # 16-bit: 3 stages per channel in slabs of 2, 1; float32: 6 in 3, 3
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("shape", SHORT_SLABS, ids=lambda s: "B%dC%dH%dW%dw%d" % s)
+def test_short_slabs(shape, dtype):
+    B, C, H, Wd, w = shape
+    d = draw(B, C, H, Wd, w, dtype, seed=81)
+    check_fused(d, w, dtype, "short slabs %s %s" % (dtype, shape))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("shape", SHORT_SLABS, ids=lambda s: "B%dC%dH%dW%dw%d" % s)
+def test_short_slabs_integer_bit_exact(shape, dtype):
+    check_integer_exact(shape, dtype, 91 + shape[4])
 
 
 def test_determinism_and_reversed_table():
