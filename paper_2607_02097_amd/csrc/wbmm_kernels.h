@@ -172,6 +172,11 @@ struct KArgs {
   int64_t chw;         // elements between images of one channel (C * H * W)
 };
 
+// Fourth word of a raw buffer resource (stride 0, byte offsets): 32-bit data
+// format, so that loads return the bytes as stored and offsets at or past the
+// record count read as zero.
+constexpr int kBufWord3 = 0x00020000;
+
 // A window row: element offset (from the tensor base) of its first element,
 // number of columns inside the image (0: the row lies outside the image or the
 // window does not exist) and how it moves:
@@ -535,18 +540,23 @@ __device__ __attribute__((always_inline)) inline void tab_load(const typename Ta
   typedef FwdCfg<Tag, WIN> G;
   constexpr int K2 = G::K2;
   const typename Tag::S *tc = tab + c * K2;
+  // unconditional loads (the index clamped to the row): with no branch
+  // around them, the wait for the table before its copy to LDS counts only
+  // the loads issued before the input rows, not those rows too
 #pragma unroll
   for (int i = 0; i < tr.N; ++i) {
-    const int k = tid + i * NTH;
-    if (k < K2) tr.v[i] = tc[REV ? K2 - 1 - k : k];
+    const int k0 = tid + i * NTH;
+    const int k = k0 < K2 ? k0 : K2 - 1;
+    tr.v[i] = tc[REV ? K2 - 1 - k : k];
   }
   if constexpr (HIER) {
     constexpr int K2L = G::K2L;
     const typename Tag::S *tl = tabl + c * K2L;
 #pragma unroll
     for (int i = 0; i < tr.NL; ++i) {
-      const int k = tid + i * NTH;
-      if (k < K2L) tr.vl[i] = tl[REV ? K2L - 1 - k : k];
+      const int k0 = tid + i * NTH;
+      const int k = k0 < K2L ? k0 : K2L - 1;
+      tr.vl[i] = tl[REV ? K2L - 1 - k : k];
     }
   }
 }
@@ -911,7 +921,7 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_img_kernel(const type
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: the sub-tile bases go to scalar registers
   u16 *raw = reinterpret_cast<u16 *>(smem + wave * IC::BUF_BYTES);  // this wave's sub-tile, image layout
   const uint32_t *raw32 = reinterpret_cast<const uint32_t *>(raw);
 
@@ -953,22 +963,29 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_img_kernel(const type
     nb = nw >> ia.lgnw;
     return (int64_t)img * ia.chw + c * ia.hw + (int64_t)(inw >> ia.lgnw) * ia.BE;
   };
-  auto load = [&](int64_t m0, uint4 (&v)[KC]) {
+  // sub-tile m0 into v, zero past its end (none at all unless any): buffer
+  // loads over the sub-tile's byte range, whose range check returns zero for
+  // the chunks beyond it without touching memory, so no lane is masked and
+  // the waits on these loads are counted exactly (chunk offsets are below
+  // 2^31; the host checks it)
+  auto load = [&](int64_t m0, bool any, uint4 (&v)[KC]) {
     uint32_t lim;
     int nb;
-    const char *src = reinterpret_cast<const char *>(x + sub_base(m0, lim, nb));
+    const int64_t base = sub_base(any ? m0 : n0, lim, nb);
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<S *>(x + base), 0, any ? (int)lim : 0, kBufWord3);
 #pragma unroll
-    for (int k = 0; k < KC; ++k) {
-      const uint32_t off = chunk_off(k);
-      v[k] = make_uint4(0, 0, 0, 0);
-      if (off < lim) v[k] = *reinterpret_cast<const uint4 *>(src + off);
-    }
+    for (int k = 0; k < KC; ++k)
+      v[k] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, (int)chunk_off(k), 0, 0));
   };
 
+  // the table loads go first and the input rows right behind them; the
+  // table's copy to LDS and the Toeplitz blocks are built while the rows are
+  // in flight
   TabRegs<Tag, WIN, HIER, kFwdThreads> tr;
   tab_load<Tag, WIN, REV, HIER, kFwdThreads>(tab, tabl, c, tid, tr);
   uint4 nxt[KC];
-  if (nsub > 0) load(n0 + first * 16, nxt);
+  load(n0 + first * 16, nsub > 0, nxt);
   fwd_tables<Tag, WIN, REV, HIER>(tr, Ts, TB, Tsl, TBL, tid);
 
   for (int j = 0; j < nsub; ++j) {
@@ -982,7 +999,7 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_img_kernel(const type
       const int q = lane + 64 * k;
       if (q < IC::CH) *reinterpret_cast<uint4 *>(raw + 8 * q) = nxt[k];
     }
-    if (j + 1 < nsub) load(m0 + 16, nxt);
+    if (j + 1 < nsub) load(m0 + 16, true, nxt);
     wave_lds_sync();
     // LDS addresses derived from ab are recomputed per sub-tile rather than
     // held in registers across the loop
