@@ -59,15 +59,23 @@ def parse():
 # otherwise reported as null.
 TRAFFIC = {
     # (workload, kernel): measured bytes per dispatch (profiles/wbmm_traffic_*.txt)
-    ("bf16_b64_c192_28_w14", "bwd"): {"source": "c221d03bff73e888", "bytes": 62505279},
-    ("bf16_b64_c192_28_w14", "fwd"): {"source": "c221d03bff73e888", "bytes": 41317002},
-    ("bf16_b64_c192_28_w14", "dx"): {"source": "c221d03bff73e888", "bytes": 41240608},
-    ("bf16_b64_c192_28_w14", "dt"): {"source": "c221d03bff73e888", "bytes": 42259690},
-    ("bf16_b64_c96_56_w7", "fwd"): {"source": "c221d03bff73e888", "bytes": 77499596},
-    ("bf16_b64_c192_28_hier7", "hbwd"): {"source": "c221d03bff73e888", "bytes": 63325433},
-    ("bf16_b16_c64_112_hier7", "hbwd"): {"source": "c221d03bff73e888", "bytes": 81969760},
-    ("bf16_b128_c384_14_w14", "bwd"): {"source": "c221d03bff73e888", "bytes": 78907740},
-    ("bf16_b16_c64_112_w14", "bwd"): {"source": "c221d03bff73e888", "bytes": 80830886},
+    ("bf16_b128_c384_14_w14", "bwd"): {"source": "11939e32619390ef", "bytes": 74908352},
+    ("bf16_b128_c384_14_w14", "dt"): {"source": "11939e32619390ef", "bytes": 53027225},
+    ("bf16_b128_c384_14_w14", "dx"): {"source": "11939e32619390ef", "bytes": 46919066},
+    ("bf16_b128_c384_14_w14", "fwd"): {"source": "11939e32619390ef", "bytes": 46919705},
+    ("bf16_b16_c64_112_hier7", "hbwd"): {"source": "11939e32619390ef", "bytes": 80484755},
+    ("bf16_b16_c64_112_hier7", "hfwd"): {"source": "11939e32619390ef", "bytes": 52565956},
+    ("bf16_b16_c64_112_w14", "bwd"): {"source": "11939e32619390ef", "bytes": 78796551},
+    ("bf16_b16_c64_112_w14", "dt"): {"source": "11939e32619390ef", "bytes": 52713702},
+    ("bf16_b16_c64_112_w14", "dx"): {"source": "11939e32619390ef", "bytes": 52289492},
+    ("bf16_b16_c64_112_w14", "fwd"): {"source": "11939e32619390ef", "bytes": 52272179},
+    ("bf16_b64_c192_28_hier7", "hbwd"): {"source": "11939e32619390ef", "bytes": 63214209},
+    ("bf16_b64_c192_28_hier7", "hfwd"): {"source": "11939e32619390ef", "bytes": 41970648},
+    ("bf16_b64_c192_28_w14", "bwd"): {"source": "11939e32619390ef", "bytes": 61610245},
+    ("bf16_b64_c192_28_w14", "dt"): {"source": "11939e32619390ef", "bytes": 42052072},
+    ("bf16_b64_c192_28_w14", "dx"): {"source": "11939e32619390ef", "bytes": 41389592},
+    ("bf16_b64_c192_28_w14", "fwd"): {"source": "11939e32619390ef", "bytes": 41209718},
+    ("bf16_b64_c96_56_w7", "fwd"): {"source": "11939e32619390ef", "bytes": 77463018},
 }
 
 
@@ -149,10 +157,11 @@ def kernel_names(wl, ncu):
         (lambda rev, hier: "<%s,%d," + rev + "," + hier + "," + (tl if hier == "false" else "false") + ">")
     tag = {"bf16": "TagBF16", "f16": "TagF16", "f32": "TagF32"}[wl.dtype]
     names = {"fwd": fk + fwd_tail("false", "false"), "dx": fk + fwd_tail("true", "false"),
-             "dt": dtk + ("<%s,%d,false,0>" if chan_stream else "<%s,%d," + tl + ">"),
-             "bwd": bwk + ("<%s,%d,true,0>" if chan_stream else "<%s,%d," + tl + ">"),
+             # stream kernels: <tag, w, dX too, local half-window (0: plain form), copy waves>
+             "dt": dtk + ("<%s,%d,false,0,0>" if chan_stream else "<%s,%d," + tl + ">"),
+             "bwd": bwk + ("<%s,%d,true,0,4>" if chan_stream else "<%s,%d," + tl + ">"),
              "hfwd": fk + fwd_tail("false", "true"),
-             "hbwd": ("wbmm_bwd_stream_kernel<%s,%d,true," + str(wl.w // 2) + ">") if chan_stream and wl.w >= 10
+             "hbwd": ("wbmm_bwd_stream_kernel<%s,%d,true," + str(wl.w // 2) + ",0>") if chan_stream and wl.w >= 10
                      else "wbmm_hier_backward (several launches) <%s,%d>"}
     return {k: v % (tag, wl.w) for k, v in names.items()}
 
