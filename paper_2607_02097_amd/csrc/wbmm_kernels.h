@@ -51,9 +51,9 @@
 // fixed-offset rows and no more channels than compute units, one 16-wave
 // workgroup per channel (or slab) streams the channel's stages through LDS:
 // four waves accumulate the table gradient while eight compute the input
-// gradient of the same stage, and four copy waves bring the next stage in
-// and send the previous stage's dX rows out, with one workgroup barrier per
-// stage.  Otherwise a
+// gradient of the same stage (the former then store the previous stage's dX
+// rows), and four copy waves bring the next stages in, with one workgroup
+// barrier per stage.  Otherwise a
 // four-wave workgroup per (channel, slab) runs the same products in turn.
 // The hierarchical form (global window 2 wl plus local wl sub-windows) adds
 // local-block products to the forward and input gradient and splits the
@@ -2046,11 +2046,13 @@ __global__ __launch_bounds__(kThreads, (TILED ? 3 : 2)) void wbmm_bwd_kernel(con
 // take the table-gradient products (the P ranges of the 4-wave kernel),
 // waves 4-11 the input-gradient products (four waves per 16-window
 // sub-tile).  The copies -- the next stage into LDS, the stage after it into
-// registers, the previous stage's dX rows to HBM -- are made either by NCW
-// dedicated copy waves (waves 12 .. 11 + NCW) while the twelve compute waves
-// multiply, or, with NCW = 0, by the compute waves themselves after their
-// products.  Products, bins and sums are those of wbmm_bwd_kernel, so the
-// results are bitwise the same.
+// registers, the previous stage's dX rows to HBM -- are made either, with NCW
+// dedicated copy waves (waves 12 .. 11 + NCW), by those waves while the
+// twelve compute waves multiply (the table-gradient waves, whose products end
+// first, store the previous stage's dX rows, and the input-gradient and copy
+// waves the last stage's), or, with NCW = 0, by the compute waves after their
+// products.  Products, bins and sums are those of wbmm_bwd_kernel, so
+// the results are bitwise the same.
 constexpr int kStreamCompute = 12;  // compute waves
 constexpr int kStreamDt = 4;        // of which table-gradient waves
 
@@ -2215,7 +2217,7 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
   constexpr bool COPY = NCW == 0 || (DTW < 0 && DXW < 0);  // this wave copies
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: copy addresses in scalar registers
   const int cw = NCW > 0 ? wave - kStreamCompute : wave;  // index among the copying waves
   const int64_t c = blockIdx.x / a.tiles_per_ch;
   const int64_t slab = blockIdx.x - c * a.tiles_per_ch;
@@ -2284,17 +2286,31 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
     if constexpr (COPY) {
       if (s + 1 < nst) stream_write<Tag, WIN, NC>(smem + ((s + 1) & 1) * SC::STAGE, cw, lane, st);
       if (s + 2 < nst) stream_load<Tag, WIN, NC>(a, x, dy, c, m0 + 2 * CW, s1, cw, lane, st);
-      if (DX && s > 0)
+      if (NCW == 0 && DX && s > 0)
         stream_store<Tag, WIN, NC * 64>(a, dx, c, m0 - CW, s1, cw * 64 + lane,
                                         smem + SC::O_OFF + ((s - 1) & 1) * G::BUF);
+    }
+    // with copy waves, the table-gradient waves (whose products end first)
+    // store the previous stage's dX rows
+    if constexpr (NCW > 0 && DX && DTW >= 0) {
+      if (s > 0)
+        stream_store<Tag, WIN, kStreamDt * 64>(a, dx, c, m0 - CW, s1, DTW * 64 + lane,
+                                               smem + SC::O_OFF + ((s - 1) & 1) * G::BUF);
     }
     __syncthreads();
   }
   // the last stage's dX rows out while the table-gradient waves bin their
   // tiles (the bins lie below the dX buffers)
-  if constexpr (DX && COPY)
+  if constexpr (DX && NCW > 0) {
+    // the input-gradient waves (idle here) and the copy waves together
+    if constexpr (DTW < 0)
+      stream_store<Tag, WIN, (kStreamCompute - kStreamDt + NCW) * 64>(
+          a, dx, c, s0 + (int64_t)(nst - 1) * CW, s1, (wave - kStreamDt) * 64 + lane,
+          smem + SC::O_OFF + ((nst - 1) & 1) * G::BUF);
+  } else if constexpr (DX && COPY) {
     stream_store<Tag, WIN, NC * 64>(a, dx, c, s0 + (int64_t)(nst - 1) * CW, s1, cw * 64 + lane,
                                     smem + SC::O_OFF + ((nst - 1) & 1) * G::BUF);
+  }
   // the table-gradient waves' tiles to the scratch, then the bins summed by
   // all the waves
   constexpr int NPM = bin_tiles_per_wave<G>();
