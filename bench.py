@@ -148,8 +148,10 @@ def kernel_names(wl, ncu):
     fk = "wbmm_fwd_img_kernel" if image_layout(wl) else "wbmm_fwd_kernel"
     tl = "true" if fixed_offset_rows(wl) else "false"
     # channel-stream gradients: fixed-offset rows and no more channels than
-    # compute units
-    chan_stream = fixed_offset_rows(wl) and wl.C <= ncu
+    # compute units, or (plain form) rounds whose last one is at least half full
+    rem = wl.C % ncu
+    chan_stream = fixed_offset_rows(wl) and (wl.C <= ncu or rem == 0 or rem >= ncu // 2)
+    hier_stream = fixed_offset_rows(wl) and wl.C <= ncu
     dtk = "wbmm_bwd_stream_kernel" if chan_stream else "wbmm_dt_kernel"
     bwk = "wbmm_bwd_stream_kernel" if chan_stream else "wbmm_bwd_kernel"
     img = fk == "wbmm_fwd_img_kernel"
@@ -161,7 +163,7 @@ def kernel_names(wl, ncu):
              "dt": dtk + ("<%s,%d,false,0,0>" if chan_stream else "<%s,%d," + tl + ">"),
              "bwd": bwk + ("<%s,%d,true,0,4>" if chan_stream else "<%s,%d," + tl + ">"),
              "hfwd": fk + fwd_tail("false", "true"),
-             "hbwd": ("wbmm_bwd_stream_kernel<%s,%d,true," + str(wl.w // 2) + ",0>") if chan_stream and wl.w >= 10
+             "hbwd": ("wbmm_bwd_stream_kernel<%s,%d,true," + str(wl.w // 2) + ",0>") if hier_stream and wl.w >= 10
                      else "wbmm_hier_backward (several launches) <%s,%d>"}
     return {k: v % (tag, wl.w) for k, v in names.items()}
 

@@ -48,8 +48,9 @@
 // slab order, so the result is bitwise reproducible.
 //
 // Fused backward: x and dy are read once for both gradients.  With
-// fixed-offset rows and no more channels than compute units, one 16-wave
-// workgroup per channel (or slab) streams the channel's stages through LDS:
+// fixed-offset rows and no more channels than compute units (or, in rounds,
+// a last round at least half full), one 16-wave workgroup per channel (or
+// slab) streams the channel's stages through LDS:
 // four waves accumulate the table gradient while eight compute the input
 // gradient of the same stage (the former then store the previous stage's dX
 // rows), and four copy waves bring the next stages in, with one workgroup
@@ -2039,8 +2040,8 @@ __global__ __launch_bounds__(kThreads, (TILED ? 3 : 2)) void wbmm_bwd_kernel(con
 }
 
 // ------------------------------------------ fused backward, channel stream
-// Fixed-offset rows, few channels per compute unit: one workgroup per
-// (channel, slab) and at most one workgroup per compute unit, streaming the
+// Fixed-offset rows: one workgroup per (channel, slab) and at most one
+// workgroup per compute unit at a time, streaming the
 // slab's stages through double-buffered LDS (x and dy tiles, and the
 // input-gradient results) with one workgroup barrier per stage.  Waves 0-3
 // take the table-gradient products (the P ranges of the 4-wave kernel),
@@ -2591,15 +2592,23 @@ static DtPlan plan_dt(const Geom &g) {
 }
 
 
-// Launch plan of the channel-stream kernel (fixed-offset rows, no more
-// channels than compute units): one workgroup per (channel, slab), at most
-// one per compute unit.  Its slabs never outnumber those of plan_dt, which
-// sizes the workspace.
+// Launch plan of the channel-stream kernel (fixed-offset rows): one
+// workgroup per (channel, slab), at most one per compute unit at a time; with
+// more channels than compute units, one slab per channel in rounds (see
+// below).  Its slabs never outnumber those of plan_dt, which sizes the
+// workspace.
 template <class Tag, int WIN>
-static bool stream_plan(const Geom &g, KArgs &b) {
+static bool stream_plan(const Geom &g, KArgs &b, bool rounds = false) {
   typedef BwdCfg<Tag, WIN> G;
   const int ncu = compute_units();
-  if (!b.tiled || ncu <= 0 || g.C > ncu) return false;
+  if (!b.tiled || ncu <= 0) return false;
+  if (g.C > ncu) {
+    // more channels than compute units: whole channels in rounds of one
+    // workgroup per compute unit, taken (where the caller allows rounds)
+    // when the last round fills at least half the chip
+    const int64_t rem = g.C % ncu;
+    if (!rounds || (rem != 0 && rem < ncu / 2)) return false;
+  }
   const int64_t stages = cdiv64(g.N, G::CW);
   int64_t slabs = ncu / g.C;
   if (slabs > stages) slabs = stages;
@@ -2632,7 +2641,7 @@ static hipError_t run_dtable(const void *x, const void *dy, float *dt, void *ws,
   set_tiled<WIN, Tag::ES>(g, a, {x, dy});
   if constexpr (Tag::ES == 4 || WIN % 2 == 0) {
     KArgs b = a;
-    if (stream_plan<Tag, WIN>(g, b)) {
+    if (stream_plan<Tag, WIN>(g, b, true)) {
       // the same stages, bins and sums as the fused pass
       float *spart = b.tiles_per_ch > 1 ? (float *)ws : nullptr;
       constexpr size_t slds = stream_lds_bytes<Tag, WIN>();
@@ -2668,7 +2677,7 @@ static hipError_t run_backward(const void *x, const void *dy, const void *t, voi
   set_tiled<WIN, Tag::ES>(g, a, {x, dy, dx});
   if constexpr (Tag::ES == 4 || WIN % 2 == 0) {
     KArgs b = a;
-    if (stream_plan<Tag, WIN>(g, b)) {
+    if (stream_plan<Tag, WIN>(g, b, true)) {
       float *spart = b.tiles_per_ch > 1 ? (float *)ws : nullptr;
       constexpr size_t slds = stream_lds_bytes<Tag, WIN>();
       static_assert(slds <= 160 * 1024, "workgroup LDS above the 160 KB of a compute unit");

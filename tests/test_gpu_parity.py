@@ -364,6 +364,25 @@ def test_more_channels_than_compute_units(shape, dtype):
     check({"fwd": to_f64(y)}, run_oracle(d, w, ("fwd",)), dtype, "channels>CUs %s %s" % (dtype, shape))
 
 
+# more channels than compute units with a last round at least half full: the
+# gradients stream whole channels in two rounds of one workgroup per compute
+# unit (fused and separate alike)
+TWO_ROUNDS = [
+    (2, 384, 28, 28, 14),  # 384 = 256 + 128 on 256 compute units
+    (1, 400, 28, 56, 14),  # 400 = 256 + 144; eight windows per image
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("shape", TWO_ROUNDS, ids=lambda s: "B%dC%dH%dW%dw%d" % s)
+def test_channel_stream_in_rounds(shape, dtype):
+    B, C, H, Wd, w = shape
+    ncu = compute_units()
+    assert C > ncu and C % ncu >= ncu // 2
+    d = draw(B, C, H, Wd, w, dtype, seed=61)
+    check_fused(d, w, dtype, "rounds %s %s" % (dtype, shape))
+
+
 def check_integer_exact(shape, dtype, seed):
     """Integers in {-1, 0, 1}: every sum is exact, so the forward and both
     gradients (separate and fused) equal the oracle bit for bit."""
@@ -405,6 +424,12 @@ def test_short_slabs(shape, dtype):
     B, C, H, Wd, w = shape
     d = draw(B, C, H, Wd, w, dtype, seed=81)
     check_fused(d, w, dtype, "short slabs %s %s" % (dtype, shape))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("shape", TWO_ROUNDS, ids=lambda s: "B%dC%dH%dW%dw%d" % s)
+def test_channel_stream_in_rounds_integer_bit_exact(shape, dtype):
+    check_integer_exact(shape, dtype, 97 + shape[1])
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
