@@ -2046,14 +2046,14 @@ __global__ __launch_bounds__(kThreads, (TILED ? 3 : 2)) void wbmm_bwd_kernel(con
 // input-gradient results) with one workgroup barrier per stage.  Waves 0-3
 // take the table-gradient products (the P ranges of the 4-wave kernel),
 // waves 4-11 the input-gradient products (four waves per 16-window
-// sub-tile).  The copies -- the next stage into LDS, the stage after it into
-// registers, the previous stage's dX rows to HBM -- are made either, with NCW
-// dedicated copy waves (waves 12 .. 11 + NCW), by those waves while the
-// twelve compute waves multiply (the table-gradient waves, whose products end
-// first, store the previous stage's dX rows, and the input-gradient and copy
-// waves the last stage's), or, with NCW = 0, by the compute waves after their
-// products.  Products, bins and sums are those of wbmm_bwd_kernel, so
-// the results are bitwise the same.
+// sub-tile).  The table-gradient waves, whose products end first, store the
+// previous stage's dX rows.  The other copies -- the next stage into LDS, the
+// stage after it into registers -- are made either by NCW dedicated copy
+// waves (waves 12 .. 11 + NCW) while the twelve compute waves multiply, or,
+// with NCW = 0, by the compute waves after their products; the last stage's
+// dX rows go out from the input-gradient and copy waves (every wave with
+// NCW = 0).  Products, bins and sums are those of wbmm_bwd_kernel, so the
+// results are bitwise the same.
 constexpr int kStreamCompute = 12;  // compute waves
 constexpr int kStreamDt = 4;        // of which table-gradient waves
 
@@ -2287,13 +2287,10 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
     if constexpr (COPY) {
       if (s + 1 < nst) stream_write<Tag, WIN, NC>(smem + ((s + 1) & 1) * SC::STAGE, cw, lane, st);
       if (s + 2 < nst) stream_load<Tag, WIN, NC>(a, x, dy, c, m0 + 2 * CW, s1, cw, lane, st);
-      if (NCW == 0 && DX && s > 0)
-        stream_store<Tag, WIN, NC * 64>(a, dx, c, m0 - CW, s1, cw * 64 + lane,
-                                        smem + SC::O_OFF + ((s - 1) & 1) * G::BUF);
     }
-    // with copy waves, the table-gradient waves (whose products end first)
-    // store the previous stage's dX rows
-    if constexpr (NCW > 0 && DX && DTW >= 0) {
+    // the table-gradient waves (whose products end first) store the previous
+    // stage's dX rows
+    if constexpr (DX && DTW >= 0) {
       if (s > 0)
         stream_store<Tag, WIN, kStreamDt * 64>(a, dx, c, m0 - CW, s1, DTW * 64 + lane,
                                                smem + SC::O_OFF + ((s - 1) & 1) * G::BUF);
