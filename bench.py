@@ -59,23 +59,23 @@ def parse():
 # otherwise reported as null.
 TRAFFIC = {
     # (workload, kernel): measured bytes per dispatch (profiles/wbmm_traffic_*.txt)
-    ("bf16_b128_c384_14_w14", "bwd"): {"source": "11939e32619390ef", "bytes": 74908352},
-    ("bf16_b128_c384_14_w14", "dt"): {"source": "11939e32619390ef", "bytes": 53027225},
-    ("bf16_b128_c384_14_w14", "dx"): {"source": "11939e32619390ef", "bytes": 46919066},
-    ("bf16_b128_c384_14_w14", "fwd"): {"source": "11939e32619390ef", "bytes": 46919705},
-    ("bf16_b16_c64_112_hier7", "hbwd"): {"source": "11939e32619390ef", "bytes": 80484755},
-    ("bf16_b16_c64_112_hier7", "hfwd"): {"source": "11939e32619390ef", "bytes": 52565956},
-    ("bf16_b16_c64_112_w14", "bwd"): {"source": "11939e32619390ef", "bytes": 78796551},
-    ("bf16_b16_c64_112_w14", "dt"): {"source": "11939e32619390ef", "bytes": 52713702},
-    ("bf16_b16_c64_112_w14", "dx"): {"source": "11939e32619390ef", "bytes": 52289492},
-    ("bf16_b16_c64_112_w14", "fwd"): {"source": "11939e32619390ef", "bytes": 52272179},
-    ("bf16_b64_c192_28_hier7", "hbwd"): {"source": "11939e32619390ef", "bytes": 63214209},
-    ("bf16_b64_c192_28_hier7", "hfwd"): {"source": "11939e32619390ef", "bytes": 41970648},
-    ("bf16_b64_c192_28_w14", "bwd"): {"source": "11939e32619390ef", "bytes": 61610245},
-    ("bf16_b64_c192_28_w14", "dt"): {"source": "11939e32619390ef", "bytes": 42052072},
-    ("bf16_b64_c192_28_w14", "dx"): {"source": "11939e32619390ef", "bytes": 41389592},
-    ("bf16_b64_c192_28_w14", "fwd"): {"source": "11939e32619390ef", "bytes": 41209718},
-    ("bf16_b64_c96_56_w7", "fwd"): {"source": "11939e32619390ef", "bytes": 77463018},
+    ("bf16_b128_c384_14_w14", "bwd"): {"source": "b9aeb56d94865c02", "bytes": 73230558},
+    ("bf16_b128_c384_14_w14", "dt"): {"source": "b9aeb56d94865c02", "bytes": 52127871},
+    ("bf16_b128_c384_14_w14", "dx"): {"source": "b9aeb56d94865c02", "bytes": 46919162},
+    ("bf16_b128_c384_14_w14", "fwd"): {"source": "b9aeb56d94865c02", "bytes": 46919321},
+    ("bf16_b16_c64_112_hier7", "hbwd"): {"source": "b9aeb56d94865c02", "bytes": 80237410},
+    ("bf16_b16_c64_112_hier7", "hfwd"): {"source": "b9aeb56d94865c02", "bytes": 52557320},
+    ("bf16_b16_c64_112_w14", "bwd"): {"source": "b9aeb56d94865c02", "bytes": 78944820},
+    ("bf16_b16_c64_112_w14", "dt"): {"source": "b9aeb56d94865c02", "bytes": 52798590},
+    ("bf16_b16_c64_112_w14", "dx"): {"source": "b9aeb56d94865c02", "bytes": 52269812},
+    ("bf16_b16_c64_112_w14", "fwd"): {"source": "b9aeb56d94865c02", "bytes": 52285874},
+    ("bf16_b64_c192_28_hier7", "hbwd"): {"source": "b9aeb56d94865c02", "bytes": 62969133},
+    ("bf16_b64_c192_28_hier7", "hfwd"): {"source": "b9aeb56d94865c02", "bytes": 41853821},
+    ("bf16_b64_c192_28_w14", "bwd"): {"source": "b9aeb56d94865c02", "bytes": 61755476},
+    ("bf16_b64_c192_28_w14", "dt"): {"source": "b9aeb56d94865c02", "bytes": 42137088},
+    ("bf16_b64_c192_28_w14", "dx"): {"source": "b9aeb56d94865c02", "bytes": 41239704},
+    ("bf16_b64_c192_28_w14", "fwd"): {"source": "b9aeb56d94865c02", "bytes": 41328182},
+    ("bf16_b64_c96_56_w7", "fwd"): {"source": "b9aeb56d94865c02", "bytes": 77463002},
 }
 
 
