@@ -424,6 +424,15 @@ __host__ __device__ constexpr size_t fwd_lds_bytes() {
          (HIER ? (size_t)(G::TSL_LEN + G::TBL_LEN) * Tag::ES : 0);
 }
 
+// Workgroup index regrouped by die: the dispatcher deals workgroups to the
+// eight dies in turn (workgroup b runs on die b mod 8), so with G a multiple
+// of 8 workgroup b takes index (b mod 8) G/8 + b/8 and each die runs one
+// consecutive block of indices: neighbouring channels, whose image planes
+// share the 128-byte lines at their ends, then share that die's L2.
+__device__ __attribute__((always_inline)) inline uint32_t die_major(uint32_t b, uint32_t G) {
+  return (G & 7u) ? b : (b & 7u) * (G >> 3) + (b >> 3);
+}
+
 // Wave-level ordering of LDS accesses made by different lanes of one wave.
 __device__ __attribute__((always_inline)) inline void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -694,8 +703,9 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_kernel(const typename
   unsigned char *buf = smem + wave * 16 * LDSW * Tag::ES;  // this wave's sub-tile
   S *rowp = reinterpret_cast<S *>(buf);
 
-  const int64_t c = blockIdx.x / a.tiles_per_ch;
-  const int64_t n0 = (int64_t)(blockIdx.x - c * a.tiles_per_ch) * a.tile;
+  const uint32_t bid = die_major(blockIdx.x, gridDim.x);
+  const int64_t c = bid / a.tiles_per_ch;
+  const int64_t n0 = (int64_t)(bid - c * a.tiles_per_ch) * a.tile;
   const int nwin = (int)((n0 + a.tile <= a.N) ? a.tile : a.N - n0);
   const int spw = a.tile / (16 * kFwdWaves);  // sub-tiles per wave
   const int first = wave * spw;               // this wave's first sub-tile
@@ -926,8 +936,9 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_img_kernel(const type
   u16 *raw = reinterpret_cast<u16 *>(smem + wave * IC::BUF_BYTES);  // this wave's sub-tile, image layout
   const uint32_t *raw32 = reinterpret_cast<const uint32_t *>(raw);
 
-  const int64_t c = blockIdx.x / a.tiles_per_ch;
-  const int64_t n0 = (int64_t)(blockIdx.x - c * a.tiles_per_ch) * a.tile;
+  const uint32_t bid = die_major(blockIdx.x, gridDim.x);
+  const int64_t c = bid / a.tiles_per_ch;
+  const int64_t n0 = (int64_t)(bid - c * a.tiles_per_ch) * a.tile;
   const int nwin = (int)((n0 + a.tile <= a.N) ? a.tile : a.N - n0);
   const int spw = a.tile / (16 * kFwdWaves);
   const int first = wave * spw;
@@ -1737,8 +1748,9 @@ __device__ __attribute__((always_inline)) void dt_wave(const typename Tag::S *__
   typedef PSpan<G::NPT, WAVE> SP;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int64_t c = blockIdx.x / a.tiles_per_ch;
-  const int64_t slab = blockIdx.x - c * a.tiles_per_ch;
+  const uint32_t bid = die_major(blockIdx.x, gridDim.x);
+  const int64_t c = bid / a.tiles_per_ch;
+  const int64_t slab = bid - c * a.tiles_per_ch;
   const int64_t s0 = slab * a.tile;
   const int64_t s1 = (s0 + a.tile < a.N) ? s0 + a.tile : a.N;
 
@@ -1978,8 +1990,9 @@ __device__ __attribute__((always_inline)) void bwd_wave(const typename Tag::S *_
   constexpr int RP = G::RP, K1 = G::K1, K2 = G::K2;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int64_t c = blockIdx.x / a.tiles_per_ch;
-  const int64_t slab = blockIdx.x - c * a.tiles_per_ch;
+  const uint32_t bid = die_major(blockIdx.x, gridDim.x);
+  const int64_t c = bid / a.tiles_per_ch;
+  const int64_t slab = bid - c * a.tiles_per_ch;
   const int64_t s0 = slab * a.tile;
   const int64_t s1 = (s0 + a.tile < a.N) ? s0 + a.tile : a.N;
   unsigned char *Xt = smem;
@@ -2220,8 +2233,9 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: copy addresses in scalar registers
   const int cw = NCW > 0 ? wave - kStreamCompute : wave;  // index among the copying waves
-  const int64_t c = blockIdx.x / a.tiles_per_ch;
-  const int64_t slab = blockIdx.x - c * a.tiles_per_ch;
+  const uint32_t bid = die_major(blockIdx.x, gridDim.x);
+  const int64_t c = bid / a.tiles_per_ch;
+  const int64_t slab = bid - c * a.tiles_per_ch;
   const int64_t s0 = slab * a.tile;
   const int64_t s1 = (s0 + a.tile < a.N) ? s0 + a.tile : a.N;
   const int nst = (int)((s1 - s0 + CW - 1) / CW);
