@@ -59,23 +59,23 @@ def parse():
 # otherwise reported as null.
 TRAFFIC = {
     # (workload, kernel): measured bytes per dispatch (profiles/wbmm_traffic_*.txt)
-    ("bf16_b128_c384_14_w14", "bwd"): {"source": "b9aeb56d94865c02", "bytes": 73230558},
-    ("bf16_b128_c384_14_w14", "dt"): {"source": "b9aeb56d94865c02", "bytes": 52127871},
-    ("bf16_b128_c384_14_w14", "dx"): {"source": "b9aeb56d94865c02", "bytes": 46919162},
-    ("bf16_b128_c384_14_w14", "fwd"): {"source": "b9aeb56d94865c02", "bytes": 46919321},
-    ("bf16_b16_c64_112_hier7", "hbwd"): {"source": "b9aeb56d94865c02", "bytes": 80237410},
-    ("bf16_b16_c64_112_hier7", "hfwd"): {"source": "b9aeb56d94865c02", "bytes": 52557320},
-    ("bf16_b16_c64_112_w14", "bwd"): {"source": "b9aeb56d94865c02", "bytes": 78944820},
-    ("bf16_b16_c64_112_w14", "dt"): {"source": "b9aeb56d94865c02", "bytes": 52798590},
-    ("bf16_b16_c64_112_w14", "dx"): {"source": "b9aeb56d94865c02", "bytes": 52269812},
-    ("bf16_b16_c64_112_w14", "fwd"): {"source": "b9aeb56d94865c02", "bytes": 52285874},
-    ("bf16_b64_c192_28_hier7", "hbwd"): {"source": "b9aeb56d94865c02", "bytes": 62969133},
-    ("bf16_b64_c192_28_hier7", "hfwd"): {"source": "b9aeb56d94865c02", "bytes": 41853821},
-    ("bf16_b64_c192_28_w14", "bwd"): {"source": "b9aeb56d94865c02", "bytes": 61755476},
-    ("bf16_b64_c192_28_w14", "dt"): {"source": "b9aeb56d94865c02", "bytes": 42137088},
-    ("bf16_b64_c192_28_w14", "dx"): {"source": "b9aeb56d94865c02", "bytes": 41239704},
-    ("bf16_b64_c192_28_w14", "fwd"): {"source": "b9aeb56d94865c02", "bytes": 41328182},
-    ("bf16_b64_c96_56_w7", "fwd"): {"source": "b9aeb56d94865c02", "bytes": 77463002},
+    ("bf16_b128_c384_14_w14", "bwd"): {"source": "1be8e102d29168c4", "bytes": 60219350},
+    ("bf16_b128_c384_14_w14", "dt"): {"source": "1be8e102d29168c4", "bytes": 40328968},
+    ("bf16_b128_c384_14_w14", "dx"): {"source": "1be8e102d29168c4", "bytes": 39192848},
+    ("bf16_b128_c384_14_w14", "fwd"): {"source": "1be8e102d29168c4", "bytes": 39195994},
+    ("bf16_b16_c64_112_hier7", "hbwd"): {"source": "1be8e102d29168c4", "bytes": 79897040},
+    ("bf16_b16_c64_112_hier7", "hfwd"): {"source": "1be8e102d29168c4", "bytes": 51802775},
+    ("bf16_b16_c64_112_w14", "bwd"): {"source": "1be8e102d29168c4", "bytes": 78631243},
+    ("bf16_b16_c64_112_w14", "dt"): {"source": "1be8e102d29168c4", "bytes": 52785286},
+    ("bf16_b16_c64_112_w14", "dx"): {"source": "1be8e102d29168c4", "bytes": 51636015},
+    ("bf16_b16_c64_112_w14", "fwd"): {"source": "1be8e102d29168c4", "bytes": 51651800},
+    ("bf16_b64_c192_28_hier7", "hbwd"): {"source": "1be8e102d29168c4", "bytes": 60637506},
+    ("bf16_b64_c192_28_hier7", "hfwd"): {"source": "1be8e102d29168c4", "bytes": 39923792},
+    ("bf16_b64_c192_28_w14", "bwd"): {"source": "1be8e102d29168c4", "bytes": 59375018},
+    ("bf16_b64_c192_28_w14", "dt"): {"source": "1be8e102d29168c4", "bytes": 39769544},
+    ("bf16_b64_c192_28_w14", "dx"): {"source": "1be8e102d29168c4", "bytes": 39766973},
+    ("bf16_b64_c192_28_w14", "fwd"): {"source": "1be8e102d29168c4", "bytes": 39281190},
+    ("bf16_b64_c96_56_w7", "fwd"): {"source": "1be8e102d29168c4", "bytes": 77261929},
 }
 
 
