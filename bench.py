@@ -148,7 +148,9 @@ def kernel_names(wl, ncu):
     fk = "wbmm_fwd_img_kernel" if image_layout(wl) else "wbmm_fwd_kernel"
     tl = "true" if fixed_offset_rows(wl) else "false"
     # channel-stream gradients: fixed-offset rows and no more channels than
-    # compute units, or (plain form) rounds whose last one is at least half full
+    # compute units, or (plain form) rounds whose last one is at least half
+    # full (a nearly empty last round takes runs of stages where they apply,
+    # in no workload here, else the four-wave kernels)
     rem = wl.C % ncu
     chan_stream = fixed_offset_rows(wl) and (wl.C <= ncu or rem == 0 or rem >= ncu // 2)
     hier_stream = fixed_offset_rows(wl) and wl.C <= ncu
@@ -159,11 +161,11 @@ def kernel_names(wl, ncu):
         (lambda rev, hier: "<%s,%d," + rev + "," + hier + "," + (tl if hier == "false" else "false") + ">")
     tag = {"bf16": "TagBF16", "f16": "TagF16", "f32": "TagF32"}[wl.dtype]
     names = {"fwd": fk + fwd_tail("false", "false"), "dx": fk + fwd_tail("true", "false"),
-             # stream kernels: <tag, w, dX too, local half-window (0: plain form), copy waves>
-             "dt": dtk + ("<%s,%d,false,0,0>" if chan_stream else "<%s,%d," + tl + ">"),
-             "bwd": bwk + ("<%s,%d,true,0,4>" if chan_stream else "<%s,%d," + tl + ">"),
+             # stream kernels: <tag, w, dX too, local half-window (0: plain form), copy waves, runs>
+             "dt": dtk + ("<%s,%d,false,0,0,false>" if chan_stream else "<%s,%d," + tl + ">"),
+             "bwd": bwk + ("<%s,%d,true,0,4,false>" if chan_stream else "<%s,%d," + tl + ">"),
              "hfwd": fk + fwd_tail("false", "true"),
-             "hbwd": ("wbmm_bwd_stream_kernel<%s,%d,true," + str(wl.w // 2) + ",0>") if hier_stream and wl.w >= 10
+             "hbwd": ("wbmm_bwd_stream_kernel<%s,%d,true," + str(wl.w // 2) + ",0,false>") if hier_stream and wl.w >= 10
                      else "wbmm_hier_backward (several launches) <%s,%d>"}
     return {k: v % (tag, wl.w) for k, v in names.items()}
 

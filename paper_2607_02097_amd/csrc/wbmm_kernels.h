@@ -171,6 +171,11 @@ struct KArgs {
   int BE;              // elements of one band (w * W)
   int WPI;             // windows per image
   int64_t chw;         // elements between images of one channel (C * H * W)
+  // Channel-stream runs (more channels than compute units): workgroup r
+  // streams the stages [r run, (r + 1) run) of all channels' stages taken in
+  // order (nstc per channel); 0: one workgroup per (channel, slab).
+  int run;
+  int nstc;
 };
 
 // Fourth word of a raw buffer resource (stride 0, byte offsets): 32-bit data
@@ -1555,6 +1560,38 @@ __device__ __attribute__((always_inline)) inline void dt_bin_sum(const float *sc
   }
 }
 
+// dt_bin_sum for one window row per tile (bin index = table index, stored
+// straight to the table gradient out), its tile loop kept rolled: called
+// between the stages of the channel-stream runs, where the unrolled loop's
+// loads in flight would take registers the stages need.  The same sums in
+// the same order.
+template <class Tag, int WIN, class G, int WAVE>
+__device__ __attribute__((always_inline)) inline void dt_bin_sum_rows(const float *scr, float *out) {
+  typedef PSpan<G::NPT, WAVE> SP;
+  static_assert(G::R == 1, "one window row per tile");
+  constexpr int NPT = G::NPT, NBT = G::NBT, PLO = SP::lo, NP = SP::np, TSTR = kBinTile;
+  const int lane = threadIdx.x & 63;
+  const int s = lane & 15;
+#pragma unroll 1
+  for (int it = 0; it < cdiv(NP * 16, 64); ++it) {
+    const int j = (lane >> 4) + 4 * it;
+    if (j < NP) {
+      const float *col = scr + j * TSTR + s;
+      float lo = 0.f, hi = 0.f;
+#pragma unroll
+      for (int xi = 0; xi < 16; ++xi) {
+        const float v = col[((xi & ~3) + ((xi + (xi >> 2)) & 3)) * 16];
+        const bool upper = xi + s <= 15;
+        lo += upper ? v : 0.f;
+        hi += upper ? 0.f : v;
+      }
+      float *bp = out + (PLO + j + NPT - 1) * NBT + WIN - 1;
+      if (s <= WIN - 1) bp[-s] = lo;
+      if (s >= 1 && 16 - s <= WIN - 1) bp[16 - s] = hi;
+    }
+  }
+}
+
 // Diagonal binning of one wave's accumulator tiles into the bins at the
 // end of the scratch (LDS of the stages); no workgroup barrier inside.
 // Every tile of the wave goes to LDS at once; bin (da, dw) of tile P sums
@@ -2089,6 +2126,15 @@ struct StreamCfg {
   static constexpr int TSL_OFF = rup(END, 16);
   static constexpr int TBL_OFF = TSL_OFF + rup(F::TSL_LEN * Tag::ES, 16);
   static constexpr int END_H = TBL_OFF + F::TBL_LEN * Tag::ES;
+  // runs (one window row per tile, 16-bit): the second channel's table row
+  // and blocks, then the table-gradient waves' bin scratch, after everything
+  // else, when it fits in the 160 KB of LDS
+  static constexpr int NPM = bin_tiles_per_wave<G>();
+  static constexpr int TS2_OFF = rup(END, 16);
+  static constexpr int TB2_OFF = TS2_OFF + rup(F::TS_LEN * Tag::ES, 16);
+  static constexpr int SCR_OFF = TB2_OFF + F::TB_LEN * Tag::ES;
+  static constexpr int END_R = SCR_OFF + kWaves * NPM * kBinTile * 4;
+  static constexpr bool RUNS = Tag::W16 && G::R == 1 && END_R <= 160 * 1024;
   static_assert(bins_lds_bytes<G>() <= O_OFF, "bins must not reach the dX buffers");
 };
 
@@ -2104,7 +2150,8 @@ struct StreamCopy {
 
 template <class Tag, int WIN, bool HIER = false>
 __host__ __device__ constexpr size_t stream_lds_bytes() {
-  return (size_t)(HIER ? StreamCfg<Tag, WIN>::END_H : StreamCfg<Tag, WIN>::END);
+  typedef StreamCfg<Tag, WIN> SC;
+  return (size_t)(HIER ? SC::END_H : SC::RUNS ? SC::END_R : SC::END);
 }
 
 template <class Tag, int WIN, int NC>
@@ -2212,7 +2259,7 @@ __device__ __attribute__((always_inline)) inline void stream_store(const KArgs &
 // when DX is false: the table gradient alone, with the same stages, bins and
 // sums as the fused pass), else a copy wave.  With NCW = 0 every wave copies
 // (after its products); otherwise only the NCW copy waves do.
-template <class Tag, int WIN, int DTW, int DXW, bool DX, int HL, int NCW>
+template <class Tag, int WIN, int DTW, int DXW, bool DX, int HL, int NCW, bool RUN>
 __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S *__restrict__ x,
                                                            const typename Tag::S *__restrict__ dy,
                                                            const typename Tag::S *__restrict__ tab,
@@ -2234,11 +2281,45 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: copy addresses in scalar registers
   const int cw = NCW > 0 ? wave - kStreamCompute : wave;  // index among the copying waves
   const uint32_t bid = die_major(blockIdx.x, gridDim.x);
-  const int64_t c = bid / a.tiles_per_ch;
-  const int64_t slab = bid - c * a.tiles_per_ch;
-  const int64_t s0 = slab * a.tile;
-  const int64_t s1 = (s0 + a.tile < a.N) ? s0 + a.tile : a.N;
-  const int nst = (int)((s1 - s0 + CW - 1) / CW);
+  // runs: stages g0 .. g0 + nst - 1 of all channels' stages (the host keeps
+  // their count below 2^31, so 32-bit arithmetic); c is the run's first
+  // channel.  Otherwise one (channel, slab).
+  constexpr bool RUNS = RUN && HL == 0 && SC::RUNS;
+  constexpr bool runs = RUNS;
+  int64_t c, slab, s0, s1;
+  uint32_t g0 = 0;
+  int nst;
+  if (runs) {
+    g0 = bid * (uint32_t)a.run;
+    const uint32_t tot = (uint32_t)a.C * (uint32_t)a.nstc;
+    nst = (int)((g0 + (uint32_t)a.run < tot ? g0 + (uint32_t)a.run : tot) - g0);
+    c = g0 / (uint32_t)a.nstc;
+    slab = 0;
+    s0 = 0;
+    s1 = a.N;
+  } else {
+    c = bid / a.tiles_per_ch;
+    slab = bid - c * a.tiles_per_ch;
+    s0 = slab * a.tile;
+    s1 = (s0 + a.tile < a.N) ? s0 + a.tile : a.N;
+    nst = (int)((s1 - s0 + CW - 1) / CW);
+  }
+  // stage j of this workgroup: channel cj, first window mj
+  auto locate = [&](int j, int64_t &cj, int64_t &mj) {
+    if (runs) {
+      const uint32_t gg = g0 + (uint32_t)j;
+      const uint32_t cc = gg / (uint32_t)a.nstc;
+      cj = cc;
+      mj = (int64_t)(gg - cc * (uint32_t)a.nstc) * CW;
+    } else {
+      cj = c;
+      mj = s0 + (int64_t)j * CW;
+    }
+  };
+  // runs: the second channel reached (if any) takes the second table copy
+  int64_t cl, ml;
+  locate(nst - 1, cl, ml);
+  const bool two = runs && cl > c;
   S *Ts = reinterpret_cast<S *>(smem + SC::TS_OFF);
   S *TB = reinterpret_cast<S *>(smem + SC::TB_OFF);
   S *Tsl = reinterpret_cast<S *>(smem + SC::TSL_OFF);  // hierarchical input gradient only
@@ -2252,24 +2333,42 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
   // of the bulk loads); the table row and (16-bit) its Toeplitz blocks ->
   // LDS; stage 0 -> LDS buffer 0, stage 1 in flight
   constexpr bool HX = DX && HL > 0;  // hierarchical input gradient: both tables
-  TabRegs<Tag, WIN, HX, NTH> tr;
-  if constexpr (DX) tab_load<Tag, WIN, true, HX, NTH>(tab, tabl, c, tid, tr);
+  TabRegs<Tag, WIN, HX, NTH> tr, tr2;
+  if constexpr (DX) {
+    tab_load<Tag, WIN, true, HX, NTH>(tab, tabl, c, tid, tr);
+    if constexpr (RUNS) tab_load<Tag, WIN, true, false, NTH>(tab, nullptr, two ? c + 1 : c, tid, tr2);
+  }
   StreamRows<Tag, WIN, NC> st;
-  if constexpr (COPY) stream_load<Tag, WIN, NC>(a, x, dy, c, s0, s1, cw, lane, st);
+  int64_t cj, mj;
+  locate(0, cj, mj);
+  if constexpr (COPY) stream_load<Tag, WIN, NC>(a, x, dy, cj, mj, s1, cw, lane, st);
   if constexpr (HX) {
     fwd_tables<Tag, WIN, true, true, NTH>(tr, Ts, TB, Tsl, TBL, tid);
   } else if constexpr (DX) {
+    S *Ts2 = reinterpret_cast<S *>(smem + SC::TS2_OFF);
+    S *TB2 = reinterpret_cast<S *>(smem + SC::TB2_OFF);
 #pragma unroll
     for (int i = 0; i < tr.N; ++i)
-      if (tid + i * NTH < K2) Ts[tid + i * NTH] = tr.v[i];
+      if (tid + i * NTH < K2) {
+        Ts[tid + i * NTH] = tr.v[i];
+        if constexpr (RUNS) {
+          if (two) Ts2[tid + i * NTH] = tr2.v[i];
+        }
+      }
     __syncthreads();
     if constexpr (Tag::W16) {
       build_tb<Tag, WIN, NTH>(Ts, TB, tid);
+      if constexpr (RUNS) {
+        if (two) build_tb<Tag, WIN, NTH>(Ts2, TB2, tid);
+      }
     }
   }
   if constexpr (COPY) {
     stream_write<Tag, WIN, NC>(smem, cw, lane, st);
-    if (nst > 1) stream_load<Tag, WIN, NC>(a, x, dy, c, s0 + CW, s1, cw, lane, st);
+    if (nst > 1) {
+      locate(1, cj, mj);
+      stream_load<Tag, WIN, NC>(a, x, dy, cj, mj, s1, cw, lane, st);
+    }
   }
   __syncthreads();
 
@@ -2285,8 +2384,38 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
     for (int i = 0; i < DS::NQ; ++i) bfw[i] = fwd_bfrag<Tag, WIN>(TB, DS::QLO + i, g, ln);
   }
 
-  for (int s = 0; s < nst; ++s) {
-    const int64_t m0 = s0 + (int64_t)s * CW;
+  // runs: the table-gradient waves' tiles of channel cx binned (into scratch
+  // of their own) and stored as that channel's partial: the first of its two
+  // (slot 0) when this run holds the channel's first stage, else the second;
+  // a channel whole in this run also zeroes its second.  The sum kernel adds
+  // the two.
+  auto run_bin = [&](int64_t cx) {
+    if constexpr (RUNS && DTW >= 0) {
+      float *mine = reinterpret_cast<float *>(smem + SC::SCR_OFF) + DTW * SC::NPM * kBinTile;
+      const int64_t first = cx * a.nstc;
+      const int slot = first >= (int64_t)g0 ? 0 : 1;
+      wave_lds_sync();
+      dt_bin_write<Tag, WIN, G, DTW>(acc, mine);
+      wave_lds_sync();
+      dt_bin_sum_rows<Tag, WIN, G, DTW>(mine, part + ((int64_t)slot * a.C + cx) * K2);
+      if (slot == 0 && first + a.nstc <= (int64_t)g0 + nst) {
+        float *z = part + (a.C + cx) * K2;
+#pragma unroll
+        for (int j = 0; j < SP::np; ++j)
+          for (int q = lane; q < K1; q += 64) z[(SP::lo + j + G::NPT - 1) * K1 + q] = 0.f;
+      }
+#pragma unroll
+      for (int j = 0; j < SP::na; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  };
+
+  // runs: channel and stage within it of this stage (cs, ls) and of the
+  // previous one (cp, lp), advanced without divisions
+  uint32_t cs = (uint32_t)c, ls = 0, cp = 0, lp = 0;
+  if constexpr (RUNS) ls = g0 - cs * (uint32_t)a.nstc;
+  auto stage = [&](int s) {
+    const int64_t m0 = RUNS ? (int64_t)ls * CW : s0 + (int64_t)s * CW;
+    const int64_t mprev = RUNS ? (int64_t)lp * CW : m0 - CW;
     unsigned char *cur = smem + (s & 1) * SC::STAGE;
     unsigned char *obuf = smem + SC::O_OFF + (s & 1) * G::BUF;
     // this stage's products
@@ -2300,16 +2429,53 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
     // the one after it in flight, the previous stage's dX rows out
     if constexpr (COPY) {
       if (s + 1 < nst) stream_write<Tag, WIN, NC>(smem + ((s + 1) & 1) * SC::STAGE, cw, lane, st);
-      if (s + 2 < nst) stream_load<Tag, WIN, NC>(a, x, dy, c, m0 + 2 * CW, s1, cw, lane, st);
+      if (s + 2 < nst) {
+        uint32_t cn = cs, ln = ls;
+        if constexpr (RUNS) {
+          ln += 2;
+          if (ln >= (uint32_t)a.nstc) { ln -= (uint32_t)a.nstc; ++cn; }
+          if (ln >= (uint32_t)a.nstc) { ln -= (uint32_t)a.nstc; ++cn; }
+        }
+        stream_load<Tag, WIN, NC>(a, x, dy, RUNS ? (int64_t)cn : c, RUNS ? (int64_t)ln * CW : m0 + 2 * CW, s1, cw,
+                                  lane, st);
+      }
     }
     // the table-gradient waves (whose products end first) store the previous
     // stage's dX rows
     if constexpr (DX && DTW >= 0) {
       if (s > 0)
-        stream_store<Tag, WIN, kStreamDt * 64>(a, dx, c, m0 - CW, s1, DTW * 64 + lane,
+        stream_store<Tag, WIN, kStreamDt * 64>(a, dx, RUNS ? (int64_t)cp : c, mprev, s1, DTW * 64 + lane,
                                                smem + SC::O_OFF + ((s - 1) & 1) * G::BUF);
     }
     __syncthreads();
+    if constexpr (RUNS) {
+      cp = cs;
+      lp = ls;
+      if (++ls == (uint32_t)a.nstc) {
+        ls = 0;
+        ++cs;
+      }
+    }
+  };
+  if constexpr (RUNS) {
+    // the first channel's stages; where the run reaches a second channel,
+    // the first one's table gradient out and the input-gradient fragments
+    // from the second table's blocks, then the second channel's stages (the
+    // binning outside the stage loop, whose registers it would take)
+    const int sw = two ? (int)((uint32_t)(c + 1) * (uint32_t)a.nstc - g0) : nst;
+    for (int s = 0; s < sw; ++s) stage(s);
+    if (two) {
+      run_bin(c);
+      if constexpr (PRE) {
+        const S *TB2 = reinterpret_cast<const S *>(smem + SC::TB2_OFF);
+        const int g = lane >> 4, ln = lane & 15;
+#pragma unroll
+        for (int i = 0; i < DS::NQ; ++i) bfw[i] = fwd_bfrag<Tag, WIN>(TB2, DS::QLO + i, g, ln);
+      }
+      for (int s = sw; s < nst; ++s) stage(s);
+    }
+  } else {
+    for (int s = 0; s < nst; ++s) stage(s);
   }
   // the last stage's dX rows out while the table-gradient waves bin their
   // tiles (the bins lie below the dX buffers)
@@ -2317,11 +2483,17 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
     // the input-gradient waves (idle here) and the copy waves together
     if constexpr (DTW < 0)
       stream_store<Tag, WIN, (kStreamCompute - kStreamDt + NCW) * 64>(
-          a, dx, c, s0 + (int64_t)(nst - 1) * CW, s1, (wave - kStreamDt) * 64 + lane,
-          smem + SC::O_OFF + ((nst - 1) & 1) * G::BUF);
+          a, dx, cl, ml, s1, (wave - kStreamDt) * 64 + lane, smem + SC::O_OFF + ((nst - 1) & 1) * G::BUF);
   } else if constexpr (DX && COPY) {
-    stream_store<Tag, WIN, NC * 64>(a, dx, c, s0 + (int64_t)(nst - 1) * CW, s1, cw * 64 + lane,
-                                    smem + SC::O_OFF + ((nst - 1) & 1) * G::BUF);
+    stream_store<Tag, WIN, NC * 64>(a, dx, cl, ml, s1, cw * 64 + lane, smem + SC::O_OFF + ((nst - 1) & 1) * G::BUF);
+  }
+  if constexpr (RUNS) {
+    // runs: the last channel's table gradient, binned by each table-gradient
+    // wave on its own (no workgroup barrier)
+    if (runs) {
+      run_bin(cl);
+      return;
+    }
   }
   // the table-gradient waves' tiles to the scratch, then the bins summed by
   // all the waves
@@ -2366,8 +2538,9 @@ __device__ __attribute__((always_inline)) void stream_wave(const typename Tag::S
 // HL > 0: the hierarchical form (global window WIN, local window
 // HL = WIN / 2): both table gradients from one pass, and with DX the input
 // gradient of the fused matrix (tables tab and tabl, read back to front).
-// NCW: dedicated copy waves (0 or 4).
-template <class Tag, int WIN, bool DX, int HL = 0, int NCW = 0>
+// NCW: dedicated copy waves (0 or 4).  RUN: runs of stages over all
+// channels (a.run, a.nstc) instead of one (channel, slab) per workgroup.
+template <class Tag, int WIN, bool DX, int HL = 0, int NCW = 0, bool RUN = false>
 __global__ __launch_bounds__(stream_threads<NCW>(), (kStreamCompute + NCW) / 4) void wbmm_bwd_stream_kernel(
     const typename Tag::S *__restrict__ x, const typename Tag::S *__restrict__ dy,
     const typename Tag::S *__restrict__ tab, typename Tag::S *__restrict__ dx, float *__restrict__ dt,
@@ -2379,7 +2552,7 @@ __global__ __launch_bounds__(stream_threads<NCW>(), (kStreamCompute + NCW) / 4) 
                 "both tables' bins within the stage buffers");
   static_assert(NCW == 0 || NCW == 4, "copy waves: none or one per SIMD");
   extern __shared__ __align__(16) unsigned char smem[];
-#define WBMM_SW(D, X) stream_wave<Tag, WIN, D, X, DX, HL, NCW>(x, dy, tab, tabl, dx, dt, part, a, smem, dtl, partl)
+#define WBMM_SW(D, X) stream_wave<Tag, WIN, D, X, DX, HL, NCW, RUN>(x, dy, tab, tabl, dx, dt, part, a, smem, dtl, partl)
   switch (threadIdx.x >> 6) {
     case 0: WBMM_SW(0, -1); break;
     case 1: WBMM_SW(1, -1); break;
@@ -2430,6 +2603,7 @@ static KArgs make_args(const Geom &g) {
   a.inv_nhw = 1.0f / (float)(g.NH * g.NW);
   a.tiled = 0;
   a.lgnw = 0; a.lgw = 0; a.BE = 0; a.WPI = 1; a.chw = 0;
+  a.run = 0; a.nstc = 0;
   return a;
 }
 
@@ -2609,16 +2783,56 @@ static DtPlan plan_dt(const Geom &g) {
 // below).  Its slabs never outnumber those of plan_dt, which sizes the
 // workspace.
 template <class Tag, int WIN>
-static bool stream_plan(const Geom &g, KArgs &b, bool rounds = false) {
+static bool stream_runs(const Geom &g, KArgs &b, int ncu) {
+  typedef BwdCfg<Tag, WIN> G;
+  if constexpr (!StreamCfg<Tag, WIN>::RUNS) {
+    (void)g; (void)b; (void)ncu;
+    return false;
+  } else {
+    const int64_t nstc = cdiv64(g.N, G::CW), tot = g.C * nstc;
+    if (tot >= ((int64_t)1 << 31)) return false;
+    const int64_t L = cdiv64(tot, ncu);
+    // every channel within at most two runs, every run over at most two
+    // channels
+    for (int64_t c = 0; c < g.C; ++c)
+      if ((c * nstc + nstc - 1) / L - (c * nstc) / L > 1) return false;
+    for (int64_t r = 0; r * L < tot; ++r) {
+      const int64_t e = ((r + 1) * L < tot ? (r + 1) * L : tot) - 1;
+      if (e / nstc - (r * L) / nstc > 1) return false;
+    }
+    b.run = (int)L;
+    b.nstc = (int)nstc;
+    b.tile = 0;
+    b.tiles_per_ch = 0;
+    return true;
+  }
+}
+
+// Workgroups of a channel-stream launch planned by stream_plan, and the
+// partial tables per channel the sum kernel adds (1: none).
+static int64_t stream_grid(const Geom &g, const KArgs &b) {
+  return b.run > 0 ? cdiv64(g.C * (int64_t)b.nstc, b.run) : g.C * b.tiles_per_ch;
+}
+static int64_t stream_parts(const KArgs &b) { return b.run > 0 ? 2 : b.tiles_per_ch; }
+
+template <class Tag, int WIN>
+static bool stream_plan(const Geom &g, KArgs &b, bool rounds = false, int64_t ws_slabs = 0) {
   typedef BwdCfg<Tag, WIN> G;
   const int ncu = compute_units();
+  b.run = 0;
+  b.nstc = 0;
   if (!b.tiled || ncu <= 0) return false;
   if (g.C > ncu) {
-    // more channels than compute units: whole channels in rounds of one
-    // workgroup per compute unit, taken (where the caller allows rounds)
-    // when the last round fills at least half the chip
+    // more channels than compute units (where the caller allows it): whole
+    // channels in rounds of one workgroup per compute unit when the last
+    // round fills at least half the chip; else runs of consecutive stages
+    // over all channels, one per compute unit, when they apply and the
+    // workspace holds two partial tables per channel (measured: runs and
+    // their sum launch lose to a half-full last round, and beat the
+    // four-wave kernels)
+    if (!rounds) return false;
     const int64_t rem = g.C % ncu;
-    if (!rounds || (rem != 0 && rem < ncu / 2)) return false;
+    if (rem != 0 && rem < ncu / 2) return ws_slabs >= 2 && stream_runs<Tag, WIN>(g, b, ncu);
   }
   const int64_t stages = cdiv64(g.N, G::CW);
   int64_t slabs = ncu / g.C;
@@ -2652,15 +2866,25 @@ static hipError_t run_dtable(const void *x, const void *dy, float *dt, void *ws,
   set_tiled<WIN, Tag::ES>(g, a, {x, dy});
   if constexpr (Tag::ES == 4 || WIN % 2 == 0) {
     KArgs b = a;
-    if (stream_plan<Tag, WIN>(g, b, true)) {
+    if (stream_plan<Tag, WIN>(g, b, true, p.slabs)) {
       // the same stages, bins and sums as the fused pass
-      float *spart = b.tiles_per_ch > 1 ? (float *)ws : nullptr;
+      float *spart = stream_parts(b) > 1 ? (float *)ws : nullptr;
       constexpr size_t slds = stream_lds_bytes<Tag, WIN>();
       // (no input-gradient products: the eight idle waves copy as well)
-      wbmm_bwd_stream_kernel<Tag, WIN, false, 0, 0><<<dim3((unsigned)(g.C * b.tiles_per_ch)),
-                                                      dim3(stream_threads<0>()), slds, st>>>(
-          (const S *)x, (const S *)dy, nullptr, nullptr, dt, spart, b, nullptr, nullptr, nullptr);
-      return sum_slabs(spart, dt, g.C * table_len<WIN>(), nullptr, nullptr, 0, b.tiles_per_ch, st);
+      bool launched = false;
+      if constexpr (StreamCfg<Tag, WIN>::RUNS) {
+        if (b.run > 0) {
+          wbmm_bwd_stream_kernel<Tag, WIN, false, 0, 0, true><<<dim3((unsigned)stream_grid(g, b)),
+                                                                 dim3(stream_threads<0>()), slds, st>>>(
+              (const S *)x, (const S *)dy, nullptr, nullptr, dt, spart, b, nullptr, nullptr, nullptr);
+          launched = true;
+        }
+      }
+      if (!launched)
+        wbmm_bwd_stream_kernel<Tag, WIN, false, 0, 0><<<dim3((unsigned)stream_grid(g, b)),
+                                                        dim3(stream_threads<0>()), slds, st>>>(
+            (const S *)x, (const S *)dy, nullptr, nullptr, dt, spart, b, nullptr, nullptr, nullptr);
+      return sum_slabs(spart, dt, g.C * table_len<WIN>(), nullptr, nullptr, 0, stream_parts(b), st);
     }
   }
   float *part = p.slabs > 1 ? (float *)ws : nullptr;
@@ -2688,14 +2912,24 @@ static hipError_t run_backward(const void *x, const void *dy, const void *t, voi
   set_tiled<WIN, Tag::ES>(g, a, {x, dy, dx});
   if constexpr (Tag::ES == 4 || WIN % 2 == 0) {
     KArgs b = a;
-    if (stream_plan<Tag, WIN>(g, b, true)) {
-      float *spart = b.tiles_per_ch > 1 ? (float *)ws : nullptr;
+    if (stream_plan<Tag, WIN>(g, b, true, p.slabs)) {
+      float *spart = stream_parts(b) > 1 ? (float *)ws : nullptr;
       constexpr size_t slds = stream_lds_bytes<Tag, WIN>();
       static_assert(slds <= 160 * 1024, "workgroup LDS above the 160 KB of a compute unit");
-      wbmm_bwd_stream_kernel<Tag, WIN, true, 0, kCopyWaves><<<dim3((unsigned)(g.C * b.tiles_per_ch)),
-                                                               dim3(stream_threads<kCopyWaves>()), slds, st>>>(
-          (const S *)x, (const S *)dy, (const S *)t, (S *)dx, dt, spart, b, nullptr, nullptr, nullptr);
-      return sum_slabs(spart, dt, g.C * table_len<WIN>(), nullptr, nullptr, 0, b.tiles_per_ch, st);
+      bool launched = false;
+      if constexpr (StreamCfg<Tag, WIN>::RUNS) {
+        if (b.run > 0) {
+          wbmm_bwd_stream_kernel<Tag, WIN, true, 0, kCopyWaves, true><<<dim3((unsigned)stream_grid(g, b)),
+                                                                         dim3(stream_threads<kCopyWaves>()), slds, st>>>(
+              (const S *)x, (const S *)dy, (const S *)t, (S *)dx, dt, spart, b, nullptr, nullptr, nullptr);
+          launched = true;
+        }
+      }
+      if (!launched)
+        wbmm_bwd_stream_kernel<Tag, WIN, true, 0, kCopyWaves><<<dim3((unsigned)stream_grid(g, b)),
+                                                                dim3(stream_threads<kCopyWaves>()), slds, st>>>(
+            (const S *)x, (const S *)dy, (const S *)t, (S *)dx, dt, spart, b, nullptr, nullptr, nullptr);
+      return sum_slabs(spart, dt, g.C * table_len<WIN>(), nullptr, nullptr, 0, stream_parts(b), st);
     }
   }
   float *part = p.slabs > 1 ? (float *)ws : nullptr;

@@ -383,6 +383,44 @@ def test_channel_stream_in_rounds(shape, dtype):
     check_fused(d, w, dtype, "rounds %s %s" % (dtype, shape))
 
 
+# more channels than compute units with at least two stages per channel
+# (16-bit): runs of consecutive stages over all channels, one workgroup per
+# compute unit; a channel is split between two runs (two partial tables, added
+# by the sum kernel) or lies whole in one (its second partial zero).  Float32
+# takes the other paths and is checked the same way.
+RUNS = [
+    (64, 300, 14, 14, 14),  # 2 stages per channel, runs of 3
+    (32, 288, 28, 28, 14),  # 4 stages per channel, runs of 5
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("shape", RUNS, ids=lambda s: "B%dC%dH%dW%dw%d" % s)
+def test_channel_stream_runs(shape, dtype):
+    B, C, H, Wd, w = shape
+    assert C > compute_units()
+    d = draw(B, C, H, Wd, w, dtype, seed=67)
+    check_fused(d, w, dtype, "runs %s %s" % (dtype, shape))
+
+
+@pytest.mark.parametrize("shape", RUNS, ids=lambda s: "B%dC%dH%dW%dw%d" % s)
+def test_channel_stream_runs_workspace_contents_do_not_matter(shape):
+    """The runs' partial tables (both slots of every channel, the zero second
+    slot of a channel whole in one run) are written before they are read: a
+    workspace holding NaN on entry gives the result of a fresh one."""
+    B, C, H, Wd, w = shape
+    d = draw(B, C, H, Wd, w, "bf16", seed=69)
+    x, dy, t = (to_device(d[k], "bf16") for k in ("x", "dy", "t"))
+    need = W.wbmm_backward_table_workspace_bytes(x.shape, w, x.dtype)
+    assert need >= 2 * C * (2 * w - 1) ** 2 * 4
+    ref = W.wbmm_backward_table(x, dy, w, workspace=W.new_workspace(need))
+    ws = garbage_workspace(need)
+    got = W.wbmm_backward_table(x, dy, w, workspace=ws)
+    _, got2 = W.wbmm_backward(x, dy, t, w, workspace=garbage_workspace(need))
+    torch.cuda.synchronize()
+    assert torch.equal(got, ref) and torch.equal(got2, ref)
+
+
 def check_integer_exact(shape, dtype, seed):
     """Integers in {-1, 0, 1}: every sum is exact, so the forward and both
     gradients (separate and fused) equal the oracle bit for bit."""
@@ -407,6 +445,13 @@ def check_integer_exact(shape, dtype, seed):
 def test_more_channels_integer_data_bit_exact(shape, dtype):
     assert shape[1] > compute_units()
     check_integer_exact(shape, dtype, 71 + shape[4])
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("shape", RUNS, ids=lambda s: "B%dC%dH%dW%dw%d" % s)
+def test_channel_stream_runs_integer_bit_exact(shape, dtype):
+    assert shape[1] > compute_units()
+    check_integer_exact(shape, dtype, 101 + shape[1])
 
 
 # few stages per channel and fewer channels than compute units: the fused
