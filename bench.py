@@ -59,23 +59,23 @@ def parse():
 # otherwise reported as null.
 TRAFFIC = {
     # (workload, kernel): measured bytes per dispatch (profiles/wbmm_traffic_*.txt)
-    ("bf16_b128_c384_14_w14", "bwd"): {"source": "1be8e102d29168c4", "bytes": 60219350},
-    ("bf16_b128_c384_14_w14", "dt"): {"source": "1be8e102d29168c4", "bytes": 40328968},
-    ("bf16_b128_c384_14_w14", "dx"): {"source": "1be8e102d29168c4", "bytes": 39192848},
-    ("bf16_b128_c384_14_w14", "fwd"): {"source": "1be8e102d29168c4", "bytes": 39195994},
-    ("bf16_b16_c64_112_hier7", "hbwd"): {"source": "1be8e102d29168c4", "bytes": 79897040},
-    ("bf16_b16_c64_112_hier7", "hfwd"): {"source": "1be8e102d29168c4", "bytes": 51802775},
-    ("bf16_b16_c64_112_w14", "bwd"): {"source": "1be8e102d29168c4", "bytes": 78631243},
-    ("bf16_b16_c64_112_w14", "dt"): {"source": "1be8e102d29168c4", "bytes": 52785286},
-    ("bf16_b16_c64_112_w14", "dx"): {"source": "1be8e102d29168c4", "bytes": 51636015},
-    ("bf16_b16_c64_112_w14", "fwd"): {"source": "1be8e102d29168c4", "bytes": 51651800},
-    ("bf16_b64_c192_28_hier7", "hbwd"): {"source": "1be8e102d29168c4", "bytes": 60637506},
-    ("bf16_b64_c192_28_hier7", "hfwd"): {"source": "1be8e102d29168c4", "bytes": 39923792},
-    ("bf16_b64_c192_28_w14", "bwd"): {"source": "1be8e102d29168c4", "bytes": 59375018},
-    ("bf16_b64_c192_28_w14", "dt"): {"source": "1be8e102d29168c4", "bytes": 39769544},
-    ("bf16_b64_c192_28_w14", "dx"): {"source": "1be8e102d29168c4", "bytes": 39766973},
-    ("bf16_b64_c192_28_w14", "fwd"): {"source": "1be8e102d29168c4", "bytes": 39281190},
-    ("bf16_b64_c96_56_w7", "fwd"): {"source": "1be8e102d29168c4", "bytes": 77261929},
+    ("bf16_b128_c384_14_w14", "bwd"): {"source": "008de5238d69b51a", "bytes": 60210046},
+    ("bf16_b128_c384_14_w14", "dt"): {"source": "008de5238d69b51a", "bytes": 40329096},
+    ("bf16_b128_c384_14_w14", "dx"): {"source": "008de5238d69b51a", "bytes": 39197578},
+    ("bf16_b128_c384_14_w14", "fwd"): {"source": "008de5238d69b51a", "bytes": 39183660},
+    ("bf16_b16_c64_112_hier7", "hbwd"): {"source": "008de5238d69b51a", "bytes": 79820781},
+    ("bf16_b16_c64_112_hier7", "hfwd"): {"source": "008de5238d69b51a", "bytes": 51799776},
+    ("bf16_b16_c64_112_w14", "bwd"): {"source": "008de5238d69b51a", "bytes": 78621812},
+    ("bf16_b16_c64_112_w14", "dt"): {"source": "008de5238d69b51a", "bytes": 52785669},
+    ("bf16_b16_c64_112_w14", "dx"): {"source": "008de5238d69b51a", "bytes": 51631855},
+    ("bf16_b16_c64_112_w14", "fwd"): {"source": "008de5238d69b51a", "bytes": 51689632},
+    ("bf16_b64_c192_28_hier7", "hbwd"): {"source": "008de5238d69b51a", "bytes": 60564251},
+    ("bf16_b64_c192_28_hier7", "hfwd"): {"source": "008de5238d69b51a", "bytes": 40012794},
+    ("bf16_b64_c192_28_w14", "bwd"): {"source": "008de5238d69b51a", "bytes": 59367987},
+    ("bf16_b64_c192_28_w14", "dt"): {"source": "008de5238d69b51a", "bytes": 39769416},
+    ("bf16_b64_c192_28_w14", "dx"): {"source": "008de5238d69b51a", "bytes": 39711325},
+    ("bf16_b64_c192_28_w14", "fwd"): {"source": "008de5238d69b51a", "bytes": 39687102},
+    ("bf16_b64_c96_56_w7", "fwd"): {"source": "008de5238d69b51a", "bytes": 77263157},
 }
 
 
