@@ -8,7 +8,9 @@
 * the five workloads at full size, in the launch configuration the benchmark
   uses, against the oracle on every channel;
 * more channels than the device has compute units (the four-wave gradient
-  kernels), in every dtype, with an exact small-integer variant;
+  kernels, the channel stream in rounds and in runs of stages), in every
+  dtype, with an exact small-integer variant;
+* a seeded sweep of random shapes over every pass and the fused backward;
 * determinism, non-default streams, the autograd composition, error paths.
 """
 import numpy as np
@@ -824,3 +826,40 @@ def test_dense_bin_matrix_exact():
         got = W.wbmm_bin_matrix(torch.from_numpy(dm64.astype(np.float32)).cuda(), wh, ww)
         torch.cuda.synchronize()
         assert np.array_equal(to_f64(got), oracle.bin_matrix(dm64, (wh, ww)))
+
+
+# -------------------------------------------------------------- seeded sweep
+
+def sweep_shapes(n, seed, ncu=256):
+    """Seeded random shapes: windows 2..16 on ragged maps and on maps the
+    windows tile (bands of one image or whole images per 16-window
+    sub-tile), channel counts on either side of the compute-unit count (the
+    launch plans that split channels into slabs, stream them, take rounds or
+    runs of stages, or fall back to the four-wave kernels)."""
+    r = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        w = int(r.integers(2, 17))
+        if r.random() < 0.6:
+            H, Wd = int(r.integers(1, 5)) * w, int(r.choice([1, 2, 4])) * w
+        else:
+            H, Wd = int(r.integers(1, 3 * w + 1)), int(r.integers(1, 3 * w + 1))
+        C = int(r.choice([1, 2, 5, 33, ncu - 3, ncu + 5, ncu + ncu // 2 + 7]))
+        B = int(r.integers(1, 9 if C < 64 else 3))
+        out.append((B, C, H, Wd, w))
+    return out
+
+
+SWEEP = sweep_shapes(24, 2026)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("shape", SWEEP, ids=lambda s: "B%dC%dH%dW%dw%d" % s)
+def test_seeded_shape_sweep(shape, dtype):
+    """Every pass against the oracle, and the fused backward equal to the
+    separate entry points bit for bit, on the seeded random shapes."""
+    B, C, H, Wd, w = shape
+    d = draw(B, C, H, Wd, w, dtype, seed=B * 7919 + C * 31 + H * 7 + Wd + w)
+    label = "sweep %s %s" % (dtype, shape)
+    check(run_gpu(d, w, dtype), run_oracle(d, w), dtype, label)
+    check_fused(d, w, dtype, label)
