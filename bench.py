@@ -58,24 +58,23 @@ def parse():
 # on (sha256 of the kernel header's code without comments and blank lines);
 # otherwise reported as null.
 TRAFFIC = {
-    # (workload, kernel): measured bytes per dispatch (profiles/wbmm_traffic_*.txt)
-    ("bf16_b128_c384_14_w14", "bwd"): {"source": "008de5238d69b51a", "bytes": 60210046},
-    ("bf16_b128_c384_14_w14", "dt"): {"source": "008de5238d69b51a", "bytes": 40329096},
-    ("bf16_b128_c384_14_w14", "dx"): {"source": "008de5238d69b51a", "bytes": 39197578},
-    ("bf16_b128_c384_14_w14", "fwd"): {"source": "008de5238d69b51a", "bytes": 39183660},
-    ("bf16_b16_c64_112_hier7", "hbwd"): {"source": "008de5238d69b51a", "bytes": 79820781},
-    ("bf16_b16_c64_112_hier7", "hfwd"): {"source": "008de5238d69b51a", "bytes": 51799776},
-    ("bf16_b16_c64_112_w14", "bwd"): {"source": "008de5238d69b51a", "bytes": 78621812},
-    ("bf16_b16_c64_112_w14", "dt"): {"source": "008de5238d69b51a", "bytes": 52785669},
-    ("bf16_b16_c64_112_w14", "dx"): {"source": "008de5238d69b51a", "bytes": 51631855},
-    ("bf16_b16_c64_112_w14", "fwd"): {"source": "008de5238d69b51a", "bytes": 51689632},
-    ("bf16_b64_c192_28_hier7", "hbwd"): {"source": "008de5238d69b51a", "bytes": 60564251},
-    ("bf16_b64_c192_28_hier7", "hfwd"): {"source": "008de5238d69b51a", "bytes": 40012794},
-    ("bf16_b64_c192_28_w14", "bwd"): {"source": "008de5238d69b51a", "bytes": 59367987},
-    ("bf16_b64_c192_28_w14", "dt"): {"source": "008de5238d69b51a", "bytes": 39769416},
-    ("bf16_b64_c192_28_w14", "dx"): {"source": "008de5238d69b51a", "bytes": 39711325},
-    ("bf16_b64_c192_28_w14", "fwd"): {"source": "008de5238d69b51a", "bytes": 39687102},
-    ("bf16_b64_c96_56_w7", "fwd"): {"source": "008de5238d69b51a", "bytes": 77263157},
+    ("bf16_b128_c384_14_w14", "bwd"): {"source": "974983de90ecae57", "bytes": 60208417},
+    ("bf16_b128_c384_14_w14", "dt"): {"source": "974983de90ecae57", "bytes": 40346355},
+    ("bf16_b128_c384_14_w14", "dx"): {"source": "974983de90ecae57", "bytes": 39191811},
+    ("bf16_b128_c384_14_w14", "fwd"): {"source": "974983de90ecae57", "bytes": 39198169},
+    ("bf16_b16_c64_112_hier7", "hbwd"): {"source": "974983de90ecae57", "bytes": 79899149},
+    ("bf16_b16_c64_112_hier7", "hfwd"): {"source": "974983de90ecae57", "bytes": 51766076},
+    ("bf16_b16_c64_112_w14", "bwd"): {"source": "974983de90ecae57", "bytes": 78620214},
+    ("bf16_b16_c64_112_w14", "dt"): {"source": "974983de90ecae57", "bytes": 52803184},
+    ("bf16_b16_c64_112_w14", "dx"): {"source": "974983de90ecae57", "bytes": 51593706},
+    ("bf16_b16_c64_112_w14", "fwd"): {"source": "974983de90ecae57", "bytes": 51629613},
+    ("bf16_b64_c192_28_hier7", "hbwd"): {"source": "974983de90ecae57", "bytes": 60639168},
+    ("bf16_b64_c192_28_hier7", "hfwd"): {"source": "974983de90ecae57", "bytes": 39743350},
+    ("bf16_b64_c192_28_w14", "bwd"): {"source": "974983de90ecae57", "bytes": 59365686},
+    ("bf16_b64_c192_28_w14", "dt"): {"source": "974983de90ecae57", "bytes": 39786802},
+    ("bf16_b64_c192_28_w14", "dx"): {"source": "974983de90ecae57", "bytes": 39446711},
+    ("bf16_b64_c192_28_w14", "fwd"): {"source": "974983de90ecae57", "bytes": 39240683},
+    ("bf16_b64_c96_56_w7", "fwd"): {"source": "974983de90ecae57", "bytes": 77251096},
 }
 
 

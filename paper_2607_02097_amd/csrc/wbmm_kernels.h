@@ -150,6 +150,14 @@ __device__ inline int fdiv(int v, int d, float inv) {
   return q;
 }
 
+// v / d for 0 <= v < 2^22 and d >= 1, from inv = 1 / d rounded to float, with
+// no correction step: (v + 1/2) / d lies at least 1 / (2d) from an integer,
+// and the two roundings move the product by less than (v + 1/2) / d * 2^-23,
+// which is below that distance, so truncating the product gives the quotient.
+__device__ __attribute__((always_inline)) inline int fdiv_small(int v, float inv) {
+  return (int)(((float)v + 0.5f) * inv);
+}
+
 // ------------------------------------------------------------- geometry
 
 struct KArgs {
@@ -881,6 +889,9 @@ struct ImgArgs {
   int SEGC;       // 16-byte chunks per contiguous piece (an image, or the sub-tile)
   float inv_segc; // 1 / SEGC
   int CPR;        // chunks per band in the rows of one output-tile pair
+  float inv_cpr;  // 1 / CPR
+  float inv_nh;   // 1 / NH
+  uint32_t gap;   // bytes from the end of one piece to the start of the next (2 chw - 16 SEGC; 0 unless whole)
   int pair_store; // 1: rows are stored per output-tile pair, else per sub-tile
 };
 
@@ -906,8 +917,8 @@ __host__ __device__ constexpr size_t fwd_img_lds_bytes() {
 // it); 0x7fffffff past the sub-tile's last chunk.  Offsets of the chunks of
 // missing pieces (a partial last sub-tile) are at least nseg * chw * 2.
 __device__ __attribute__((always_inline)) inline uint32_t img_chunk(const ImgArgs &ia, int q, int nch) {
-  const int seg = ia.whole ? fdiv(q, ia.SEGC, ia.inv_segc) : 0;
-  const uint32_t off = (uint32_t)seg * (uint32_t)(2 * ia.chw) + 16u * (uint32_t)(q - seg * ia.SEGC);
+  const int seg = ia.whole ? fdiv_small(q, ia.inv_segc) : 0;  // q < 2^22
+  const uint32_t off = 16u * (uint32_t)q + (uint32_t)seg * ia.gap;
   return q < nch ? off : 0x7fffffffu;
 }
 
@@ -962,9 +973,9 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_img_kernel(const type
   const int nwm = (1 << ia.lgnw) - 1;
   const int abase = (ln >> ia.lgnw) * ia.BE + (ln & nwm) * WIN;  // window ln of the sub-tile in LDS
   // store task of this lane per output-tile pair: band jj, chunk i of its rows
-  const int sjj = lane / ia.CPR;
+  const int sjj = fdiv_small(lane, ia.inv_cpr);
   const int si = lane - sjj * ia.CPR;
-  const int sseg = ia.whole ? sjj / ia.NH : 0;
+  const int sseg = ia.whole ? fdiv_small(sjj, ia.inv_nh) : 0;
   const uint32_t soff = (uint32_t)sseg * (uint32_t)(2 * ia.chw) + 2u * (uint32_t)((sjj - sseg * ia.NH) * ia.BE + 8 * si);
   const int sloff = sjj * ia.BE + 8 * si;
 
@@ -2676,6 +2687,9 @@ static bool img_layout(const Geom &g, const void *x, const void *y, ImgArgs &ia)
   ia.inv_segc = 1.0f / (float)ia.SEGC;
   ia.pair_store = (RPP * g.W) % 8 == 0 && ((WIN % RPP) * g.W) % 8 == 0 && be % 8 == 0;
   ia.CPR = ia.pair_store ? (int)(RPP * g.W / 8) : 1;
+  ia.inv_cpr = 1.0f / (float)ia.CPR;
+  ia.inv_nh = 1.0f / (float)ia.NH;
+  ia.gap = whole ? (uint32_t)(2 * ia.chw - 16 * (int64_t)ia.SEGC) : 0u;
   return true;
 }
 

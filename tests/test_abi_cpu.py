@@ -234,3 +234,23 @@ def test_noalloc_validates_on_the_host(lib):
     assert call(dx=G) == W.WBMM_ERR_INVALID_ARG  # dx aliases x
     assert call(w=17) == W.WBMM_ERR_UNSUPPORTED
     assert "scratch" in W.wbmm_status_string(W.WBMM_ERR_SCRATCH)
+
+
+def test_float_quotient_without_correction():
+    """The image-layout kernels split chunk and lane indices by a divisor d
+    with trunc((v + 1/2) * fl(1/d)) in float32 and no correction step; that
+    is the integer quotient for 0 <= v < 2^22.  Checked exhaustively with
+    IEEE float32 arithmetic (the device's round-to-nearest-even): every d up
+    to 4096 with v below 2^13 (chunk, lane and band indices), and every v
+    below 2^22 for d up to 48."""
+    f = np.float32
+
+    def quotient(v, d):
+        return ((v.astype(np.float32) + f(0.5)) * (f(1.0) / f(d))).astype(np.int64)
+
+    v = np.arange(1 << 13, dtype=np.int64)
+    for d in range(1, 4097):
+        assert np.array_equal(quotient(v, d), v // d), d
+    v = np.arange(1 << 22, dtype=np.int64)
+    for d in range(1, 49):
+        assert np.array_equal(quotient(v, d), v // d), d
