@@ -58,23 +58,23 @@ def parse():
 # on (sha256 of the kernel header's code without comments and blank lines);
 # otherwise reported as null.
 TRAFFIC = {
-    ("bf16_b128_c384_14_w14", "bwd"): {"source": "974983de90ecae57", "bytes": 60208417},
-    ("bf16_b128_c384_14_w14", "dt"): {"source": "974983de90ecae57", "bytes": 40346355},
-    ("bf16_b128_c384_14_w14", "dx"): {"source": "974983de90ecae57", "bytes": 39191811},
-    ("bf16_b128_c384_14_w14", "fwd"): {"source": "974983de90ecae57", "bytes": 39198169},
-    ("bf16_b16_c64_112_hier7", "hbwd"): {"source": "974983de90ecae57", "bytes": 79899149},
-    ("bf16_b16_c64_112_hier7", "hfwd"): {"source": "974983de90ecae57", "bytes": 51766076},
-    ("bf16_b16_c64_112_w14", "bwd"): {"source": "974983de90ecae57", "bytes": 78620214},
-    ("bf16_b16_c64_112_w14", "dt"): {"source": "974983de90ecae57", "bytes": 52803184},
-    ("bf16_b16_c64_112_w14", "dx"): {"source": "974983de90ecae57", "bytes": 51593706},
-    ("bf16_b16_c64_112_w14", "fwd"): {"source": "974983de90ecae57", "bytes": 51629613},
-    ("bf16_b64_c192_28_hier7", "hbwd"): {"source": "974983de90ecae57", "bytes": 60639168},
-    ("bf16_b64_c192_28_hier7", "hfwd"): {"source": "974983de90ecae57", "bytes": 39743350},
-    ("bf16_b64_c192_28_w14", "bwd"): {"source": "974983de90ecae57", "bytes": 59365686},
-    ("bf16_b64_c192_28_w14", "dt"): {"source": "974983de90ecae57", "bytes": 39786802},
-    ("bf16_b64_c192_28_w14", "dx"): {"source": "974983de90ecae57", "bytes": 39446711},
-    ("bf16_b64_c192_28_w14", "fwd"): {"source": "974983de90ecae57", "bytes": 39240683},
-    ("bf16_b64_c96_56_w7", "fwd"): {"source": "974983de90ecae57", "bytes": 77251096},
+    ("bf16_b128_c384_14_w14", "bwd"): {"source": "c5c88ade4f762eae", "bytes": 60216951},
+    ("bf16_b128_c384_14_w14", "dt"): {"source": "c5c88ade4f762eae", "bytes": 40341241},
+    ("bf16_b128_c384_14_w14", "dx"): {"source": "c5c88ade4f762eae", "bytes": 39186822},
+    ("bf16_b128_c384_14_w14", "fwd"): {"source": "c5c88ade4f762eae", "bytes": 39195548},
+    ("bf16_b16_c64_112_hier7", "hbwd"): {"source": "c5c88ade4f762eae", "bytes": 79881986},
+    ("bf16_b16_c64_112_hier7", "hfwd"): {"source": "c5c88ade4f762eae", "bytes": 51712583},
+    ("bf16_b16_c64_112_w14", "bwd"): {"source": "c5c88ade4f762eae", "bytes": 78627980},
+    ("bf16_b16_c64_112_w14", "dt"): {"source": "c5c88ade4f762eae", "bytes": 52797942},
+    ("bf16_b16_c64_112_w14", "dx"): {"source": "c5c88ade4f762eae", "bytes": 51593424},
+    ("bf16_b16_c64_112_w14", "fwd"): {"source": "c5c88ade4f762eae", "bytes": 51586736},
+    ("bf16_b64_c192_28_hier7", "hbwd"): {"source": "c5c88ade4f762eae", "bytes": 60621653},
+    ("bf16_b64_c192_28_hier7", "hfwd"): {"source": "c5c88ade4f762eae", "bytes": 40013008},
+    ("bf16_b64_c192_28_w14", "bwd"): {"source": "c5c88ade4f762eae", "bytes": 59373612},
+    ("bf16_b64_c192_28_w14", "dt"): {"source": "c5c88ade4f762eae", "bytes": 39781561},
+    ("bf16_b64_c192_28_w14", "dx"): {"source": "c5c88ade4f762eae", "bytes": 39369981},
+    ("bf16_b64_c192_28_w14", "fwd"): {"source": "c5c88ade4f762eae", "bytes": 39392765},
+    ("bf16_b64_c96_56_w7", "fwd"): {"source": "c5c88ade4f762eae", "bytes": 77247279},
 }
 
 

@@ -887,7 +887,7 @@ struct ImgArgs {
   int WPI;        // windows per image (NH * NW)
   int whole;      // 1: a sub-tile is 16 / WPI whole images
   int SEGC;       // 16-byte chunks per contiguous piece (an image, or the sub-tile)
-  float inv_segc; // 1 / SEGC
+  float inv_segc; // 1 / SEGC when whole, else 0
   int CPR;        // chunks per band in the rows of one output-tile pair
   float inv_cpr;  // 1 / CPR
   float inv_nh;   // 1 / NH
@@ -914,12 +914,15 @@ __host__ __device__ constexpr size_t fwd_img_lds_bytes() {
 
 // Byte offset of chunk q of a sub-tile from the sub-tile's first element
 // (pieces of a sub-tile lie within 2^31 bytes of each other; the host checks
-// it); 0x7fffffff past the sub-tile's last chunk.  Offsets of the chunks of
-// missing pieces (a partial last sub-tile) are at least nseg * chw * 2.
+// it); 0x7fffffff past the sub-tile's last chunk, unless INSIDE (q < nch
+// known).  Offsets of the chunks of missing pieces (a partial last sub-tile)
+// are at least nseg * chw * 2.  inv_segc is 0 for a one-piece sub-tile, so
+// seg is 0 there.
+template <bool INSIDE>
 __device__ __attribute__((always_inline)) inline uint32_t img_chunk(const ImgArgs &ia, int q, int nch) {
-  const int seg = ia.whole ? fdiv_small(q, ia.inv_segc) : 0;  // q < 2^22
+  const int seg = fdiv_small(q, ia.inv_segc);  // q < 2^22
   const uint32_t off = 16u * (uint32_t)q + (uint32_t)seg * ia.gap;
-  return q < nch ? off : 0x7fffffffu;
+  return (INSIDE || q < nch) ? off : 0x7fffffffu;
 }
 
 // HIER: the hierarchical form (WIN = 2 wl, local table tabl): the local
@@ -966,7 +969,9 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_img_kernel(const type
   auto chunk_off = [&](int k) -> uint32_t {
     int l = lane;
     asm volatile("" : "+v"(l));
-    return img_chunk(ia, l + 64 * k, IC::CH);
+    // (k is a constant of the unrolled loops: chunks of the first CH / 64
+    // rounds lie inside the sub-tile)
+    return 64 * (k + 1) <= IC::CH ? img_chunk<true>(ia, l + 64 * k, IC::CH) : img_chunk<false>(ia, l + 64 * k, IC::CH);
   };
   const int g = lane >> 4;
   const int ln = lane & 15;
@@ -1044,7 +1049,9 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_img_kernel(const type
       const bool rok = r < WIN;
       const int e0 = ab + (rok ? r : 0) * ia.W + x0;
       const uint32_t *p = raw32 + (e0 >> 1);
-      const uint32_t sh = (uint32_t)(e0 & 1) * 16u;
+      // (an even window tiles an even image width, so its rows start at
+      // even elements: no shift)
+      const uint32_t sh = (WIN & 1) ? (uint32_t)(e0 & 1) * 16u : 0u;
       uint32_t d[5];
 #pragma unroll
       for (int i = 0; i < 5; ++i) d[i] = p[i];
@@ -1071,6 +1078,20 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_img_kernel(const type
     // local fragments leave no registers for a second accumulator chain);
     // each tile takes the same products in the same order either way
     constexpr int TS = HIER ? 1 : 2;
+    // 16-position rows and an even window: output tile t is window row t,
+    // so each of the lane's two result dwords moves down one image row per
+    // tile (byte offsets in raw, advanced per tile); one whose columns lie
+    // past the window stays on the dummy element
+    constexpr bool STEP = RP == 16 && (WIN & 1) == 0;
+    uint32_t pa = 0, pb = 0, sa = 0, sb = 0;
+    if constexpr (STEP) {
+      const int xo0 = 4 * g;
+      const bool va = xo0 < WIN, vb = xo0 + 2 < WIN;
+      pa = 2u * (uint32_t)(va ? ab + xo0 : IC::DUMMY);
+      pb = 2u * (uint32_t)(vb ? ab + xo0 + 2 : IC::DUMMY);
+      sa = va ? 2u * (uint32_t)ia.W : 0u;
+      sb = vb ? 2u * (uint32_t)ia.W : 0u;
+    }
     Frag bf[NB];
 #pragma unroll
     for (int t0 = 0; t0 < NT; t0 += TS) {
@@ -1103,7 +1124,24 @@ __global__ __launch_bounds__(kFwdThreads, 3) void wbmm_fwd_img_kernel(const type
         const int ho = RP == 8 ? 2 * t + (g >> 1) : t;
         const int xo0 = RP == 8 ? 4 * (g & 1) : 4 * g;
         const int o = ab + (ho < WIN ? ho : 0) * ia.W + xo0;
-        if constexpr ((WIN & 1) == 0) {
+        if constexpr (STEP) {
+          uint32_t *wa = reinterpret_cast<uint32_t *>(reinterpret_cast<unsigned char *>(raw) + pa);
+          uint32_t *wb = reinterpret_cast<uint32_t *>(reinterpret_cast<unsigned char *>(raw) + pb);
+          f32x4 r = acc;
+          if constexpr (HIER) {
+            // the two identity shortcuts: + 2 x at the output's own
+            // position, read before the result overwrites it
+            const uint32_t xa = *wa, xb = *wb;
+            r[0] += 2.f * to_f32<Tag>((u16)(xa & 0xffffu));
+            r[1] += 2.f * to_f32<Tag>((u16)(xa >> 16));
+            r[2] += 2.f * to_f32<Tag>((u16)(xb & 0xffffu));
+            r[3] += 2.f * to_f32<Tag>((u16)(xb >> 16));
+          }
+          *wa = pack2<Tag>(r[0], r[1]);
+          *wb = pack2<Tag>(r[2], r[3]);
+          pa += sa;
+          pb += sb;
+        } else if constexpr ((WIN & 1) == 0) {
           // even windows: every window row starts at an even element
           uint32_t *o32 = reinterpret_cast<uint32_t *>(raw);
           const int da = (ho < WIN && xo0 < WIN) ? o : IC::DUMMY;
@@ -2684,7 +2722,7 @@ static bool img_layout(const Geom &g, const void *x, const void *y, ImgArgs &ia)
   ia.WPI = (int)wpi;
   ia.whole = whole ? 1 : 0;
   ia.SEGC = whole ? (int)(hw / 8) : ImgCfg<WIN>::CH;
-  ia.inv_segc = 1.0f / (float)ia.SEGC;
+  ia.inv_segc = whole ? 1.0f / (float)ia.SEGC : 0.0f;  // one piece: chunk q is at 16 q
   ia.pair_store = (RPP * g.W) % 8 == 0 && ((WIN % RPP) * g.W) % 8 == 0 && be % 8 == 0;
   ia.CPR = ia.pair_store ? (int)(RPP * g.W / 8) : 1;
   ia.inv_cpr = 1.0f / (float)ia.CPR;
